@@ -1,0 +1,248 @@
+"""Benchmark of the im2win hot path on one MI355X.
+
+One step = the whole path on one batch of synthetic input, in both
+precisions the path has:
+    fp32: im2win transform -> fp32 windowed conv (vector ALUs)
+    fp16: im2win transform -> filter pack + fp16 windowed conv (MFMA, fp32 acc)
+Default workload: N=128, C_i=64, H=W=56, C_o=64, 3x3, stride 1, uniform[-1,1]
+values (seed 1), inputs resident in HBM before timing starts.
+
+value = conv FLOPs of the step (2 * 2*N*H_o*W_o*C_o*K_h*K_w*C_i) / step time.
+Per-kernel durations come from HIP events recorded on the stream the kernels
+are launched on, around every call in the timed region.
+
+Prints ONE JSON line.  `--layer NAME` picks another configured layer and
+`--sweep` prints one line per configured layer instead (for reports).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# MI355X published peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_FP32_VECTOR_TF = 157.3     # counts packed fp32 FMA
+PEAK_FP32_UNPACKED_TF = 78.6    # 256 CU x 64 lanes x 2 flop x 2.4 GHz, plain v_fma_f32
+PEAK_FP16_MFMA_TF = 2516.6      # dense
+
+
+def layer_numbers(l, pkg):
+    Ho, Wo = pkg.conv_output_dims(l.H, l.W, l.K_h, l.K_w, l.stride)
+    P = l.N * Ho * Wo
+    K = l.K_h * l.K_w * l.C_i
+    flops = 2.0 * P * l.C_o * K
+    d = {"Ho": Ho, "Wo": Wo, "P": P, "K": K, "flops": flops}
+    for dt, elt in (("f32", 4), ("f16", 2)):
+        win = l.N * Ho * l.W * l.K_h * l.C_i * elt
+        d[dt] = {
+            "window_bytes": win,
+            "workspace_bytes": pkg.conv_workspace_bytes(l.N, l.C_i, l.H, l.W, l.C_o, l.K_h, l.K_w,
+                                                        l.stride, dt),
+            "im2col_bytes": pkg.conv_im2col_bytes(l.N, l.C_i, l.H, l.W, l.K_h, l.K_w, l.stride, dt),
+            "input_bytes": l.N * l.H * l.W * l.C_i * elt,
+            "filter_bytes": K * l.C_o * elt,
+            "output_bytes": P * l.C_o * elt,
+            # algorithmic traffic: read every window-tensor element, the filter
+            # and write every output once
+            "conv_bytes": win + K * l.C_o * elt + P * l.C_o * elt,
+            # transform: read the input rows the windows use, write the window tensor
+            "transform_bytes": l.N * ((Ho - 1) * l.stride + l.K_h) * l.W * l.C_i * elt + win,
+        }
+    return d
+
+
+class Path:
+    """Device buffers of one layer in one precision; `step()` runs transform + conv."""
+
+    def __init__(self, l, x, w, dtype, pkg, torch):
+        self.pkg, self.torch = pkg, torch
+        self.l = l
+        dev = torch.device("cuda")
+        self.x = x.to(dtype).contiguous().to(dev)
+        self.w = w.to(dtype).contiguous().to(dev)
+        Ho, Wo = pkg.conv_output_dims(l.H, l.W, l.K_h, l.K_w, l.stride)
+        need = pkg.conv_workspace_bytes(l.N, l.C_i, l.H, l.W, l.C_o, l.K_h, l.K_w, l.stride, dtype)
+        self.ws = torch.empty(need, dtype=torch.uint8, device=dev)
+        self.out = torch.empty((l.N, Ho, Wo, l.C_o), dtype=dtype, device=dev)
+        self.conv = pkg.conv_im2win_fp32 if dtype == torch.float32 else pkg.conv_im2win_fp16
+
+    def transform(self):
+        l = self.l
+        self.pkg.conv_im2win_transform(self.x, self.ws, l.C_o, l.K_h, l.K_w, l.stride)
+
+    def run_conv(self):
+        l = self.l
+        self.conv(self.ws, self.w, self.out, l.N, l.C_i, l.H, l.W, l.stride)
+
+
+def cpu_baseline(l, x, w, budget_s=10.0):
+    """The fp64 oracle on the host cores over whole images of the same layer,
+    chunk by chunk, until `budget_s` has elapsed or the batch is done."""
+    import oracle
+    oracle.build()
+    xs = x.double().numpy()
+    wd = w.double().numpy()
+    Ho = (l.H - l.K_h) // l.stride + 1
+    Wo = (l.W - l.K_w) // l.stride + 1
+    per_img = 2.0 * Ho * Wo * l.C_o * l.K_h * l.K_w * l.C_i
+    done, t0 = 0, time.perf_counter()
+    chunk = 4
+    while done < l.N and time.perf_counter() - t0 < budget_s:
+        n = min(chunk, l.N - done)
+        oracle.conv(xs[done:done + n], wd, l.stride)
+        done += n
+    dt = time.perf_counter() - t0
+    return {"value": per_img * done / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": "%d of %d images of the same layer, fp64 direct convolution, %.1f s"
+                      % (done, l.N, dt)}
+
+
+def measure(l, steps, warmup, pkg, torch, workloads):
+    x, w = workloads.draw_layer(l)
+    paths = {"f32": Path(l, x, w, torch.float32, pkg, torch),
+             "f16": Path(l, x, w, torch.float16, pkg, torch)}
+    nums = layer_numbers(l, pkg)
+
+    def step(ev=None):
+        for k, name in enumerate(("f32", "f16")):
+            p = paths[name]
+            if ev is not None:
+                ev[3 * k].record()
+            p.transform()
+            if ev is not None:
+                ev[3 * k + 1].record()
+            p.run_conv()
+            if ev is not None:
+                ev[3 * k + 2].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    def avg(a, b):
+        v = sorted(evs[i][a].elapsed_time(evs[i][b]) for i in range(steps))
+        return sum(v) / len(v), v[0], v[len(v) // 2]
+
+    k = {}
+    for j, name in enumerate(("f32", "f16")):
+        k[name + "_transform_ms"] = avg(3 * j, 3 * j + 1)
+        k[name + "_conv_ms"] = avg(3 * j + 1, 3 * j + 2)
+    return nums, k, elapsed, x, w, paths
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--layer", default=None, help="configured layer name (default: cfg2)")
+    ap.add_argument("--sweep", action="store_true", help="one line per configured layer")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the im2win path runs on a single MI355X here "
+              "(batch sharding across GPUs is described, not built); use --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_20725_amd as pkg
+    from paper_2608_20725_amd import workloads
+
+    if not os.path.exists(pkg.library_path()):
+        from paper_2608_20725_amd import build
+        build.build()
+    pkg.load_library()
+
+    layers = list(workloads.ALL) if args.sweep else [
+        workloads.BY_NAME[args.layer] if args.layer else workloads.CFG2]
+    for l in layers:
+        torch.cuda.reset_peak_memory_stats()
+        nums, k, elapsed, x, w, paths = measure(l, args.steps, args.warmup, pkg, torch, workloads)
+        peak_alloc = torch.cuda.max_memory_allocated()
+        ms = elapsed / args.steps * 1e3
+        flops = nums["flops"]
+        value = 2 * flops / (ms * 1e-3) / 1e12
+        c32 = k["f32_conv_ms"][0]
+        c16 = k["f16_conv_ms"][0]
+        t32 = k["f32_transform_ms"][0]
+        t16 = k["f16_transform_ms"][0]
+        tf32 = flops / (c32 * 1e-3) / 1e12
+        tf16 = flops / (c16 * 1e-3) / 1e12
+        f32, f16 = nums["f32"], nums["f16"]
+        rec = {
+            "metric": "conv TFLOPS (fp32 VALU, fp16 MFMA) + peak workspace bytes vs im2col",
+            "value": round(value, 3),
+            "unit": "TFLOP/s",
+            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": round(ms, 4),
+            "higher_is_better": True,
+            "scaling": "weak",
+            "vs_baseline": None,
+            "dtype": "f32+f16(f32acc)",
+            "data": "synthetic",
+            "config": {"workload": "%s: N=%d C_i=%d H=W=%d C_o=%d %dx%d stride %d, %s values, "
+                                   "fp32 and fp16 paths" % (l.name, l.N, l.C_i, l.H, l.C_o, l.K_h,
+                                                            l.K_w, l.stride, l.dist),
+                       "global_batch": l.N, "parallelism": "single GPU"},
+            "roofline": {
+                "kernel": "conv_fp32_kernel (fp32 windowed conv, VALU)",
+                "bound": "alu",
+                "achieved": round(tf32, 3),
+                "peak": PEAK_FP32_VECTOR_TF,
+                "unit": "TFLOP/s",
+                "frac": round(tf32 / PEAK_FP32_VECTOR_TF, 4),
+                "frac_of_unpacked_fma_peak": round(tf32 / PEAK_FP32_UNPACKED_TF, 4),
+                "traffic": None,
+            },
+            "kernels": {
+                "f32_transform": {"ms": round(t32, 5), "GB/s": round(f32["transform_bytes"] / t32 / 1e6, 1),
+                                  "frac_hbm": round(f32["transform_bytes"] / t32 / 1e6 / PEAK_HBM_GBS, 4)},
+                "f32_conv": {"ms": round(c32, 5), "TFLOP/s": round(tf32, 3),
+                             "frac_fp32_vector": round(tf32 / PEAK_FP32_VECTOR_TF, 4),
+                             "GB/s": round(f32["conv_bytes"] / c32 / 1e6, 1)},
+                "f16_transform": {"ms": round(t16, 5), "GB/s": round(f16["transform_bytes"] / t16 / 1e6, 1),
+                                  "frac_hbm": round(f16["transform_bytes"] / t16 / 1e6 / PEAK_HBM_GBS, 4)},
+                "f16_pack_conv": {"ms": round(c16, 5), "TFLOP/s": round(tf16, 3),
+                                  "frac_fp16_mfma": round(tf16 / PEAK_FP16_MFMA_TF, 4),
+                                  "GB/s": round(f16["conv_bytes"] / c16 / 1e6, 1),
+                                  "frac_hbm": round(f16["conv_bytes"] / c16 / 1e6 / PEAK_HBM_GBS, 4)},
+                "median_ms": {n: round(v[2], 5) for n, v in k.items()},
+                "min_ms": {n: round(v[1], 5) for n, v in k.items()},
+            },
+            "end_to_end_TFLOP/s": {"f32": round(flops / ((t32 + c32) * 1e-3) / 1e12, 3),
+                                   "f16": round(flops / ((t16 + c16) * 1e-3) / 1e12, 3)},
+            "workspace": {
+                "f32_window_bytes": f32["window_bytes"], "f32_im2col_bytes": f32["im2col_bytes"],
+                "f32_window_over_im2col": round(f32["window_bytes"] / f32["im2col_bytes"], 4),
+                "f16_window_bytes": f16["window_bytes"], "f16_im2col_bytes": f16["im2col_bytes"],
+                "f16_workspace_bytes": f16["workspace_bytes"],
+                "f16_workspace_over_im2col": round(f16["workspace_bytes"] / f16["im2col_bytes"], 4),
+                "allocator_peak_bytes": peak_alloc,
+            },
+        }
+        if not args.no_cpu_baseline and not args.sweep:
+            rec["cpu_baseline"] = cpu_baseline(l, x, w)
+        print(json.dumps(rec), flush=True)
+        del paths
+        torch.cuda.empty_cache()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,153 @@
+/*
+ * im2win.h -- im2win convolution on AMD Instinct MI355X (gfx950).
+ *
+ * Plain C interface: no HIP or framework types cross it, only host scalars
+ * and device pointers.  The operation follows the paper's definitions:
+ *
+ *   convolution (Sec. III-A, Eq. 1), with the stride written in, 0-based:
+ *     O[i][m][n][j] = sum_{u<K_h} sum_{v<K_w} sum_{r<C_i}
+ *                       I[i][m*s+u][n*s+v][r] * F[u][v][r][j]
+ *   window tensor (Sec. III-B, Eq. 2), NHWC element order:
+ *     W[i][m][k*K_h+u][r] = I[i][m*s+u][k][r]
+ *   windowed convolution (Sec. III-C, Eq. 3): the window of output (i,m,n) is
+ *     the contiguous span of strip (i,m) that starts at element n*s*K_h*C_i and
+ *     holds K = K_h*K_w*C_i elements in (filter column, filter row, channel)
+ *     order.
+ *
+ * Layouts (all dense, row-major, no padding):
+ *   input  I  NHWC [N][H_i][W_i][C_i]
+ *   filter F  [K_h][K_w][C_i][C_o]     (filter height, width, in, out channel)
+ *   output O  NHWC [N][H_o][W_o][C_o], H_o = (H_i-K_h)/s + 1, W_o = (W_i-K_w)/s + 1
+ *   workspace (caller-allocated device memory, see conv_workspace_bytes):
+ *     [0, win)        window tensor W [N][H_o][W_i*K_h][C_i], win = N*H_o*W_i*K_h*C_i*elt
+ *     [win, pad_end)  zero bytes, pad_end = round_up(win, 256) + 256; they let
+ *                     the kernels read past the last window without leaving
+ *                     the buffer
+ *     [pad_end, ...)  fp16 only: the filter repacked as [C_o_pad][K_pad] fp16
+ *                     in window order, zero-padded, C_o_pad = round_up(C_o, 128),
+ *                     K_pad = round_up(K, 64); written by conv_im2win_fp16
+ *
+ * Scope: one stride for both axes, no padding, dilation, groups or bias.
+ *
+ * Ownership and threading: the caller allocates and frees every buffer; the
+ * library allocates nothing and keeps no state except a once-filled per-device
+ * record of whether the device is a gfx950.  Calls are reentrant.
+ *
+ * Streams: every device call only enqueues work on `hip_stream` (a
+ * hipStream_t; NULL is the null stream) and returns without synchronising.
+ * A conv call reads the window tensor, so it must be ordered after the
+ * transform that wrote it (same stream, or an event).
+ *
+ * Errors: arguments are checked before anything is enqueued, in this order:
+ * null pointers -> dimensions -> index ranges -> alignment -> buffer extents
+ * (each pointer must lie in one device allocation that holds the whole
+ * buffer) -> overlap -> workspace size -> device -> launch.  The first failing
+ * check's status is returned; nothing is printed and no exception leaves the
+ * library.  Numerics: fp32 conv accumulates in fp32 (FMA); fp16 conv takes
+ * fp16 operands, accumulates in fp32 and rounds to nearest-even on store.
+ */
+#ifndef IM2WIN_H
+#define IM2WIN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { IM2WIN_F32 = 0, IM2WIN_F16 = 1 } im2win_dtype_t;
+
+enum {
+    IM2WIN_OK = 0,
+    IM2WIN_EINVAL = -1,     /* null pointer, bad dtype, dims <= 0, K_h > H_i, K_w > W_i, s < 1 */
+    IM2WIN_EALIGN = -2,     /* a device pointer is not 16-byte aligned */
+    IM2WIN_ERANGE = -3,     /* a size overflows the library's index ranges (see below) */
+    IM2WIN_ENODEV = -4,     /* the current device is not a gfx950 GPU, or none is usable */
+    IM2WIN_ELAUNCH = -5,    /* a kernel launch was rejected by the runtime */
+    IM2WIN_EWORKSPACE = -6, /* ws_bytes < conv_workspace_bytes(...) */
+    IM2WIN_EOVERLAP = -7,   /* two buffers overlap */
+    IM2WIN_EBUFFER = -8     /* a pointer is not device memory, or its allocation is too small */
+};
+
+/*
+ * Output extent (no padding): *H_o = (H_i - K_h)/s + 1, *W_o = (W_i - K_w)/s + 1
+ * (Table I sizes).  Host only.  Returns IM2WIN_OK or IM2WIN_EINVAL.
+ */
+int conv_output_dims(int64_t H_i, int64_t W_i, int64_t K_h, int64_t K_w, int64_t stride,
+                     int64_t *H_o, int64_t *W_o);
+
+/*
+ * Bytes of workspace the transform and the conv of this layer need (layout
+ * above): the window tensor of Eq. 2 plus the 256-byte zero pad, plus, for
+ * IM2WIN_F16, the packed filter.  Host only, no device calls.  Returns a
+ * negative status for invalid arguments (IM2WIN_EINVAL, IM2WIN_ERANGE).
+ *
+ * Index ranges the kernels support (else IM2WIN_ERANGE): one strip
+ * W_i*K_h*C_i < 2^20 elements, K = K_h*K_w*C_i < 2^24, C_o < 2^19,
+ * N*H_o*W_o < 2^31 output pixels, N*H_o < 2^31 strips, and every byte count
+ * below 2^62.
+ */
+int64_t conv_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
+                             int64_t K_h, int64_t K_w, int64_t stride, im2win_dtype_t dt);
+
+/*
+ * Bytes of the full-batch im2col matrix of the same layer,
+ * N*H_o*W_o * K_h*K_w*C_i * elt (one row per output pixel, one column per
+ * filter tap and channel; Sec. III-B and Fig. 1).  The comparator for the
+ * workspace figure; the library never builds it.  Host only.
+ */
+int64_t conv_im2col_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
+                          int64_t K_h, int64_t K_w, int64_t stride, im2win_dtype_t dt);
+
+/*
+ * The im2win transform (Sec. III-B, Eq. 2).
+ *   in_nhwc  device, input I (fp32 or fp16 bits, per `dt`), read only
+ *   ws       device, workspace of ws_bytes >= conv_workspace_bytes(..., dt);
+ *            the window tensor and the zero pad are written, the rest of the
+ *            workspace is left alone
+ * The copy is bit-exact and does not depend on the element type beyond its
+ * size.  C_o and K_w only size the workspace check.
+ */
+int conv_im2win_transform(const void *in_nhwc, void *ws, int64_t ws_bytes,
+                          int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
+                          int64_t K_h, int64_t K_w, int64_t stride, im2win_dtype_t dt,
+                          void *hip_stream);
+
+/*
+ * fp32 windowed convolution on the vector ALUs (Sec. III-C, Eq. 3; the
+ * paper's CUDA-core variant, Sec. IV-A).
+ *   ws              device, workspace holding the fp32 window tensor written
+ *                   by conv_im2win_transform(..., IM2WIN_F32); read only
+ *   filt_khkwcico   device, fp32 filter F [K_h][K_w][C_i][C_o]; read only
+ *   out_nhwc        device, fp32 output O [N][H_o][W_o][C_o]; every element
+ *                   is written exactly once
+ * Accumulation is fp32 fused multiply-add.
+ */
+int conv_im2win_fp32(const void *ws, int64_t ws_bytes, const float *filt_khkwcico,
+                     float *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
+                     int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream);
+
+/*
+ * fp16 windowed convolution on the matrix cores (Sec. III-D, Alg. 1: the
+ * output as an M = C_o by N = N*H_o*W_o product over K = C_i*K_h*K_w).
+ *   ws              device, workspace holding the fp16 window tensor written
+ *                   by conv_im2win_transform(..., IM2WIN_F16); the window
+ *                   tensor is read, the packed-filter region is overwritten
+ *   filt_khkwcico   device, fp16 bits of F [K_h][K_w][C_i][C_o]; read only
+ *   out_nhwc        device, fp16 bits of O [N][H_o][W_o][C_o]; every element
+ *                   is written exactly once
+ * Products of fp16 operands are accumulated in fp32; each output is rounded
+ * to fp16 (nearest-even) once.
+ */
+int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
+                     uint16_t *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
+                     int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream);
+
+/* A static, human-readable name for a status code. */
+const char *conv_im2win_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IM2WIN_H */

@@ -1,0 +1,192 @@
+"""im2win convolution on AMD Instinct MI355X (gfx950).
+
+A thin ctypes binding over ``libim2win.so`` (``include/im2win.h``).  Every
+function only marshals arguments: shapes and device pointers of PyTorch
+tensors, and the current HIP stream.  All work runs in the library's gfx950
+kernels; there is no fallback, and a missing library raises.
+
+    H_o, W_o = conv_output_dims(H_i, W_i, K_h, K_w, stride)
+    nbytes   = conv_workspace_bytes(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dtype)
+    conv_im2win_transform(x, ws, C_o, K_h, K_w, stride)        # Sec. III-B, Eq. 2
+    conv_im2win_fp32(ws, w, out, N, C_i, H_i, W_i, stride)     # Sec. III-C, Eq. 3
+    conv_im2win_fp16(ws, w, out, N, C_i, H_i, W_i, stride)     # Sec. III-D, Alg. 1
+
+Layouts: ``x`` NHWC, ``w`` [K_h][K_w][C_i][C_o], ``out`` NHWC; ``ws`` is a
+flat byte tensor on the same device.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "Im2winError", "load_library", "library_path", "F32", "F16",
+    "conv_output_dims", "conv_workspace_bytes", "conv_im2col_bytes",
+    "conv_im2win_transform", "conv_im2win_fp32", "conv_im2win_fp16",
+    "conv_im2win_strerror", "im2win_conv2d",
+]
+
+F32 = 0
+F16 = 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libim2win.so")
+_lib = None
+
+_i64 = ctypes.c_int64
+_vp = ctypes.c_void_p
+
+
+class Im2winError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (what, conv_im2win_strerror(status), status))
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Loads libim2win.so from the package directory (built in-tree)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError("libim2win.so is not built (expected at %s); run "
+                           "`python -c 'import __graft_entry__ as g; g.build()'`" % _LIB_PATH)
+    lib = ctypes.CDLL(_LIB_PATH)
+    lib.conv_output_dims.restype = ctypes.c_int
+    lib.conv_output_dims.argtypes = [_i64] * 5 + [ctypes.POINTER(_i64)] * 2
+    lib.conv_workspace_bytes.restype = _i64
+    lib.conv_workspace_bytes.argtypes = [_i64] * 8 + [ctypes.c_int]
+    lib.conv_im2col_bytes.restype = _i64
+    lib.conv_im2col_bytes.argtypes = [_i64] * 7 + [ctypes.c_int]
+    lib.conv_im2win_transform.restype = ctypes.c_int
+    lib.conv_im2win_transform.argtypes = [_vp, _vp, _i64] + [_i64] * 8 + [ctypes.c_int, _vp]
+    lib.conv_im2win_fp32.restype = ctypes.c_int
+    lib.conv_im2win_fp32.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
+    lib.conv_im2win_fp16.restype = ctypes.c_int
+    lib.conv_im2win_fp16.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
+    lib.conv_im2win_strerror.restype = ctypes.c_char_p
+    lib.conv_im2win_strerror.argtypes = [ctypes.c_int]
+    _lib = lib
+    return lib
+
+
+def conv_im2win_strerror(status: int) -> str:
+    return load_library().conv_im2win_strerror(int(status)).decode()
+
+
+def _dtype_code(dtype) -> int:
+    import torch
+    if dtype in (F32, "f32", "fp32", torch.float32):
+        return F32
+    if dtype in (F16, "f16", "fp16", torch.float16):
+        return F16
+    raise ValueError("dtype must be fp32 or fp16, got %r" % (dtype,))
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise Im2winError(rc, what)
+
+
+def conv_output_dims(H_i: int, W_i: int, K_h: int, K_w: int, stride: int):
+    ho, wo = _i64(), _i64()
+    _check(load_library().conv_output_dims(H_i, W_i, K_h, K_w, stride,
+                                           ctypes.byref(ho), ctypes.byref(wo)), "conv_output_dims")
+    return ho.value, wo.value
+
+
+def conv_workspace_bytes(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dtype) -> int:
+    n = load_library().conv_workspace_bytes(N, C_i, H_i, W_i, C_o, K_h, K_w, stride,
+                                            _dtype_code(dtype))
+    if n < 0:
+        raise Im2winError(int(n), "conv_workspace_bytes")
+    return int(n)
+
+
+def conv_im2col_bytes(N, C_i, H_i, W_i, K_h, K_w, stride, dtype) -> int:
+    n = load_library().conv_im2col_bytes(N, C_i, H_i, W_i, K_h, K_w, stride, _dtype_code(dtype))
+    if n < 0:
+        raise Im2winError(int(n), "conv_im2col_bytes")
+    return int(n)
+
+
+def conv_im2win_transform(x, ws, C_o: int, K_h: int, K_w: int, stride: int, stream=None):
+    """Writes the window tensor of NHWC input ``x`` (fp32 or fp16) into ``ws``."""
+    if x.dim() != 4 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous NHWC tensor")
+    N, H_i, W_i, C_i = x.shape
+    rc = load_library().conv_im2win_transform(
+        _ptr(x), _ptr(ws), _nbytes(ws), N, C_i, H_i, W_i, C_o, K_h, K_w, stride,
+        _dtype_code(x.dtype), _stream(stream))
+    _check(rc, "conv_im2win_transform")
+
+
+def _conv(fn, what, ws, w, out, N, C_i, H_i, W_i, stride, stream):
+    if w.dim() != 4 or not w.is_contiguous() or not out.is_contiguous():
+        raise ValueError("w must be a contiguous [K_h][K_w][C_i][C_o] tensor, out contiguous")
+    K_h, K_w, C_i2, C_o = w.shape
+    if C_i2 != C_i:
+        raise ValueError("filter has %d input channels, layer has %d" % (C_i2, C_i))
+    rc = fn(_ptr(ws), _nbytes(ws), _ptr(w), _ptr(out), N, C_i, H_i, W_i, C_o, K_h, K_w, stride,
+            _stream(stream))
+    _check(rc, what)
+
+
+def conv_im2win_fp32(ws, w, out, N: int, C_i: int, H_i: int, W_i: int, stride: int, stream=None):
+    """fp32 conv from the fp32 window tensor in ``ws``; ``out`` is NHWC fp32."""
+    import torch
+    if w.dtype != torch.float32 or out.dtype != torch.float32:
+        raise TypeError("conv_im2win_fp32 takes fp32 filter and output")
+    _conv(load_library().conv_im2win_fp32, "conv_im2win_fp32", ws, w, out, N, C_i, H_i, W_i,
+          stride, stream)
+
+
+def conv_im2win_fp16(ws, w, out, N: int, C_i: int, H_i: int, W_i: int, stride: int, stream=None):
+    """fp16 conv (fp32 accumulation) from the fp16 window tensor in ``ws``."""
+    import torch
+    if w.dtype != torch.float16 or out.dtype != torch.float16:
+        raise TypeError("conv_im2win_fp16 takes fp16 filter and output")
+    _conv(load_library().conv_im2win_fp16, "conv_im2win_fp16", ws, w, out, N, C_i, H_i, W_i,
+          stride, stream)
+
+
+def im2win_conv2d(x, w, stride: int, ws=None, out=None, stream=None):
+    """Transform + conv on the current stream; allocates what is not given.
+
+    Returns (out, ws)."""
+    import torch
+    N, H_i, W_i, C_i = x.shape
+    K_h, K_w, _, C_o = w.shape
+    H_o, W_o = conv_output_dims(H_i, W_i, K_h, K_w, stride)
+    need = conv_workspace_bytes(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, x.dtype)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=x.device)
+    if out is None:
+        out = torch.empty((N, H_o, W_o, C_o), dtype=x.dtype, device=x.device)
+    conv_im2win_transform(x, ws, C_o, K_h, K_w, stride, stream)
+    if x.dtype == torch.float32:
+        conv_im2win_fp32(ws, w, out, N, C_i, H_i, W_i, stride, stream)
+    else:
+        conv_im2win_fp16(ws, w, out, N, C_i, H_i, W_i, stride, stream)
+    return out, ws

@@ -1,0 +1,48 @@
+"""Builds libim2win.so (the C-ABI library and its gfx950 kernels) in-tree.
+
+Every HIP source is compiled for gfx950 only, with packed fp32 VALU
+instructions disabled (``-packed-fp32-ops``): the fp32 path uses plain
+v_fma_f32 / v_fmac_f32.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+LIB = os.path.join(HERE, "libim2win.so")
+SOURCES = ["api.cpp", "transform.hip", "conv_fp32.hip", "conv_fp16.hip"]
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+FLAGS = [
+    "-x", "hip", "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-function",
+    "-I", os.path.join(ROOT, "include"),
+]
+
+
+def build(verbose: bool = False) -> str:
+    srcs = [os.path.join(CSRC, s) for s in SOURCES]
+    tmp = LIB + ".tmp%d" % os.getpid()
+    cmd = [HIPCC] + FLAGS + srcs + ["-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    p = subprocess.run(cmd, capture_output=True, text=True)
+    # the host pass does not know the gfx950 feature name: drop that warning
+    noise = [l for l in (p.stdout + p.stderr).splitlines()
+             if l.strip() and "packed-fp32-ops" not in l]
+    if p.returncode != 0:
+        sys.stderr.write("\n".join(noise) + "\n")
+        raise RuntimeError("hipcc failed building libim2win.so")
+    if verbose and noise:
+        print("\n".join(noise))
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

@@ -1,0 +1,277 @@
+// Host side of the C interface: argument checks, workspace accounting,
+// device check and kernel dispatch.  The operations themselves run in the
+// gfx950 kernels of transform.hip, conv_fp32.hip and conv_fp16.hip.
+#include "../../include/im2win.h"
+#include "common.hpp"
+
+#include <atomic>
+#include <string.h>
+
+using namespace im2win;
+
+namespace {
+
+constexpr int64_t kMaxStrip = int64_t(1) << 20;
+constexpr int64_t kMaxK = int64_t(1) << 24;
+constexpr int64_t kMaxCo = int64_t(1) << 19;
+constexpr int64_t kMaxBytes = int64_t(1) << 62;
+constexpr int64_t kPad = 256;
+
+bool mul_ok(int64_t a, int64_t b, int64_t lim, int64_t *out)
+{
+    if (a < 0 || b < 0)
+        return false;
+    if (a != 0 && b > lim / a)
+        return false;
+    *out = a * b;
+    return true;
+}
+
+// Fills `sh` from the user's arguments; returns a status.
+int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_t Kh,
+               int64_t Kw, int64_t s, int dt, Shape *sh)
+{
+    if (dt != IM2WIN_F32 && dt != IM2WIN_F16)
+        return IM2WIN_EINVAL;
+    if (N <= 0 || Ci <= 0 || Hi <= 0 || Wi <= 0 || Co <= 0 || Kh <= 0 || Kw <= 0 || s <= 0)
+        return IM2WIN_EINVAL;
+    if (Kh > Hi || Kw > Wi)
+        return IM2WIN_EINVAL;
+    Shape r;
+    memset(&r, 0, sizeof r);
+    r.N = N; r.Ci = Ci; r.Hi = Hi; r.Wi = Wi; r.Co = Co; r.Kh = Kh; r.Kw = Kw; r.s = s;
+    r.Ho = (Hi - Kh) / s + 1;
+    r.Wo = (Wi - Kw) / s + 1;
+    r.elt = dt == IM2WIN_F32 ? 4 : 2;
+    int64_t t;
+    if (!mul_ok(Wi, Kh, kMaxStrip, &t) || !mul_ok(t, Ci, kMaxStrip - 1, &r.L))
+        return IM2WIN_ERANGE;
+    if (!mul_ok(Kh, Kw, kMaxK, &t) || !mul_ok(t, Ci, kMaxK - 1, &r.K))
+        return IM2WIN_ERANGE;
+    if (Co >= kMaxCo)
+        return IM2WIN_ERANGE;
+    r.S = s * Kh * Ci;  // s <= W_i and Kh*Ci <= L: below 2^46
+    if (!mul_ok(N, r.Ho, INT32_MAX, &r.strips))
+        return IM2WIN_ERANGE;
+    if (!mul_ok(r.strips, r.Wo, INT32_MAX, &r.P))
+        return IM2WIN_ERANGE;
+    if (!mul_ok(r.strips, r.L, kMaxBytes, &r.win_elems) ||
+        !mul_ok(r.win_elems, r.elt, kMaxBytes, &r.win_bytes))
+        return IM2WIN_ERANGE;
+    r.pad_end = round_up(r.win_bytes, kPad) + kPad;
+    r.Co_pad = round_up(Co, 128);
+    r.K_pad = round_up(r.K, 64);
+    *sh = r;
+    return IM2WIN_OK;
+}
+
+int64_t packed_filter_bytes(const Shape &sh) { return sh.Co_pad * sh.K_pad * 2; }
+
+int64_t workspace_bytes(const Shape &sh, int dt)
+{
+    return sh.pad_end + (dt == IM2WIN_F16 ? packed_filter_bytes(sh) : 0);
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+// The buffer [p, p+bytes) must lie inside one device allocation.
+int check_extent(const void *p, int64_t bytes)
+{
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    hipError_t e = hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();  // leave no sticky error behind for the caller
+        return IM2WIN_EBUFFER;
+    }
+    uintptr_t b = (uintptr_t)base, q = (uintptr_t)p;
+    if (q < b || (uint64_t)(q - b) + (uint64_t)bytes > (uint64_t)size)
+        return IM2WIN_EBUFFER;
+    return IM2WIN_OK;
+}
+
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb)
+{
+    uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x < y + (uint64_t)nb && y < x + (uint64_t)na;
+}
+
+// Per-device record: 0 unknown, 1 gfx950, -1 something else.
+std::atomic<int> g_arch[64];
+
+int check_device()
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+        (void)hipGetLastError();
+        return IM2WIN_ENODEV;
+    }
+    int known = g_arch[dev].load(std::memory_order_acquire);
+    if (known == 0) {
+        hipDeviceProp_t prop;
+        if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+            (void)hipGetLastError();
+            return IM2WIN_ENODEV;
+        }
+        known = strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+        g_arch[dev].store(known, std::memory_order_release);
+    }
+    return known == 1 ? IM2WIN_OK : IM2WIN_ENODEV;
+}
+
+int launch_status(hipError_t e)
+{
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return IM2WIN_ELAUNCH;
+    }
+    return IM2WIN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int conv_output_dims(int64_t H_i, int64_t W_i, int64_t K_h, int64_t K_w, int64_t stride,
+                     int64_t *H_o, int64_t *W_o)
+{
+    if (!H_o || !W_o)
+        return IM2WIN_EINVAL;
+    if (H_i <= 0 || W_i <= 0 || K_h <= 0 || K_w <= 0 || stride <= 0 || K_h > H_i || K_w > W_i)
+        return IM2WIN_EINVAL;
+    *H_o = (H_i - K_h) / stride + 1;
+    *W_o = (W_i - K_w) / stride + 1;
+    return IM2WIN_OK;
+}
+
+int64_t conv_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
+                             int64_t K_h, int64_t K_w, int64_t stride, im2win_dtype_t dt)
+{
+    Shape sh;
+    int rc = make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, (int)dt, &sh);
+    if (rc != IM2WIN_OK)
+        return rc;
+    return workspace_bytes(sh, (int)dt);
+}
+
+int64_t conv_im2col_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t K_h,
+                          int64_t K_w, int64_t stride, im2win_dtype_t dt)
+{
+    Shape sh;
+    int rc = make_shape(N, C_i, H_i, W_i, 1, K_h, K_w, stride, (int)dt, &sh);
+    if (rc != IM2WIN_OK)
+        return rc;
+    int64_t e, b;
+    if (!mul_ok(sh.P, sh.K, kMaxBytes, &e) || !mul_ok(e, sh.elt, kMaxBytes, &b))
+        return IM2WIN_ERANGE;
+    return b;
+}
+
+int conv_im2win_transform(const void *in_nhwc, void *ws, int64_t ws_bytes, int64_t N,
+                          int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h,
+                          int64_t K_w, int64_t stride, im2win_dtype_t dt, void *hip_stream)
+{
+    if (!in_nhwc || !ws)
+        return IM2WIN_EINVAL;
+    Shape sh;
+    int rc = make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, (int)dt, &sh);
+    if (rc != IM2WIN_OK)
+        return rc;
+    if (!transform_range_ok(sh))
+        return IM2WIN_ERANGE;
+    if (!aligned16(in_nhwc) || !aligned16(ws))
+        return IM2WIN_EALIGN;
+    const int64_t in_bytes = N * H_i * W_i * C_i * sh.elt;
+    if (ws_bytes < 0)
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_extent(in_nhwc, in_bytes)) != IM2WIN_OK)
+        return rc;
+    if ((rc = check_extent(ws, ws_bytes)) != IM2WIN_OK)
+        return rc;
+    if (overlaps(in_nhwc, in_bytes, ws, ws_bytes))
+        return IM2WIN_EOVERLAP;
+    if (ws_bytes < workspace_bytes(sh, (int)dt))
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_device()) != IM2WIN_OK)
+        return rc;
+    return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream));
+}
+
+int conv_im2win_fp32(const void *ws, int64_t ws_bytes, const float *filt_khkwcico,
+                     float *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
+                     int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream)
+{
+    if (!ws || !filt_khkwcico || !out_nhwc)
+        return IM2WIN_EINVAL;
+    Shape sh;
+    int rc = make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, IM2WIN_F32, &sh);
+    if (rc != IM2WIN_OK)
+        return rc;
+    if (!aligned16(ws) || !aligned16(filt_khkwcico) || !aligned16(out_nhwc))
+        return IM2WIN_EALIGN;
+    const int64_t f_bytes = sh.K * C_o * 4, o_bytes = sh.P * C_o * 4;
+    if (ws_bytes < 0)
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_extent(ws, ws_bytes)) != IM2WIN_OK ||
+        (rc = check_extent(filt_khkwcico, f_bytes)) != IM2WIN_OK ||
+        (rc = check_extent(out_nhwc, o_bytes)) != IM2WIN_OK)
+        return rc;
+    if (overlaps(ws, ws_bytes, out_nhwc, o_bytes) || overlaps(filt_khkwcico, f_bytes, out_nhwc, o_bytes) ||
+        overlaps(ws, ws_bytes, filt_khkwcico, f_bytes))
+        return IM2WIN_EOVERLAP;
+    if (ws_bytes < workspace_bytes(sh, IM2WIN_F32))
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_device()) != IM2WIN_OK)
+        return rc;
+    return launch_status(launch_conv_fp32(sh, ws, filt_khkwcico, out_nhwc, (hipStream_t)hip_stream));
+}
+
+int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
+                     uint16_t *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
+                     int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream)
+{
+    if (!ws || !filt_khkwcico || !out_nhwc)
+        return IM2WIN_EINVAL;
+    Shape sh;
+    int rc = make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, IM2WIN_F16, &sh);
+    if (rc != IM2WIN_OK)
+        return rc;
+    if (!aligned16(ws) || !aligned16(filt_khkwcico) || !aligned16(out_nhwc))
+        return IM2WIN_EALIGN;
+    const int64_t f_bytes = sh.K * C_o * 2, o_bytes = sh.P * C_o * 2;
+    if (ws_bytes < 0)
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_extent(ws, ws_bytes)) != IM2WIN_OK ||
+        (rc = check_extent(filt_khkwcico, f_bytes)) != IM2WIN_OK ||
+        (rc = check_extent(out_nhwc, o_bytes)) != IM2WIN_OK)
+        return rc;
+    if (overlaps(ws, ws_bytes, out_nhwc, o_bytes) || overlaps(filt_khkwcico, f_bytes, out_nhwc, o_bytes) ||
+        overlaps(ws, ws_bytes, filt_khkwcico, f_bytes))
+        return IM2WIN_EOVERLAP;
+    if (ws_bytes < workspace_bytes(sh, IM2WIN_F16))
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_device()) != IM2WIN_OK)
+        return rc;
+    void *packed = (char *)ws + sh.pad_end;
+    if ((rc = launch_status(launch_pack_fp16(sh, filt_khkwcico, packed, (hipStream_t)hip_stream))) != IM2WIN_OK)
+        return rc;
+    return launch_status(launch_conv_fp16(sh, ws, packed, out_nhwc, (hipStream_t)hip_stream));
+}
+
+const char *conv_im2win_strerror(int status)
+{
+    switch (status) {
+    case IM2WIN_OK: return "ok";
+    case IM2WIN_EINVAL: return "invalid argument";
+    case IM2WIN_EALIGN: return "pointer not 16-byte aligned";
+    case IM2WIN_ERANGE: return "size outside the supported index range";
+    case IM2WIN_ENODEV: return "no gfx950 device";
+    case IM2WIN_ELAUNCH: return "kernel launch failed";
+    case IM2WIN_EWORKSPACE: return "workspace too small";
+    case IM2WIN_EOVERLAP: return "buffers overlap";
+    case IM2WIN_EBUFFER: return "not device memory, or the allocation is too small";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,105 @@
+// Internal definitions shared by the host API and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace im2win {
+
+// Division of a 32-bit unsigned value by a launch-constant divisor d >= 1
+// with one high multiply, one add and one shift (Granlund & Montgomery,
+// "Division by invariant integers using multiplication", PLDI 1994, Fig. 4.1:
+// l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1, q = (mulhi(m, x) + x) >> l,
+// the add done in 33 bits).  Exact for every x < 2^32.
+struct FastDiv {
+    uint32_t d;
+    uint32_t mul;
+    uint32_t shift;
+};
+
+inline FastDiv make_fastdiv(uint32_t d)
+{
+    uint32_t l = 0;
+    while ((1ull << l) < d)
+        ++l;
+    uint64_t m = ((1ull << 32) * ((1ull << l) - d)) / d + 1;
+    return FastDiv{d, (uint32_t)m, l};
+}
+
+__host__ __device__ inline uint32_t fdiv(uint32_t x, const FastDiv &f)
+{
+#if defined(__HIP_DEVICE_COMPILE__)
+    uint32_t hi = __umulhi(x, f.mul);
+#else
+    uint32_t hi = (uint32_t)(((uint64_t)x * f.mul) >> 32);
+#endif
+    return (uint32_t)(((uint64_t)hi + x) >> f.shift);
+}
+
+// Everything a kernel needs to know about one layer.  Built and validated on
+// the host (api.cpp).
+struct Shape {
+    int64_t N, Ci, Hi, Wi, Co, Kh, Kw, s;
+    int64_t Ho, Wo;
+    int64_t P;          // output pixels N*Ho*Wo
+    int64_t K;          // window length Kh*Kw*Ci
+    int64_t L;          // strip length Wi*Kh*Ci (elements)
+    int64_t S;          // window step along a strip s*Kh*Ci (elements)
+    int64_t strips;     // N*Ho
+    int64_t win_elems;  // strips*L
+    int64_t elt;        // element bytes
+    int64_t win_bytes;  // win_elems*elt
+    int64_t pad_end;    // end of the zero pad (bytes)
+    int64_t Co_pad;     // packed fp16 filter rows
+    int64_t K_pad;      // packed fp16 filter columns
+};
+
+inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+// Raw buffer resource (gfx9 family): base, no swizzle, num_records bytes.
+// Loads whose byte offset falls outside [0, num_records) return zero and
+// stores there are dropped by the hardware.
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+// Byte offset used for a masked-off load: beyond every num_records the
+// kernels use (they cap num_records at kMaxRecords), so the load returns 0.
+constexpr uint32_t kOOB = 0x80000000u;
+
+// Native 4 x 32-bit vector (kept in registers; HIP's uint4 is a struct whose
+// copies can end up in scratch memory).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr uint32_t kMaxRecords = 0x7fffff00u;
+
+__device__ inline u32x4 ld_b128(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+}
+
+__device__ inline uint32_t ld_b32(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+}
+
+__device__ inline uint32_t ld_b16(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
+}
+
+} // namespace im2win
+
+// Kernel launchers (one per translation unit).  Each returns a hipError_t from
+// the launch itself; the shape has been validated.
+namespace im2win {
+// The gather form of the transform indexes elements with 32 bits.
+bool transform_range_ok(const Shape &sh);
+hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st);
+hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const float *filt, float *out,
+                            hipStream_t st);
+hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed, hipStream_t st);
+hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed, uint16_t *out,
+                            hipStream_t st);
+} // namespace im2win

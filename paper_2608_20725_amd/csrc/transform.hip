@@ -1,0 +1,185 @@
+// im2win transform (Sec. III-B, Eq. 2) for gfx950.
+//
+//   W[i][m][k*K_h + u][r] = I[i][m*s + u][k][r]
+//
+// Pure copy, HBM-bound: every byte of the window tensor is written once with
+// a 16-byte store; the K_h/s-fold re-reads of input rows are served by L2 and
+// the Infinity Cache.  Two kernels:
+//   * vec:    C_i*elt is a multiple of 16 bytes.  A thread copies whole
+//             16-byte granules; one workgroup covers a contiguous run of one
+//             strip, so the stores of a wave are one contiguous 1 KiB run.
+//   * gather: any other C_i (e.g. the 3-channel stem layers).  A thread
+//             assembles one 16-byte granule of the flat window tensor element
+//             by element; granules may straddle strips.
+// Both zero the pad bytes that follow the window tensor.
+#include "common.hpp"
+
+namespace im2win {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kGranPerThread = 4;
+
+struct TArgs {
+    const char *in;
+    char *ws;
+    uint32_t Ci, Hi, Wi, Kh, s, Ho;
+    uint32_t L;              // strip length (elements)
+    uint32_t strips;
+    uint32_t gran_per_strip; // vec: 16-byte granules per strip
+    uint64_t win_elems;
+    uint64_t win_bytes, pad_end;
+    uint64_t grans;          // gather: 16-byte granules of the window tensor
+    FastDiv div_Ci, div_Kh, div_Wi, div_Ho, div_L;
+};
+
+__device__ inline void zero_pad(const TArgs &a)
+{
+    // [win_bytes, pad_end) holds at most 256 + 255 + 15 bytes
+    for (uint64_t b = a.win_bytes + threadIdx.x; b < a.pad_end; b += blockDim.x)
+        a.ws[b] = 0;
+}
+
+template <int ELT>
+__global__ __launch_bounds__(kThreads) void transform_vec(TArgs a)
+{
+    constexpr uint32_t V = 16 / ELT;  // elements per granule
+    // strip index q over gridDim.y * gridDim.z
+    const uint32_t q = blockIdx.y + blockIdx.z * gridDim.y;
+    if (q >= a.strips)
+        return;
+    if (q == 0 && blockIdx.x == 0)
+        zero_pad(a);
+    const uint32_t i = fdiv(q, a.div_Ho);
+    const uint32_t m = q - i * a.Ho;
+    const char *img = a.in + (uint64_t)i * a.Hi * a.Wi * a.Ci * ELT;
+    char *strip = a.ws + (uint64_t)q * a.L * ELT;
+    const uint32_t g0 = blockIdx.x * (kThreads * kGranPerThread) + threadIdx.x;
+#pragma unroll
+    for (int t = 0; t < kGranPerThread; ++t) {
+        const uint32_t g = g0 + t * kThreads;
+        if (g < a.gran_per_strip) {
+            const uint32_t pos = g * V;                // element within the strip
+            const uint32_t seg = fdiv(pos, a.div_Ci);  // k*K_h + u
+            const uint32_t r = pos - seg * a.Ci;
+            const uint32_t k = fdiv(seg, a.div_Kh);
+            const uint32_t u = seg - k * a.Kh;
+            const uint64_t src = ((uint64_t)(m * a.s + u) * a.Wi + k) * a.Ci + r;
+            const uint4 v = *reinterpret_cast<const uint4 *>(img + src * ELT);
+            *reinterpret_cast<uint4 *>(strip + (uint64_t)pos * ELT) = v;
+        }
+    }
+}
+
+template <int ELT>
+__device__ inline void store_elem(uint32_t *w, int e, uint32_t bits)
+{
+    if (ELT == 4) {
+        w[e] = bits;
+    } else {
+        const int d = e >> 1;
+        w[d] = (e & 1) ? (w[d] & 0xffffu) | (bits << 16) : (w[d] & 0xffff0000u) | (bits & 0xffffu);
+    }
+}
+
+template <int ELT>
+__global__ __launch_bounds__(kThreads) void transform_gather(TArgs a)
+{
+    constexpr uint32_t V = 16 / ELT;
+    const uint64_t g = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (blockIdx.x == 0)
+        zero_pad(a);
+    if (g >= a.grans)
+        return;
+    // first element of this granule; win_elems < 2^32 is checked on the host
+    uint32_t e = (uint32_t)(g * V);
+    uint32_t q = fdiv(e, a.div_L);
+    uint32_t pos = e - q * a.L;
+    uint32_t seg = fdiv(pos, a.div_Ci);
+    uint32_t r = pos - seg * a.Ci;
+    uint32_t k = fdiv(seg, a.div_Kh);
+    uint32_t u = seg - k * a.Kh;
+    uint32_t i = fdiv(q, a.div_Ho);
+    uint32_t m = q - i * a.Ho;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (uint32_t t = 0; t < V; ++t) {
+        if ((uint64_t)e + t < a.win_elems) {
+            const uint64_t src = (((uint64_t)i * a.Hi + m * a.s + u) * a.Wi + k) * a.Ci + r;
+            uint32_t bits;
+            if (ELT == 4)
+                bits = reinterpret_cast<const uint32_t *>(a.in)[src];
+            else
+                bits = reinterpret_cast<const uint16_t *>(a.in)[src];
+            store_elem<ELT>(w, (int)t, bits);
+            // advance (r, u, k, m, i) to the next window-tensor element
+            if (++r == a.Ci) {
+                r = 0;
+                if (++u == a.Kh) {
+                    u = 0;
+                    if (++k == a.Wi) {
+                        k = 0;
+                        if (++m == a.Ho) {
+                            m = 0;
+                            ++i;
+                        }
+                    }
+                }
+            }
+        }
+    }
+    // bytes past the window tensor are inside the zero pad: zeros are written
+    *reinterpret_cast<uint4 *>(a.ws + g * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+}  // namespace
+
+bool transform_range_ok(const Shape &sh)
+{
+    if ((sh.Ci * sh.elt) % 16 == 0)
+        return true;
+    return (uint64_t)sh.win_elems + 16 < (1ull << 32);
+}
+
+hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st)
+{
+    TArgs a;
+    a.in = static_cast<const char *>(in);
+    a.ws = static_cast<char *>(ws);
+    a.Ci = (uint32_t)sh.Ci; a.Hi = (uint32_t)sh.Hi; a.Wi = (uint32_t)sh.Wi;
+    a.Kh = (uint32_t)sh.Kh; a.s = (uint32_t)sh.s; a.Ho = (uint32_t)sh.Ho;
+    a.L = (uint32_t)sh.L;
+    a.strips = (uint32_t)sh.strips;
+    a.win_elems = (uint64_t)sh.win_elems;
+    a.win_bytes = (uint64_t)sh.win_bytes;
+    a.pad_end = (uint64_t)sh.pad_end;
+    a.div_Ci = make_fastdiv((uint32_t)sh.Ci);
+    a.div_Kh = make_fastdiv((uint32_t)sh.Kh);
+    a.div_Wi = make_fastdiv((uint32_t)sh.Wi);
+    a.div_Ho = make_fastdiv((uint32_t)sh.Ho);
+    a.div_L = make_fastdiv((uint32_t)sh.L);
+    void *args[] = {&a};
+    const bool vec = (sh.Ci * sh.elt) % 16 == 0;
+    if (vec) {
+        a.gran_per_strip = (uint32_t)(sh.L * sh.elt / 16);
+        a.grans = 0;
+        const uint32_t per_block = kThreads * kGranPerThread;
+        dim3 grid((a.gran_per_strip + per_block - 1) / per_block, 1, 1);
+        // strips over y (<= 65535) and z
+        uint32_t gy = a.strips < 65535u ? a.strips : 65535u;
+        grid.y = gy;
+        grid.z = (a.strips + gy - 1) / gy;
+        const void *f = sh.elt == 4 ? (const void *)&transform_vec<4> : (const void *)&transform_vec<2>;
+        return hipLaunchKernel(f, grid, dim3(kThreads), args, 0, st);
+    }
+    // gather: element indices fit 32 bits (transform_range_ok)
+    a.gran_per_strip = 0;
+    a.grans = ((uint64_t)sh.win_bytes + 15) / 16;
+    const uint64_t blocks = (a.grans + kThreads - 1) / kThreads;
+    if (blocks > 0x7fffffffull)
+        return hipErrorInvalidValue;
+    const void *f = sh.elt == 4 ? (const void *)&transform_gather<4> : (const void *)&transform_gather<2>;
+    return hipLaunchKernel(f, dim3((uint32_t)blocks), dim3(kThreads), args, 0, st);
+}
+
+}  // namespace im2win

@@ -1,0 +1,159 @@
+"""The C-ABI library on the host: it loads, exports every function the header
+declares, and its host-only functions and argument checks behave as the header
+states.  No call here reaches a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_20725_amd as pkg
+from paper_2608_20725_amd import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "im2win.h")
+
+OK, EINVAL, EALIGN, ERANGE, ENODEV, ELAUNCH, EWORKSPACE, EOVERLAP, EBUFFER = 0, -1, -2, -3, -4, -5, -6, -7, -8
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(pkg.library_path()):
+        from paper_2608_20725_amd import build
+        build.build()
+    return pkg.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(conv_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("conv_im2win_transform", "conv_im2win_fp32", "conv_im2win_fp16",
+              "conv_workspace_bytes"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_library_exports_nothing_undeclared(lib):
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", pkg.library_path()],
+                         capture_output=True, text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    ours = {n for n in exported if n.startswith("conv_")}
+    assert ours == set(declared_functions())
+
+
+def _closed_form(l, elt, fp16):
+    Ho = (l.H - l.K_h) // l.stride + 1
+    Wo = (l.W - l.K_w) // l.stride + 1
+    win = l.N * Ho * l.W * l.K_h * l.C_i * elt
+    pad_end = (win + 255) // 256 * 256 + 256
+    K = l.K_h * l.K_w * l.C_i
+    packed = ((l.C_o + 127) // 128 * 128) * ((K + 63) // 64 * 64) * 2 if fp16 else 0
+    im2col = l.N * Ho * Wo * K * elt
+    return pad_end + packed, im2col, win
+
+
+@pytest.mark.parametrize("layer", workloads.ALL, ids=lambda l: l.name)
+def test_workspace_and_im2col_bytes(lib, layer, orc):
+    for dt, elt in ((pkg.F32, 4), (pkg.F16, 2)):
+        ws, im2col, win = _closed_form(layer, elt, dt == pkg.F16)
+        args = (layer.N, layer.C_i, layer.H, layer.W, layer.C_o, layer.K_h, layer.K_w, layer.stride)
+        assert pkg.conv_workspace_bytes(*args, dt) == ws
+        assert pkg.conv_im2col_bytes(layer.N, layer.C_i, layer.H, layer.W, layer.K_h, layer.K_w,
+                                     layer.stride, dt) == im2col
+        # the oracle counts the same two tensors from their index ranges
+        assert win == elt * orc.window_elems(layer.N, layer.C_i, layer.H, layer.W, layer.K_h,
+                                             layer.stride)
+        assert im2col == elt * orc.im2col_elems(layer.N, layer.C_i, layer.H, layer.W, layer.K_h,
+                                                layer.K_w, layer.stride)
+        # the window tensor is smaller than im2col whenever windows overlap
+        if layer.K_w > layer.stride:
+            assert win < im2col
+        else:
+            assert win == im2col
+
+
+def test_output_dims_table1(lib):
+    from oracle_checks import read_table
+    for row in read_table("table1_layers.txt"):
+        _, ci, hi, wi, co, hf, wf, s, oc, ho, wo = map(lambda v: int(v) if v.isdigit() else v, row)
+        assert pkg.conv_output_dims(hi, wi, hf, wf, s) == (ho, wo)
+
+
+@pytest.mark.parametrize("args", [
+    (0, 3, 8, 8, 4, 3, 3, 1), (1, 0, 8, 8, 4, 3, 3, 1), (1, 3, 8, 8, 0, 3, 3, 1),
+    (1, 3, 8, 8, 4, 9, 3, 1), (1, 3, 8, 8, 4, 3, 9, 1), (1, 3, 8, 8, 4, 3, 3, 0),
+    (1, 3, 8, 8, 4, -1, 3, 1), (-2, 3, 8, 8, 4, 3, 3, 1),
+])
+def test_workspace_rejects_bad_dims(lib, args):
+    assert lib.conv_workspace_bytes(*args, pkg.F32) == EINVAL
+
+
+def test_workspace_rejects_bad_dtype(lib):
+    assert lib.conv_workspace_bytes(1, 3, 8, 8, 4, 3, 3, 1, 7) == EINVAL
+
+
+def test_ranges(lib):
+    # strip W_i*K_h*C_i must stay below 2^20 elements
+    assert lib.conv_workspace_bytes(1, 1 << 12, 300, 300, 4, 1, 1, 1, pkg.F32) == ERANGE
+    # K_h*K_w*C_i below 2^24
+    assert lib.conv_workspace_bytes(1, 1 << 20, 4, 4, 4, 4, 4, 1, pkg.F32) == ERANGE
+    # C_o below 2^19
+    assert lib.conv_workspace_bytes(1, 3, 8, 8, 1 << 19, 3, 3, 1, pkg.F32) == ERANGE
+    # more than 2^31 output pixels
+    assert lib.conv_workspace_bytes(1 << 20, 1, 64, 64, 1, 1, 1, 1, pkg.F32) == ERANGE
+
+
+def test_output_dims_rejects(lib):
+    ho, wo = ctypes.c_int64(), ctypes.c_int64()
+    assert lib.conv_output_dims(8, 8, 9, 3, 1, ctypes.byref(ho), ctypes.byref(wo)) == EINVAL
+    assert lib.conv_output_dims(8, 8, 3, 3, 0, ctypes.byref(ho), ctypes.byref(wo)) == EINVAL
+    assert lib.conv_output_dims(8, 8, 3, 3, 1, None, ctypes.byref(wo)) == EINVAL
+
+
+def test_null_pointers_rejected_first(lib):
+    v = ctypes.c_void_p
+    # null pointers win over bad dims
+    assert lib.conv_im2win_transform(None, v(256), 1 << 20, 0, 3, 8, 8, 4, 3, 3, 1, 0, None) == EINVAL
+    assert lib.conv_im2win_fp32(v(256), 1 << 20, None, v(512), 1, 3, 8, 8, 4, 3, 3, 1, None) == EINVAL
+    assert lib.conv_im2win_fp16(v(256), 1 << 20, v(512), None, 1, 3, 8, 8, 4, 3, 3, 1, None) == EINVAL
+
+
+def test_misaligned_pointers_rejected(lib):
+    v = ctypes.c_void_p
+    assert lib.conv_im2win_transform(v(0x1008), v(0x100000), 1 << 20, 1, 3, 8, 8, 4, 3, 3, 1, 0,
+                                     None) == EALIGN
+    assert lib.conv_im2win_fp32(v(0x100000), 1 << 20, v(0x2004), v(0x3000), 1, 3, 8, 8, 4, 3, 3, 1,
+                                None) == EALIGN
+    assert lib.conv_im2win_fp16(v(0x100000), 1 << 20, v(0x2000), v(0x3002), 1, 3, 8, 8, 4, 3, 3, 1,
+                                None) == EALIGN
+
+
+def test_dims_checked_before_pointers_resolve(lib):
+    v = ctypes.c_void_p
+    assert lib.conv_im2win_fp32(v(0x100000), 1 << 20, v(0x2000), v(0x3000), 1, 3, 8, 8, 4, 9, 3, 1,
+                                None) == EINVAL
+    assert lib.conv_im2win_transform(v(0x1000), v(0x100000), 1 << 20, 1, 3, 8, 8, 4, 3, 3, 1, 5,
+                                     None) == EINVAL
+
+
+def test_strerror(lib):
+    for code in (OK, EINVAL, EALIGN, ERANGE, ENODEV, ELAUNCH, EWORKSPACE, EOVERLAP, EBUFFER):
+        assert pkg.conv_im2win_strerror(code)
+    assert pkg.conv_im2win_strerror(12345) == "unknown status"
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(pkg, "_lib", None)
+    monkeypatch.setattr(pkg, "_LIB_PATH", str(tmp_path / "nope.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        pkg.load_library()

@@ -1,0 +1,135 @@
+"""fp32 (vector ALU) and fp16 (MFMA, fp32 accumulation) windowed convolution
+on the GPU against the fp64 oracle.
+
+Bar: max over outputs of |y - O| / sum|x||w| <= 1e-5 (fp32) and <= 2e-3
+(fp16, oracle on the fp16-rounded inputs); where sum|x||w| = 0 the output
+must be exactly 0.  Integer-valued inputs must match bit for bit.  Outputs
+are NaN-poisoned before each call (every element must be written) and
+guarded on both sides (nothing written outside)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import Run, TOL, check_full, check_sampled, oracle_inputs, rel_err, say
+from oracle_checks import TINY
+from paper_2608_20725_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+DTYPES = [torch.float32, torch.float16]
+DT_IDS = ["f32", "f16"]
+
+# (N, C_i, H, W, C_o, K_h, K_w, s): tiles with ragged tails in pixels, taps
+# and channels; C_o below, at and above one wave's 16 channels and the MFMA
+# tile sizes; windows that are and are not 16-byte aligned; K_h != K_w;
+# s > K; 1x1; filter as large as the input.
+EDGE = list(TINY) + [
+    (1, 3, 32, 32, 16, 3, 3, 1),      # cfg1 shape
+    (2, 8, 17, 19, 10, 3, 2, 1),      # C_o < 16
+    (1, 16, 15, 23, 17, 2, 3, 2),     # C_o = 16 + 1
+    (3, 4, 13, 11, 33, 3, 3, 1),      # C_o = 32 + 1
+    (1, 32, 12, 12, 100, 3, 3, 1),    # C_o = 100
+    (2, 24, 9, 9, 130, 3, 3, 2),      # C_o = 128 + 2
+    (1, 64, 10, 10, 64, 1, 1, 1),     # 1x1
+    (2, 7, 9, 9, 40, 9, 9, 1),        # filter = input: one output pixel per image
+    (2, 5, 20, 20, 24, 2, 2, 3),      # s > K
+    (1, 12, 30, 30, 48, 5, 4, 2),
+    (1, 96, 14, 14, 256, 5, 5, 1),    # cv5-like, K = 2400 (ragged for 64-tap stages)
+    (5, 3, 40, 37, 96, 11, 11, 4),    # stem-like, K = 363
+    (1, 130, 6, 6, 20, 3, 3, 1),      # K = 1170
+    (300, 1, 3, 3, 5, 2, 2, 1),       # many tiny images: tiles span many strips
+]
+
+
+def _id(t):
+    return "x".join(map(str, t))
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=DT_IDS)
+@pytest.mark.parametrize("shape", EDGE, ids=_id)
+def test_conv_edge_shapes(shape, dtype):
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    say("conv", shape, dtype)
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=7 + sum(shape))
+    run = Run(x, w, s, dtype)
+    check_full(run, x, w)
+    run.check_out_guards()
+    run.check_workspace_guard()
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=DT_IDS)
+@pytest.mark.parametrize("shape", EDGE[-9:], ids=_id)
+def test_conv_integer_inputs_exact(shape, dtype):
+    """Inputs in {-2..2}: every partial sum is an integer below 2^24, so any
+    summation order gives the exact result."""
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    say("conv int", shape, dtype)
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=11, dist="int2")
+    run = Run(x, w, s, dtype)
+    ref = oracle.conv(x.double().numpy(), w.double().numpy(), s)
+    if dtype == torch.float16:
+        ref = ref.astype(np.float16).astype(np.float64)   # the one rounding on store
+    assert np.array_equal(run.out_np(), ref)
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=DT_IDS)
+@pytest.mark.parametrize("layer", workloads.ALL, ids=lambda l: l.name)
+def test_conv_layers_small_batch(layer, dtype):
+    """Every configured layer shape with batch 2, all outputs checked."""
+    say("conv N=2", layer.name, dtype)
+    x, w = workloads.draw_layer(layer, N=min(2, layer.N))
+    run = Run(x, w, layer.stride, dtype)
+    check_full(run, x, w)
+    run.check_out_guards()
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=DT_IDS)
+@pytest.mark.parametrize("layer", workloads.ALL, ids=lambda l: l.name)
+def test_conv_layers_full_batch_sampled(layer, dtype):
+    """Every configured layer at its full batch, in the launch configuration
+    the benchmark times: all outputs of images 0 and N-1 (when affordable) and
+    4096 random outputs, each against the oracle."""
+    say("conv full", layer.name, dtype)
+    x, w = workloads.draw_layer(layer)
+    run = Run(x, w, layer.stride, dtype)
+    r, n = check_sampled(run, x, w, seed=layer.seed)
+    say("  max rel err %.3g over %d outputs" % (r, n))
+    run.check_out_guards()
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=DT_IDS)
+def test_conv_deterministic(dtype):
+    layer = workloads.CFG2
+    say("determinism", dtype)
+    x, w = workloads.draw_layer(layer, N=4)
+    run = Run(x, w, layer.stride, dtype)
+    first = run.out.clone()
+    run.rerun_conv()
+    assert torch.equal(first.view(torch.int16 if dtype == torch.float16 else torch.int32),
+                       run.out.view(torch.int16 if dtype == torch.float16 else torch.int32))
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=DT_IDS)
+def test_conv_on_side_stream(dtype):
+    shape = (3, 16, 14, 14, 48, 3, 3, 1)
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    say("side stream", dtype)
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=5)
+    st = torch.cuda.Stream()
+    with torch.cuda.stream(st):
+        run = Run(x, w, s, dtype, stream=st)
+    st.synchronize()
+    check_full(run, x, w)
+
+
+def test_fp16_rounding_once():
+    """Output rounding: the fp16 result of a dot product whose exact value is
+    representable is that value."""
+    x = torch.zeros(1, 1, 1, 64)
+    w = torch.zeros(1, 1, 64, 16)
+    x[0, 0, 0, :] = torch.arange(64) % 5 - 2
+    w[0, 0, :, :] = (torch.arange(64 * 16).reshape(64, 16) % 7 - 3).float()
+    run = Run(x, w, 1, torch.float16)
+    ref = oracle.conv(x.double().numpy(), w.double().numpy(), 1)
+    assert np.array_equal(run.out_np(), ref)
