@@ -56,8 +56,8 @@ struct Stage {
     static constexpr int NT = 64 * WAVES;
     // VEC: float4 granules of the [BM][KC] stage; else single floats
     static constexpr int ITEMS = VEC ? (BM * KC / 4 + NT - 1) / NT : (BM * KC + NT - 1) / NT;
-    float4 v4[VEC ? ITEMS : 1];
-    float v1[VEC ? 1 : ITEMS];
+    u32x4 v4[VEC ? ITEMS : 1];
+    uint32_t v1[VEC ? 1 : ITEMS];
 
     // Masked-off loads (pixel past P, tap past K) use an out-of-range offset
     // and read zero: no branches, and no access leaves the window tensor.
@@ -72,9 +72,7 @@ struct Stage {
                 const uint32_t row = (f >> 2) & (BM - 1), kq = f & 3;
                 const uint32_t k = k0 + 4 * kq;
                 const bool ok = f < BM * KC / 4 && p0 + row < a.P && k < a.K;
-                const u32x4 x = ld_b128(rs, ok ? (rowoff[row] + k) * 4u : kOOB);
-                v4[j] = make_float4(__builtin_bit_cast(float, x[0]), __builtin_bit_cast(float, x[1]),
-                                    __builtin_bit_cast(float, x[2]), __builtin_bit_cast(float, x[3]));
+                v4[j] = ld_b128(rs, ok ? (rowoff[row] + k) * 4u : kOOB);
             }
         } else {
 #pragma unroll
@@ -83,7 +81,7 @@ struct Stage {
                 const uint32_t row = (f >> 4) & (BM - 1), kk = f & 15;
                 const uint32_t k = k0 + kk;
                 const bool ok = f < BM * KC && p0 + row < a.P && k < a.K;
-                v1[j] = __builtin_bit_cast(float, ld_b32(rs, ok ? (rowoff[row] + k) * 4u : kOOB));
+                v1[j] = ld_b32(rs, ok ? (rowoff[row] + k) * 4u : kOOB);
             }
         }
     }
@@ -96,11 +94,12 @@ struct Stage {
             for (int j = 0; j < ITEMS; ++j) {
                 const uint32_t f = tid + j * NT;
                 if (f < BM * KC / 4) {
+                    // element by value: taking the bits of a vector element
+                    // through its address is not reliable with this compiler
                     const uint32_t row = f >> 2, kq = f & 3;
-                    As[4 * kq + 0][row] = v4[j].x;
-                    As[4 * kq + 1][row] = v4[j].y;
-                    As[4 * kq + 2][row] = v4[j].z;
-                    As[4 * kq + 3][row] = v4[j].w;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        As[4 * kq + e][row] = __uint_as_float(v4[j][e]);
                 }
             }
         } else {
@@ -108,7 +107,7 @@ struct Stage {
             for (int j = 0; j < ITEMS; ++j) {
                 const uint32_t f = tid + j * NT;
                 if (f < BM * KC)
-                    As[f & 15][f >> 4] = v1[j];
+                    As[f & 15][f >> 4] = __uint_as_float(v1[j]);
             }
         }
     }
