@@ -19,6 +19,9 @@
 // once (nearest-even) and stores NHWC.
 #include "common.hpp"
 
+#include <stdlib.h>
+#include <string.h>
+
 namespace im2win {
 namespace {
 
@@ -77,6 +80,44 @@ __global__ __launch_bounds__(256) void pack_filter_fp16(PackArgs a)
             w[e / 2] = lo | (hi << 16);
         }
         *reinterpret_cast<uint4 *>(a.packed + g * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+}
+
+// Epilogue shared by both kernels.  D[ch][px] of one wave: lane holds pixel
+// pbase + 32*j + (lane & 31) and, for accumulator element e of block (i, j),
+// channel chbase + 32*i + 8*(e/4) + 4*(lane/32) + e%4.  Each sum is rounded to
+// fp16 once (nearest-even) and four consecutive channels go out as 8 bytes.
+template <int WM, int WN>
+__device__ inline void store_tile(const floatx16 (&acc)[WM][WN], const C16Args &a, uint32_t pbase,
+                                  uint32_t chbase, uint32_t lane)
+{
+#pragma unroll
+    for (int j = 0; j < WN; ++j) {
+        const uint32_t p = pbase + 32 * j + (lane & 31);
+        if (p >= a.P)
+            continue;
+        uint16_t *o = a.out + (uint64_t)p * a.Co;
+#pragma unroll
+        for (int i = 0; i < WM; ++i) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const uint32_t c = chbase + 32 * i + 8 * g + 4 * (lane >> 5);
+                uint32_t h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const _Float16 v = (_Float16)acc[i][j][4 * g + e];
+                    h[e] = __builtin_bit_cast(uint16_t, v);
+                }
+                if (c + 3 < a.Co && (a.Co & 3) == 0) {
+                    *reinterpret_cast<uint2 *>(o + c) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (c + e < a.Co)
+                            o[c + e] = (uint16_t)h[e];
+                }
+            }
+        }
     }
 }
 
@@ -223,49 +264,267 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
         __syncthreads();
     }
 
-    // D[ch][px]: lane holds px = lane & 31 of its block and, for accumulator
-    // element e, channel 8*(e/4) + 4*(lane/32) + e%4.
+    store_tile<WM, WN>(acc, a, p0 + wn * 32 * WN, ch0 + wm * 32 * WM, lane);
+}
+
+// ---------------------------------------------------------------------------
+// Pipelined kernel for 16-byte-aligned windows (C_i a multiple of 8).
+//
+// A stage holds 64 taps of the workgroup's BMc filter rows and BNp window
+// rows, 128 bytes per row, in LDS.  Stages are fetched with
+// buffer_load_dwordx4 ... lds, which writes each lane's 16 bytes straight to
+// LDS at base + 16 * lane: one wave instruction fills 8 consecutive rows.  An
+// NSTAGE-deep ring keeps NSTAGE-1 stages in flight while the matrix cores
+// work on the current one (the double buffering and asynchronous copy of
+// Alg. 1, with a deeper ring because HBM latency on this part is long
+// compared with one stage of MFMA work).  Rows past the last pixel and taps
+// past K use an out-of-range offset, for which the load writes zeros.
+//
+// LDS rows are XOR-swizzled: 16-byte chunk c of row r sits in slot c ^ (r & 7),
+// so the 8 lanes that read one chunk of 8 consecutive rows for an MFMA
+// operand touch 8 different slots (all 32 banks).
+template <int WM, int WN, int WGM, int WGN, int NSTAGE>
+struct PipeCfg {
+    static_assert(WGM * WGN == 4, "four waves per workgroup");
+    static constexpr int BMc = 32 * WM * WGM;
+    static constexpr int BNp = 32 * WN * WGN;
+    static constexpr int ROWS = BMc + BNp;
+    static constexpr int STAGE = ROWS * 128;  // bytes per stage
+    static constexpr int BLOCKS = ROWS / 8;   // 8-row (1 KiB) blocks per stage
+    static_assert(BLOCKS % 4 == 0, "blocks split evenly over the four waves");
+    static constexpr int I = BLOCKS / 4;      // load instructions per wave per stage
+    static_assert((NSTAGE - 2) * I <= 63, "vmcnt range");
+    static constexpr int LDS = NSTAGE * STAGE;
+};
+
+template <int VM>
+__device__ inline void wait_vmcnt()
+{
+    // s_waitcnt with vmcnt = VM, expcnt and lgkmcnt left alone
+    __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+typedef __attribute__((address_space(3))) void *lds_ptr;
+
+// Workgroup barrier for the ring.  __syncthreads() carries a release fence
+// that waits for every outstanding memory operation, including the stages
+// still in flight, which would collapse the ring to one stage; the explicit
+// vmcnt wait before it already covers the stage about to be read.  The empty
+// asm statements keep the compiler from moving LDS accesses across it.
+__device__ inline void ring_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// State of one workgroup of the pipelined kernel.  Ring slots are separate
+// LDS arrays and every step of the main loop names its slot at compile time,
+// so the compiler can tell that reading one slot does not depend on the
+// loads still landing in the others (and inserts no wait for them).
+template <int WM, int WN, int WGM, int WGN, int NSTAGE>
+struct Pipe {
+    using C = PipeCfg<WM, WN, WGM, WGN, NSTAGE>;
+    __amdgpu_buffer_rsrc_t rf, rw;
+    uint32_t voff[C::I];    // byte offset of this lane's chunk at tap 0 (kOOB: no pixel)
+    uint32_t vchunk[C::I];  // first tap of this lane's chunk within a stage
+    uint32_t wave, lane, K, nst;
+    uint32_t arow, brow, sw;
+    floatx16 acc[WM][WN];
+
+    // Stage s >= nst (past the end of K) loads nothing: every offset is out of
+    // range and the slot is filled with zeros.
+    __device__ inline void issue(uint32_t s, char *stage)
+    {
+        const uint32_t k0 = s * BK;
+        const bool tail = k0 + BK > K;
+        const bool past = s >= nst;
 #pragma unroll
-    for (int j = 0; j < WN; ++j) {
-        const uint32_t p = p0 + wn * 32 * WN + 32 * j + (lane & 31);
-        if (p >= a.P)
-            continue;
-        uint16_t *o = a.out + (uint64_t)p * a.Co;
-#pragma unroll
-        for (int i = 0; i < WM; ++i) {
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const uint32_t c = ch0 + wm * 32 * WM + 32 * i + 8 * g + 4 * (lane >> 5);
-                _Float16 h[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    h[e] = (_Float16)acc[i][j][4 * g + e];
-                if (c + 3 < a.Co && (a.Co & 3) == 0) {
-                    uint2 v;
-                    v.x = (uint32_t)__builtin_bit_cast(uint16_t, h[0]) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, h[1]) << 16);
-                    v.y = (uint32_t)__builtin_bit_cast(uint16_t, h[2]) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, h[3]) << 16);
-                    *reinterpret_cast<uint2 *>(o + c) = v;
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (c + e < a.Co)
-                            o[c + e] = __builtin_bit_cast(uint16_t, h[e]);
-                }
-            }
+        for (int j = 0; j < C::I; ++j) {
+            const uint32_t b = wave + 4 * j;
+            const bool filt = b < (uint32_t)C::BMc / 8;
+            uint32_t off = voff[j] + 2u * k0;
+            if (past || (!filt && tail && k0 + vchunk[j] >= K))
+                off = kOOB;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(filt ? rf : rw, (lds_ptr)(stage + 1024 * b), 16, off,
+                                                     0, 0, 0);
         }
     }
+
+    __device__ inline void compute(const char *stage)
+    {
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            const uint32_t cofs = 16u * ((2 * ks + (lane >> 5)) ^ sw);
+            half8 af[WM], bf[WN];
+#pragma unroll
+            for (int i = 0; i < WM; ++i)
+                af[i] = *reinterpret_cast<const half8 *>(stage + (arow + 32 * i) * 128 + cofs);
+#pragma unroll
+            for (int j = 0; j < WN; ++j)
+                bf[j] = *reinterpret_cast<const half8 *>(stage + (brow + 32 * j) * 128 + cofs);
+#pragma unroll
+            for (int i = 0; i < WM; ++i)
+#pragma unroll
+                for (int j = 0; j < WN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+        }
+    }
+
+    // Stage st sits in slot `cur`: wait for it, then refill the slot freed by
+    // stage st-1 (`next`) with stage st+NSTAGE-1, then multiply.  Every step
+    // waits for the same count and issues one stage, so the wait is exact
+    // without branches; only the multiply is skipped past the last stage.
+    // The slots are passed as the LDS arrays themselves so that, once
+    // inlined, every access names its array.
+    template <int N>
+    __device__ inline void step(uint32_t st, char (&cur)[N], char (&next)[N])
+    {
+        wait_vmcnt<(NSTAGE - 2) * C::I>();
+        ring_barrier();
+        issue(st + NSTAGE - 1, next);
+        if (st < nst)
+            compute(cur);
+    }
+};
+
+template <int WM, int WN, int WGM, int WGN, int NSTAGE>
+__global__ __launch_bounds__(256) void conv_fp16_pipe(C16Args a)
+{
+    using C = PipeCfg<WM, WN, WGM, WGN, NSTAGE>;
+    static_assert(NSTAGE >= 2 && NSTAGE <= 4, "ring depth");
+    constexpr int S2 = NSTAGE > 2 ? C::STAGE : 1024, S3 = NSTAGE > 3 ? C::STAGE : 1024;
+    __shared__ __attribute__((aligned(1024))) char r0[C::STAGE];
+    __shared__ __attribute__((aligned(1024))) char r1[C::STAGE];
+    __shared__ __attribute__((aligned(1024))) char r2[S2];
+    __shared__ __attribute__((aligned(1024))) char r3[S3];
+    __shared__ uint32_t rowoff[C::BNp];
+
+    Pipe<WM, WN, WGM, WGN, NSTAGE> w;
+    const uint32_t tid = threadIdx.x;
+    w.lane = tid & 63;
+    w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    w.K = a.K;
+    w.nst = a.K_pad / BK;
+    const uint32_t wm = w.wave / WGN, wn = w.wave % WGN;
+    const uint32_t p0 = blockIdx.x * C::BNp;
+    const uint32_t ch0 = blockIdx.y * C::BMc;
+
+    const uint32_t q0 = fdiv(p0, a.div_Wo);
+    const uint64_t tb_elem = (uint64_t)q0 * a.L;
+    const uint64_t left = a.win_bytes - tb_elem * 2;
+    w.rw = make_rsrc(a.ws + tb_elem, (uint32_t)(left < kMaxRecords ? left : kMaxRecords));
+    w.rf = make_rsrc(a.packed + (uint64_t)ch0 * a.K_pad, (uint32_t)C::BMc * a.K_pad * 2u);
+    for (uint32_t t = tid; t < C::BNp; t += 256) {
+        const uint32_t p = p0 + t;
+        uint32_t off = 0;
+        if (p < a.P) {
+            const uint32_t q = fdiv(p, a.div_Wo);
+            off = (q - q0) * a.L + (p - q * a.Wo) * a.S;
+        }
+        rowoff[t] = off;
+    }
+    __syncthreads();
+
+    // Lane L of a load instruction fills LDS slot L & 7 of row 8*block + L/8
+    // with 16-byte chunk (L & 7) ^ (row & 7) of that row.
+    const uint32_t rib = w.lane >> 3, slot = w.lane & 7;
+#pragma unroll
+    for (int j = 0; j < C::I; ++j) {
+        const uint32_t b = w.wave + 4 * j;
+        if (b < (uint32_t)C::BMc / 8) {
+            const uint32_t row = 8 * b + rib;
+            const uint32_t c = slot ^ (row & 7);
+            w.voff[j] = row * a.K_pad * 2u + 16u * c;
+            w.vchunk[j] = 8 * c;
+        } else {
+            const uint32_t row = 8 * (b - C::BMc / 8) + rib;
+            const uint32_t c = slot ^ (row & 7);
+            w.voff[j] = (p0 + row < a.P) ? rowoff[row] * 2u + 16u * c : kOOB;
+            w.vchunk[j] = 8 * c;
+        }
+    }
+    w.arow = wm * 32 * WM + (w.lane & 31);
+    w.brow = C::BMc + wn * 32 * WN + (w.lane & 31);
+    w.sw = w.lane & 7;  // row & 7 of every row this lane reads
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                w.acc[i][j][e] = 0.f;
+
+    // prologue: stages 0 .. NSTAGE-2 into slots 0 .. NSTAGE-2, then stage st
+    // in slot st % NSTAGE
+    w.issue(0, r0);
+    if constexpr (NSTAGE == 2) {
+        for (uint32_t st = 0; st < w.nst; st += 2) {
+            w.step(st, r0, r1);
+            w.step(st + 1, r1, r0);
+        }
+    } else if constexpr (NSTAGE == 3) {
+        w.issue(1, r1);
+        for (uint32_t st = 0; st < w.nst; st += 3) {
+            w.step(st, r0, r2);
+            w.step(st + 1, r1, r0);
+            w.step(st + 2, r2, r1);
+        }
+    } else {
+        w.issue(1, r1);
+        w.issue(2, r2);
+        for (uint32_t st = 0; st < w.nst; st += 4) {
+            w.step(st, r0, r3);
+            w.step(st + 1, r1, r0);
+            w.step(st + 2, r2, r1);
+            w.step(st + 3, r3, r2);
+        }
+    }
+    // no load may still be writing LDS when the workgroup ends
+    wait_vmcnt<0>();
+
+    store_tile<WM, WN>(w.acc, a, p0 + wn * 32 * WN, ch0 + wm * 32 * WM, w.lane);
 }
 
 template <int WM, int WN, int WGM, int WGN>
-void pick(bool aligned, const void **f, int *nt, int *bm, int *bn)
+void pick_regs(bool aligned, const void **f, int *bm, int *bn)
 {
     *f = aligned ? (const void *)&conv_fp16_kernel<WM, WN, WGM, WGN, true>
                  : (const void *)&conv_fp16_kernel<WM, WN, WGM, WGN, false>;
-    *nt = 64 * WGM * WGN;
     *bm = 32 * WM * WGM;
     *bn = 32 * WN * WGN;
+}
+
+struct PipeVariant {
+    const char *name;
+    const void *f;
+    int bm, bn;
+};
+
+template <int WM, int WN, int WGM, int WGN, int NS>
+PipeVariant pipe_variant(const char *name)
+{
+    return PipeVariant{name, (const void *)&conv_fp16_pipe<WM, WN, WGM, WGN, NS>, 32 * WM * WGM,
+                       32 * WN * WGN};
+}
+
+// Tile shapes of the pipelined kernel: channels x pixels per workgroup,
+// ring depth.
+const PipeVariant *pipe_variants(int *n)
+{
+    static const PipeVariant v[] = {
+        pipe_variant<1, 2, 1, 4, 4>("c32p256s4"),
+        pipe_variant<1, 1, 1, 4, 3>("c32p128s3"),
+        pipe_variant<2, 2, 1, 4, 3>("c64p256s3"),
+        pipe_variant<1, 2, 2, 2, 3>("c64p128s3"),
+        pipe_variant<2, 2, 2, 2, 4>("c128p128s4"),
+        pipe_variant<2, 2, 2, 2, 2>("c128p128s2"),
+        pipe_variant<2, 4, 2, 2, 3>("c128p256s3"),
+        pipe_variant<4, 2, 1, 4, 2>("c128p256s2w"),
+        pipe_variant<2, 4, 2, 2, 2>("c128p256s2"),
+    };
+    *n = (int)(sizeof v / sizeof v[0]);
+    return v;
 }
 
 }  // namespace
@@ -296,18 +555,34 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
     a.P = (uint32_t)sh.P; a.K = (uint32_t)sh.K; a.K_pad = (uint32_t)sh.K_pad;
     a.Co = (uint32_t)sh.Co; a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.S = (uint32_t)sh.S;
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
-    const bool aligned = (sh.Ci % 8) == 0;  // every window starts on a 16-byte boundary
-    const void *f;
-    int nt, bm, bn;
-    if (sh.Co <= 32)
-        pick<1, 2, 1, 4>(aligned, &f, &nt, &bm, &bn);
-    else if (sh.Co <= 64)
-        pick<2, 2, 1, 4>(aligned, &f, &nt, &bm, &bn);
-    else
-        pick<2, 2, 2, 2>(aligned, &f, &nt, &bm, &bn);
-    dim3 grid((uint32_t)((sh.P + bn - 1) / bn), (uint32_t)((sh.Co + bm - 1) / bm));
     void *args[] = {&a};
-    return hipLaunchKernel(f, grid, dim3(nt), args, 0, st);
+    const bool aligned = (sh.Ci % 8) == 0;  // every window starts on a 16-byte boundary
+    if (aligned) {
+        int n;
+        const PipeVariant *v = pipe_variants(&n);
+        // Shapes that leave LDS for two workgroups per CU measured fastest on
+        // every layer tried (latency hiding beats ring depth).
+        int pick = sh.Co <= 32 ? 1 : sh.Co <= 64 ? 3 : 5;
+        // IM2WIN_FP16_TILE=<name> overrides the tile shape (for tuning).
+        if (const char *e = getenv("IM2WIN_FP16_TILE")) {
+            for (int t = 0; t < n; ++t)
+                if (strcmp(e, v[t].name) == 0)
+                    pick = t;
+        }
+        const PipeVariant &p = v[pick];
+        dim3 grid((uint32_t)((sh.P + p.bn - 1) / p.bn), (uint32_t)((sh.Co + p.bm - 1) / p.bm));
+        return hipLaunchKernel(p.f, grid, dim3(256), args, 0, st);
+    }
+    const void *f;
+    int bm, bn;
+    if (sh.Co <= 32)
+        pick_regs<1, 2, 1, 4>(false, &f, &bm, &bn);
+    else if (sh.Co <= 64)
+        pick_regs<2, 2, 1, 4>(false, &f, &bm, &bn);
+    else
+        pick_regs<2, 2, 2, 2>(false, &f, &bm, &bn);
+    dim3 grid((uint32_t)((sh.P + bn - 1) / bn), (uint32_t)((sh.Co + bm - 1) / bm));
+    return hipLaunchKernel(f, grid, dim3(256), args, 0, st);
 }
 
 }  // namespace im2win
