@@ -154,6 +154,9 @@ def main():
     ap.add_argument("--layer", default=None, help="configured layer name (default: cfg2)")
     ap.add_argument("--sweep", action="store_true", help="one line per configured layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES bytes (HBM counter "
+                         "calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the im2win path runs on a single MI355X here "
@@ -162,6 +165,14 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.calibrate_copy:
+        src = torch.ones(args.calibrate_copy // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(max(args.steps, 1)):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": src.numel() * 4, "copies": max(args.steps, 1)}), flush=True)
+        return
     import paper_2608_20725_amd as pkg
     from paper_2608_20725_amd import workloads
 

@@ -23,9 +23,12 @@
  *     [win, pad_end)  zero bytes, pad_end = round_up(win, 256) + 256; they let
  *                     the kernels read past the last window without leaving
  *                     the buffer
- *     [pad_end, ...)  fp16 only: the filter repacked as [C_o_pad][K_pad] fp16
- *                     in window order, zero-padded, C_o_pad = round_up(C_o, 128),
- *                     K_pad = round_up(K, 64); written by conv_im2win_fp16
+ *     [pad_end, ...)  the filter repacked in window order (tap k = (v*K_h+u)*C_i+r)
+ *                     and zero-padded, written by the conv call:
+ *                       fp16: [C_o_pad][K_pad] fp16, C_o_pad = round_up(C_o, 128),
+ *                             K_pad = round_up(K, 64)
+ *                       fp32: [K_pad32][C_o_pad32] fp32, K_pad32 = round_up(K, 16),
+ *                             C_o_pad32 = round_up(C_o, 32)
  *
  * Scope: one stride for both axes, no padding, dilation, groups or bias.
  *
@@ -78,8 +81,7 @@ int conv_output_dims(int64_t H_i, int64_t W_i, int64_t K_h, int64_t K_w, int64_t
 
 /*
  * Bytes of workspace the transform and the conv of this layer need (layout
- * above): the window tensor of Eq. 2 plus the 256-byte zero pad, plus, for
- * IM2WIN_F16, the packed filter.  Host only, no device calls.  Returns a
+ * above): the window tensor of Eq. 2, the zero pad and the packed filter.  Host only, no device calls.  Returns a
  * negative status for invalid arguments (IM2WIN_EINVAL, IM2WIN_ERANGE).
  *
  * Index ranges the kernels support (else IM2WIN_ERANGE): one strip
@@ -117,13 +119,15 @@ int conv_im2win_transform(const void *in_nhwc, void *ws, int64_t ws_bytes,
  * fp32 windowed convolution on the vector ALUs (Sec. III-C, Eq. 3; the
  * paper's CUDA-core variant, Sec. IV-A).
  *   ws              device, workspace holding the fp32 window tensor written
- *                   by conv_im2win_transform(..., IM2WIN_F32); read only
+ *                   by conv_im2win_transform(..., IM2WIN_F32); the window
+ *                   tensor is read, the packed-filter region is overwritten
  *   filt_khkwcico   device, fp32 filter F [K_h][K_w][C_i][C_o]; read only
  *   out_nhwc        device, fp32 output O [N][H_o][W_o][C_o]; every element
  *                   is written exactly once
- * Accumulation is fp32 fused multiply-add.
+ * Each output is one fp32 fused multiply-add chain over the window's taps in
+ * (filter column, filter row, channel) order.
  */
-int conv_im2win_fp32(const void *ws, int64_t ws_bytes, const float *filt_khkwcico,
+int conv_im2win_fp32(void *ws, int64_t ws_bytes, const float *filt_khkwcico,
                      float *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream);
 

@@ -61,16 +61,18 @@ int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_
     r.pad_end = round_up(r.win_bytes, kPad) + kPad;
     r.Co_pad = round_up(Co, 128);
     r.K_pad = round_up(r.K, 64);
+    r.K_pad32 = round_up(r.K, 16);
+    r.Co_pad32 = round_up(Co, 32);
     *sh = r;
     return IM2WIN_OK;
 }
 
-int64_t packed_filter_bytes(const Shape &sh) { return sh.Co_pad * sh.K_pad * 2; }
-
-int64_t workspace_bytes(const Shape &sh, int dt)
+int64_t packed_filter_bytes(const Shape &sh, int dt)
 {
-    return sh.pad_end + (dt == IM2WIN_F16 ? packed_filter_bytes(sh) : 0);
+    return dt == IM2WIN_F16 ? sh.Co_pad * sh.K_pad * 2 : sh.K_pad32 * sh.Co_pad32 * 4;
 }
+
+int64_t workspace_bytes(const Shape &sh, int dt) { return sh.pad_end + packed_filter_bytes(sh, dt); }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -197,7 +199,7 @@ int conv_im2win_transform(const void *in_nhwc, void *ws, int64_t ws_bytes, int64
     return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream));
 }
 
-int conv_im2win_fp32(const void *ws, int64_t ws_bytes, const float *filt_khkwcico,
+int conv_im2win_fp32(void *ws, int64_t ws_bytes, const float *filt_khkwcico,
                      float *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream)
 {
@@ -223,7 +225,10 @@ int conv_im2win_fp32(const void *ws, int64_t ws_bytes, const float *filt_khkwcic
         return IM2WIN_EWORKSPACE;
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
-    return launch_status(launch_conv_fp32(sh, ws, filt_khkwcico, out_nhwc, (hipStream_t)hip_stream));
+    void *packed = (char *)ws + sh.pad_end;
+    if ((rc = launch_status(launch_pack_fp32(sh, filt_khkwcico, packed, (hipStream_t)hip_stream))) != IM2WIN_OK)
+        return rc;
+    return launch_status(launch_conv_fp32(sh, ws, packed, out_nhwc, (hipStream_t)hip_stream));
 }
 
 int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,

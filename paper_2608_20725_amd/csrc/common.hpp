@@ -52,6 +52,8 @@ struct Shape {
     int64_t pad_end;    // end of the zero pad (bytes)
     int64_t Co_pad;     // packed fp16 filter rows
     int64_t K_pad;      // packed fp16 filter columns
+    int64_t K_pad32;    // packed fp32 filter rows (taps)
+    int64_t Co_pad32;   // packed fp32 filter columns (channels)
 };
 
 inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
@@ -97,7 +99,8 @@ namespace im2win {
 // The gather form of the transform indexes elements with 32 bits.
 bool transform_range_ok(const Shape &sh);
 hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st);
-hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const float *filt, float *out,
+hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hipStream_t st);
+hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed, float *out,
                             hipStream_t st);
 hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed, hipStream_t st);
 hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed, uint16_t *out,

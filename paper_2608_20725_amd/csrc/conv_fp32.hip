@@ -1,63 +1,95 @@
 // fp32 windowed convolution on the gfx950 vector ALUs (Sec. III-C, Eq. 3).
 //
-//   O[p][j] = sum_{k<K} Wn[p][k] * F[frow(k)][j]
+//   O[p][j] = sum_{k<K} Wn[p][k] * F'[k][j]
 //
 // Wn[p][.] is the window of output pixel p = (i, m, n): the contiguous span of
 // strip (i, m) starting at n*s*K_h*C_i, in (filter column v, filter row u,
-// channel r) order; frow(k) = (u*K_w + v)*C_i + r is the matching row of the
-// [K_h][K_w][C_i][C_o] filter, so no repacked filter is needed.
+// channel r) order.  F' is the filter repacked into the same tap order,
+// F'[(v*K_h + u)*C_i + r][j] = F[u][v][r][j] (the filter laid out height
+// before width, Sec. III-C), zero-padded to [K_pad32][C_o_pad32]: a tap's
+// filter row is one row of F' and consecutive taps are consecutive rows.
 //
 // Work split (wave64):
-//   * a workgroup owns 256 consecutive output pixels and WAVES*16 output
-//     channels; each wave owns 16 channels, each lane 4 consecutive pixels,
-//     so a lane keeps a 4 x 16 block of fp32 accumulators;
-//   * windows are staged through LDS 16 taps at a time, transposed to
-//     [tap][pixel] so that a lane fetches its 4 pixels with one 16-byte LDS
-//     read; stages are double-buffered: the global loads of stage t+1 are in
+//   * a workgroup owns 64*TM consecutive output pixels and WAVES*TN output
+//     channels; each wave owns TN channels and each lane TM consecutive
+//     pixels, so a lane keeps a TM x TN block of fp32 accumulators;
+//   * windows are staged through LDS KC taps at a time, transposed to
+//     [tap][pixel] so that a lane fetches its TM pixels with 16-byte LDS
+//     reads; stages are double-buffered: the global loads of stage t+1 are in
 //     flight while stage t is multiplied;
 //   * filter values are the same for every lane of a wave, so they are read
-//     with scalar loads into SGPRs and each multiply-add takes one operand from
-//     an SGPR: per tap a lane does 64 FMAs for one LDS read.
+//     with scalar loads into SGPRs and every multiply-add takes one operand
+//     from an SGPR: per tap a lane does TM*TN FMAs for TM/4 LDS reads and one
+//     scalar load, and the filter pointer advances by one row per tap.
 // The row offset of every pixel's window is computed once per workgroup (the
-// index precomputation of Sec. III-E).
+// index precomputation of Sec. III-E).  Taps past K read zero window values
+// (masked loads) against zero filter rows (padding): they add exactly 0.
 #include "common.hpp"
+
+#include <stdlib.h>
+#include <string.h>
 
 namespace im2win {
 namespace {
 
-constexpr int TM = 4;        // pixels per lane
-constexpr int TN = 16;       // channels per wave
-constexpr int KC = 16;       // taps per LDS stage
-constexpr int BM = 64 * TM;  // pixels per workgroup
-constexpr int LDA = BM + 4;  // floats per staged tap row
-
 struct C32Args {
     const float *ws;
-    const float *filt;
+    const float *packed;  // F' [K_pad32][Co_pad32]
     float *out;
     uint64_t win_bytes;
-    uint32_t P, K, Co, Ci, Kh, Kw, Wo, L, S, KhCi;
-    FastDiv div_Wo, div_Ci, div_KhCi;
+    uint32_t P, K, K_pad, Co, Co_pad, Wo, L, S;
+    FastDiv div_Wo;
 };
 
-// Filter row of window tap k = (v*K_h + u)*C_i + r, i.e. (u*K_w + v)*C_i + r.
-// k is wave-uniform, so this runs on the scalar unit, branch-free.
-__device__ inline uint32_t filter_row(uint32_t k, const C32Args &a)
+// ---------------------------------------------------------------------------
+// Filter repack: one thread per 4 consecutive channels of one tap row of F'.
+struct Pack32Args {
+    const float *filt;
+    float *packed;
+    uint64_t quads;
+    uint32_t K, Co, Co_pad, Ci, Kh, Kw;
+};
+
+__global__ __launch_bounds__(256) void pack_filter_fp32(Pack32Args a)
 {
-    const uint32_t v = fdiv(k, a.div_KhCi);
-    const uint32_t rem = k - v * a.KhCi;
-    const uint32_t u = fdiv(rem, a.div_Ci);
-    const uint32_t r = rem - u * a.Ci;
-    return (u * a.Kw + v) * a.Ci + r;
+    const uint32_t qpr = a.Co_pad / 4;  // quads per packed row
+    for (uint64_t g = (uint64_t)blockIdx.x * 256 + threadIdx.x; g < a.quads;
+         g += (uint64_t)gridDim.x * 256) {
+        const uint32_t k = (uint32_t)(g / qpr);
+        const uint32_t j0 = (uint32_t)(g % qpr) * 4;
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        if (k < a.K) {
+            const uint32_t khci = a.Kh * a.Ci;
+            const uint32_t vv = k / khci, rem = k % khci;
+            const uint32_t u = rem / a.Ci, r = rem % a.Ci;
+            const float *src = a.filt + (((uint64_t)u * a.Kw + vv) * a.Ci + r) * a.Co;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (j0 + e < a.Co)
+                    v[e] = src[j0 + e];
+        }
+        *reinterpret_cast<float4 *>(a.packed + g * 4) = make_float4(v[0], v[1], v[2], v[3]);
+    }
 }
 
-template <bool VEC, int WAVES>
-struct Stage {
+// ---------------------------------------------------------------------------
+template <int TM, int TN, int KC, int WAVES, bool V4>
+struct Geo {
+    static constexpr int BM = 64 * TM;      // pixels per workgroup
+    static constexpr int LDA = BM + 4;      // floats per staged tap row
     static constexpr int NT = 64 * WAVES;
-    // VEC: float4 granules of the [BM][KC] stage; else single floats
-    static constexpr int ITEMS = VEC ? (BM * KC / 4 + NT - 1) / NT : (BM * KC + NT - 1) / NT;
-    u32x4 v4[VEC ? ITEMS : 1];
-    uint32_t v1[VEC ? 1 : ITEMS];
+    // V4: float4 granules of the [BM][KC] stage; else single floats
+    static constexpr int ITEMS = V4 ? (BM * KC / 4 + NT - 1) / NT : (BM * KC + NT - 1) / NT;
+    static_assert(KC == 8 || KC == 16, "stage depth (the packed filter has 16-tap padding)");
+    static_assert(TM % 4 == 0, "pixels per lane in 16-byte LDS reads");
+    static_assert(TN % 16 == 0 && TN <= 32, "channels per wave (32-channel padding)");
+};
+
+template <int TM, int TN, int KC, int WAVES, bool V4>
+struct Stage {
+    using G = Geo<TM, TN, KC, WAVES, V4>;
+    u32x4 v4[V4 ? G::ITEMS : 1];
+    uint32_t v1[V4 ? 1 : G::ITEMS];
 
     // Masked-off loads (pixel past P, tap past K) use an out-of-range offset
     // and read zero: no branches, and no access leaves the window tensor.
@@ -65,38 +97,40 @@ struct Stage {
                                 uint32_t k0, const C32Args &a)
     {
         const uint32_t tid = threadIdx.x;
-        if (VEC) {
+        constexpr int Q = KC / 4;  // granules per row
+        if (V4) {
 #pragma unroll
-            for (int j = 0; j < ITEMS; ++j) {
-                const uint32_t f = tid + j * NT;
-                const uint32_t row = (f >> 2) & (BM - 1), kq = f & 3;
+            for (int j = 0; j < G::ITEMS; ++j) {
+                const uint32_t f = tid + j * G::NT;
+                const uint32_t row = (f / Q) % G::BM, kq = f % Q;
                 const uint32_t k = k0 + 4 * kq;
-                const bool ok = f < BM * KC / 4 && p0 + row < a.P && k < a.K;
+                const bool ok = f < G::BM * Q && p0 + row < a.P && k < a.K;
                 v4[j] = ld_b128(rs, ok ? (rowoff[row] + k) * 4u : kOOB);
             }
         } else {
 #pragma unroll
-            for (int j = 0; j < ITEMS; ++j) {
-                const uint32_t f = tid + j * NT;
-                const uint32_t row = (f >> 4) & (BM - 1), kk = f & 15;
+            for (int j = 0; j < G::ITEMS; ++j) {
+                const uint32_t f = tid + j * G::NT;
+                const uint32_t row = (f / KC) % G::BM, kk = f % KC;
                 const uint32_t k = k0 + kk;
-                const bool ok = f < BM * KC && p0 + row < a.P && k < a.K;
+                const bool ok = f < G::BM * KC && p0 + row < a.P && k < a.K;
                 v1[j] = ld_b32(rs, ok ? (rowoff[row] + k) * 4u : kOOB);
             }
         }
     }
 
-    __device__ inline void store(float (*As)[LDA])
+    __device__ inline void store(float (*As)[G::LDA])
     {
         const uint32_t tid = threadIdx.x;
-        if (VEC) {
+        constexpr int Q = KC / 4;
+        if (V4) {
 #pragma unroll
-            for (int j = 0; j < ITEMS; ++j) {
-                const uint32_t f = tid + j * NT;
-                if (f < BM * KC / 4) {
+            for (int j = 0; j < G::ITEMS; ++j) {
+                const uint32_t f = tid + j * G::NT;
+                if (f < G::BM * Q) {
                     // element by value: taking the bits of a vector element
                     // through its address is not reliable with this compiler
-                    const uint32_t row = f >> 2, kq = f & 3;
+                    const uint32_t row = f / Q, kq = f % Q;
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         As[4 * kq + e][row] = __uint_as_float(v4[j][e]);
@@ -104,105 +138,109 @@ struct Stage {
             }
         } else {
 #pragma unroll
-            for (int j = 0; j < ITEMS; ++j) {
-                const uint32_t f = tid + j * NT;
-                if (f < BM * KC)
-                    As[f & 15][f >> 4] = __uint_as_float(v1[j]);
+            for (int j = 0; j < G::ITEMS; ++j) {
+                const uint32_t f = tid + j * G::NT;
+                if (f < G::BM * KC)
+                    As[f % KC][f / KC] = __uint_as_float(v1[j]);
             }
         }
     }
 };
 
-// The 16 filter values of channels jw..jw+15 at one filter row: identical
-// for every lane, so they land in SGPRs (one s_load_dwordx16 when the wave's
-// channels are all valid).
-// The filter is read through the constant address space: the kernel never
-// writes it, and loads from that space with a uniform address become s_load.
+// The packed filter is read through the constant address space: the kernel
+// never writes it, and loads from that space with a uniform address become
+// s_load.
 typedef const __attribute__((address_space(4))) float cfloat;
 typedef float f32x16 __attribute__((ext_vector_type(16), aligned(4)));
 typedef const __attribute__((address_space(4))) f32x16 cf32x16;
 
-template <bool FULLCH>
-__device__ inline void load_filter(float (&f)[TN], uint32_t frow, const C32Args &a, uint32_t jw)
+// TN filter values of one packed row: identical for every lane, so they land
+// in SGPRs (one s_load_dwordx16 per 16 channels).
+template <int TN>
+__device__ inline void load_filter(float (&f)[TN], cfloat *fp)
 {
-    cfloat *fp = (cfloat *)a.filt + (uint64_t)frow * a.Co + jw;
-    if (FULLCH) {
-        const f32x16 v = *(cf32x16 *)fp;
 #pragma unroll
-        for (int c = 0; c < TN; ++c)
-            f[c] = v[c];
-    } else {
+    for (int h = 0; h < TN / 16; ++h) {
+        const f32x16 v = *(cf32x16 *)(fp + 16 * h);
 #pragma unroll
-        for (int c = 0; c < TN; ++c)
-            f[c] = fp[(jw + c < a.Co) ? c : 0];
+        for (int c = 0; c < 16; ++c)
+            f[16 * h + c] = v[c];
     }
 }
 
-__device__ inline void tap_fma(float (&acc)[TM][TN], const float4 x, const float (&f)[TN])
+template <int TM, int TN>
+__device__ inline void tap_fma(float (&acc)[TM][TN], const float (&x)[TM], const float (&f)[TN])
 {
-    const float xs[TM] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int t = 0; t < TM; ++t)
 #pragma unroll
         for (int c = 0; c < TN; ++c)
-            acc[t][c] = __builtin_fmaf(xs[t], f[c], acc[t][c]);
+            acc[t][c] = __builtin_fmaf(x[t], f[c], acc[t][c]);
+}
+
+template <int TM, int LDA>
+__device__ inline void read_pixels(float (&x)[TM], const float (*As)[LDA], int kk, uint32_t lane)
+{
+#pragma unroll
+    for (int q = 0; q < TM / 4; ++q) {
+        const float4 v = *reinterpret_cast<const float4 *>(&As[kk][TM * lane + 4 * q]);
+        x[4 * q + 0] = v.x;
+        x[4 * q + 1] = v.y;
+        x[4 * q + 2] = v.z;
+        x[4 * q + 3] = v.w;
+    }
 }
 
 // Waits for every outstanding LDS and scalar load (lgkmcnt = 0), leaving
 // vector-memory loads in flight.
 __device__ inline void wait_lgkm() { __builtin_amdgcn_s_waitcnt(0xc07f); }
 
-// Multiplies one LDS stage of `ntaps` (<= KC) taps starting at tap k0.  The
-// LDS read and the filter loads of tap kk+1 are issued before the 64 FMAs of
-// tap kk and waited for after them; the scheduling fence keeps the compiler
-// from hoisting further loads (which would exhaust the SGPRs).  The tap
-// guards are wave-uniform branches; full and partial stages share one body so
-// the accumulators stay in one set of registers.
-template <bool FULLCH>
-__device__ inline void stage_fma(float (&acc)[TM][TN], float (*As)[LDA], uint32_t k0,
-                                 uint32_t ntaps, const C32Args &a, uint32_t jc, uint32_t lane)
+// Multiplies one LDS stage of KC taps whose first packed filter row is `fp`.
+// The LDS reads and the filter loads of tap kk+1 are issued before the FMAs
+// of tap kk and waited for after them (scalar loads can return out of order,
+// so the only safe wait is for all of them); the scheduling fence keeps the
+// compiler from hoisting further loads, which would exhaust the SGPRs.
+template <int TM, int TN, int KC, int LDA>
+__device__ inline void stage_fma(float (&acc)[TM][TN], const float (*As)[LDA], cfloat *fp,
+                                 uint32_t row_stride, uint32_t lane)
 {
-    float fc[TN], fn[TN];
-    float4 xc, xn;
-    load_filter<FULLCH>(fc, filter_row(k0, a), a, jc);
-    xc = *reinterpret_cast<const float4 *>(&As[0][TM * lane]);
+    float fc[TN], fn[TN], xc[TM], xn[TM];
+    load_filter<TN>(fc, fp);
+    read_pixels<TM, LDA>(xc, As, 0, lane);
     wait_lgkm();
 #pragma unroll
     for (int kk = 0; kk < KC; ++kk) {
-        const bool more = kk + 1 < KC && (uint32_t)kk + 1 < ntaps;
-        if (more) {
-            load_filter<FULLCH>(fn, filter_row(k0 + kk + 1, a), a, jc);
-            xn = *reinterpret_cast<const float4 *>(&As[kk + 1][TM * lane]);
+        if (kk + 1 < KC) {
+            fp += row_stride;
+            load_filter<TN>(fn, fp);
+            read_pixels<TM, LDA>(xn, As, kk + 1, lane);
         }
-        if ((uint32_t)kk < ntaps)
-            tap_fma(acc, xc, fc);
+        tap_fma<TM, TN>(acc, xc, fc);
         wait_lgkm();
         __builtin_amdgcn_sched_barrier(0);
-        if (more) {
+        if (kk + 1 < KC) {
 #pragma unroll
             for (int c = 0; c < TN; ++c)
                 fc[c] = fn[c];
-            xc = xn;
+#pragma unroll
+            for (int t = 0; t < TM; ++t)
+                xc[t] = xn[t];
         }
     }
 }
 
-// FULLCH (C_o >= 16): every wave multiplies 16 existing channels; a wave
-// whose 16 channels would run past C_o computes channels C_o-16..C_o-1
-// instead and stores only the ones no other wave owns.  Otherwise (C_o < 16)
-// filter reads are clamped channel by channel.
-template <bool VEC, int WAVES, bool FULLCH>
+template <int TM, int TN, int KC, int WAVES, bool V4>
 __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
 {
-    __shared__ float As[2][KC][LDA];
-    __shared__ uint32_t rowoff[BM];
+    using G = Geo<TM, TN, KC, WAVES, V4>;
+    __shared__ __attribute__((aligned(16))) float As[2][KC][G::LDA];
+    __shared__ uint32_t rowoff[G::BM];
 
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const uint32_t p0 = blockIdx.x * BM;
-    const uint32_t jw = blockIdx.y * (TN * WAVES) + wave * TN;  // first channel this wave owns
-    const uint32_t jc = (!FULLCH || jw + TN <= a.Co) ? jw : a.Co - TN;  // first channel it computes
+    const uint32_t p0 = blockIdx.x * G::BM;
+    const uint32_t jw = blockIdx.y * (TN * WAVES) + wave * TN;  // first channel of this wave
 
     // window offsets of the workgroup's pixels, relative to the strip of p0
     const uint32_t q0 = fdiv(p0, a.div_Wo);
@@ -210,7 +248,7 @@ __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
     const uint64_t left = a.win_bytes - tb_elem * 4;
     const __amdgpu_buffer_rsrc_t rs =
         make_rsrc(a.ws + tb_elem, (uint32_t)(left < kMaxRecords ? left : kMaxRecords));
-    for (uint32_t t = tid; t < BM; t += 64 * WAVES) {
+    for (uint32_t t = tid; t < G::BM; t += G::NT) {
         const uint32_t p = p0 + t;
         uint32_t off = 0;
         if (p < a.P) {
@@ -228,20 +266,22 @@ __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
         for (int c = 0; c < TN; ++c)
             acc[t][c] = 0.f;
 
-    const uint32_t nst = (a.K + KC - 1) / KC;
-    Stage<VEC, WAVES> stg;
+    const uint32_t nst = a.K_pad / KC;
+    Stage<TM, TN, KC, WAVES, V4> stg;
     stg.load(rs, rowoff, p0, 0, a);
     stg.store(As[0]);
     __syncthreads();
 
+    // a wave whose channels all lie past C_o (a ragged last channel block)
+    // only helps with the loads
     const bool active = jw < a.Co;
+    cfloat *fp = (cfloat *)a.packed + jw;
     for (uint32_t st = 0; st < nst; ++st) {
-        const uint32_t k0 = st * KC;
         if (st + 1 < nst)
-            stg.load(rs, rowoff, p0, k0 + KC, a);
-        const uint32_t ntaps = min((uint32_t)KC, a.K - k0);
+            stg.load(rs, rowoff, p0, (st + 1) * KC, a);
         if (active)
-            stage_fma<FULLCH>(acc, As[st & 1], k0, ntaps, a, jc, lane);
+            stage_fma<TM, TN, KC, G::LDA>(acc, As[st & 1], fp + (uint64_t)st * KC * a.Co_pad,
+                                         a.Co_pad, lane);
         if (st + 1 < nst)
             stg.store(As[(st + 1) & 1]);
         __syncthreads();
@@ -254,8 +294,8 @@ __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
         const uint32_t p = p0 + TM * lane + t;
         if (p >= a.P)
             continue;
-        float *o = a.out + (uint64_t)p * a.Co + jc;
-        if (jc == jw && jw + TN <= a.Co && (a.Co & 3) == 0) {
+        float *o = a.out + (uint64_t)p * a.Co + jw;
+        if (jw + TN <= a.Co && (a.Co & 3) == 0) {
 #pragma unroll
             for (int c = 0; c < TN; c += 4)
                 *reinterpret_cast<float4 *>(o + c) =
@@ -263,58 +303,109 @@ __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
         } else {
 #pragma unroll
             for (int c = 0; c < TN; ++c)
-                if (jc + c >= jw && jc + c < a.Co)
+                if (jw + c < a.Co)
                     o[c] = acc[t][c];
         }
     }
 }
 
-template <int WAVES>
-const void *pick(bool vec, bool fullch)
+// ---------------------------------------------------------------------------
+// Kernel selection.  A tile is (pixels per lane TM, channels per wave TN,
+// taps per stage KC); the number of waves per workgroup is chosen per layer.
+struct Tile {
+    const char *name;
+    int tm, tn, kc;
+};
+
+const Tile kTiles[] = {
+    {"m4n16", 4, 16, 16},
+    {"m8n16", 8, 16, 8},
+    {"m4n32", 4, 32, 16},
+};
+
+template <int TM, int TN, int KC, int W>
+const void *kernel_for(bool v4)
 {
-    if (fullch)
-        return vec ? (const void *)&conv_fp32_kernel<true, WAVES, true>
-                   : (const void *)&conv_fp32_kernel<false, WAVES, true>;
-    return vec ? (const void *)&conv_fp32_kernel<true, WAVES, false>
-               : (const void *)&conv_fp32_kernel<false, WAVES, false>;
+    return v4 ? (const void *)&conv_fp32_kernel<TM, TN, KC, W, true>
+              : (const void *)&conv_fp32_kernel<TM, TN, KC, W, false>;
+}
+
+template <int TM, int TN, int KC>
+const void *kernel_for(int waves, bool v4)
+{
+    switch (waves) {
+    case 8: return kernel_for<TM, TN, KC, 8>(v4);
+    case 4: return kernel_for<TM, TN, KC, 4>(v4);
+    case 2: return kernel_for<TM, TN, KC, 2>(v4);
+    default: return kernel_for<TM, TN, KC, 1>(v4);
+    }
+}
+
+const void *kernel_for(const Tile &t, int waves, bool v4)
+{
+    if (t.tm == 4 && t.tn == 16)
+        return kernel_for<4, 16, 16>(waves, v4);
+    if (t.tm == 8 && t.tn == 16)
+        return kernel_for<8, 16, 8>(waves, v4);
+    return kernel_for<4, 32, 16>(waves, v4);
 }
 
 }  // namespace
 
-hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const float *filt, float *out,
+hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hipStream_t st)
+{
+    Pack32Args a;
+    a.filt = filt;
+    a.packed = static_cast<float *>(packed);
+    a.quads = (uint64_t)sh.K_pad32 * sh.Co_pad32 / 4;
+    a.K = (uint32_t)sh.K; a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
+    a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
+    uint64_t blocks = (a.quads + 255) / 256;
+    if (blocks > 65536)
+        blocks = 65536;
+    void *args[] = {&a};
+    return hipLaunchKernel((const void *)&pack_filter_fp32, dim3((uint32_t)blocks), dim3(256), args, 0, st);
+}
+
+hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed, float *out,
                             hipStream_t st)
 {
     C32Args a;
     a.ws = static_cast<const float *>(ws);
-    a.filt = filt;
+    a.packed = static_cast<const float *>(packed);
     a.out = out;
     a.win_bytes = (uint64_t)sh.win_bytes;
-    a.P = (uint32_t)sh.P; a.K = (uint32_t)sh.K; a.Co = (uint32_t)sh.Co; a.Ci = (uint32_t)sh.Ci;
-    a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw; a.Wo = (uint32_t)sh.Wo;
-    a.L = (uint32_t)sh.L; a.S = (uint32_t)sh.S; a.KhCi = (uint32_t)(sh.Kh * sh.Ci);
+    a.P = (uint32_t)sh.P; a.K = (uint32_t)sh.K; a.K_pad = (uint32_t)sh.K_pad32;
+    a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
+    a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.S = (uint32_t)sh.S;
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
-    a.div_Ci = make_fastdiv((uint32_t)sh.Ci);
-    a.div_KhCi = make_fastdiv(a.KhCi);
-    // Channel groups per workgroup: the largest of 8, 4, 2, 1 waves (16
+
+    const int ntiles = (int)(sizeof kTiles / sizeof kTiles[0]);
+    int ti = 0;
+    // IM2WIN_FP32_TILE=<name> overrides the tile (for tuning).
+    if (const char *e = getenv("IM2WIN_FP32_TILE")) {
+        for (int t = 0; t < ntiles; ++t)
+            if (strcmp(e, kTiles[t].name) == 0)
+                ti = t;
+    }
+    const Tile &tile = kTiles[ti];
+    // Channel groups per workgroup: the largest of 8, 4, 2, 1 waves (TN
     // channels each) that leaves no more idle channels than any smaller one.
     int waves = 1;
     int64_t best = -1;
     for (int w : {8, 4, 2, 1}) {
-        const int64_t span = 16 * w, tiles = (sh.Co + span - 1) / span;
+        const int64_t span = (int64_t)tile.tn * w, tiles = (sh.Co + span - 1) / span;
         const int64_t idle = tiles * span - sh.Co;
         if (best < 0 || idle < best) {
             best = idle;
             waves = w;
         }
     }
-    const bool vec = (sh.Ci % 4) == 0;  // every window starts on a 16-byte boundary
-    const bool fullch = sh.Co >= TN;
-    const void *f = waves == 8   ? pick<8>(vec, fullch)
-                    : waves == 4 ? pick<4>(vec, fullch)
-                    : waves == 2 ? pick<2>(vec, fullch)
-                                 : pick<1>(vec, fullch);
-    const int64_t span = 16 * waves;
-    dim3 grid((uint32_t)((sh.P + BM - 1) / BM), (uint32_t)((sh.Co + span - 1) / span));
+    const bool v4 = (sh.Ci % 4) == 0;  // every window starts on a 16-byte boundary
+    const void *f = kernel_for(tile, waves, v4);
+    const int64_t span = (int64_t)tile.tn * waves;
+    const int64_t bm = 64 * tile.tm;
+    dim3 grid((uint32_t)((sh.P + bm - 1) / bm), (uint32_t)((sh.Co + span - 1) / span));
     void *args[] = {&a};
     return hipLaunchKernel(f, grid, dim3(64 * waves), args, 0, st);
 }
