@@ -29,8 +29,7 @@ if ROOT not in sys.path:
 
 # MI355X published peaks
 PEAK_HBM_GBS = 8000.0
-PEAK_FP32_VECTOR_TF = 157.3     # counts packed fp32 FMA
-PEAK_FP32_UNPACKED_TF = 78.6    # 256 CU x 64 lanes x 2 flop x 2.4 GHz, plain v_fma_f32
+PEAK_FP32_VECTOR_TF = 157.3     # 256 CU x 256 flop/clk x 2.4 GHz
 PEAK_FP16_MFMA_TF = 2516.6      # dense
 
 
@@ -219,7 +218,6 @@ def main():
                 "peak": PEAK_FP32_VECTOR_TF,
                 "unit": "TFLOP/s",
                 "frac": round(tf32 / PEAK_FP32_VECTOR_TF, 4),
-                "frac_of_unpacked_fma_peak": round(tf32 / PEAK_FP32_UNPACKED_TF, 4),
                 "traffic": None,
             },
             "kernels": {

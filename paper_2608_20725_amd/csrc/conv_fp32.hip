@@ -17,10 +17,14 @@
 //     [tap][pixel] so that a lane fetches its TM pixels with 16-byte LDS
 //     reads; stages are double-buffered: the global loads of stage t+1 are in
 //     flight while stage t is multiplied;
-//   * filter values are the same for every lane of a wave, so they are read
-//     with scalar loads into SGPRs and every multiply-add takes one operand
-//     from an SGPR: per tap a lane does TM*TN FMAs for TM/4 LDS reads and one
-//     scalar load, and the filter pointer advances by one row per tap.
+//   * filter values are the same for every lane of a wave: the stage's slab
+//     of the packed filter (KC rows, the workgroup's channels) is staged into
+//     LDS with the windows, and each wave reads its TN values of a tap with
+//     broadcast LDS reads; per tap a lane does TM*TN FMAs for TM/4 + TN/4
+//     16-byte LDS reads.  (A variant reads the filter rows with scalar loads
+//     into SGPRs instead; it loses on this part because the scalar cache
+//     misses most rows, and remains only for filters too large for the LDS
+//     variant's 31-bit offsets.)
 // The row offset of every pixel's window is computed once per workgroup (the
 // index precomputation of Sec. III-E).  Taps past K read zero window values
 // (masked loads) against zero filter rows (padding): they add exactly 0.
@@ -147,6 +151,45 @@ struct Stage {
     }
 };
 
+// Filter slab of one stage for the LDS-filter variant: KC packed rows times
+// the workgroup's TN*WAVES channels, staged through LDS next to the windows
+// with coalesced 16-byte loads issued a stage ahead.  Columns past the
+// packed filter read zero.
+template <int TN, int KC, int WAVES>
+struct FStage {
+    static constexpr int NT = 64 * WAVES;
+    static constexpr int CW = TN * WAVES;  // channels of the workgroup
+    static constexpr int Q = KC * CW / 4;  // 16-byte granules per stage
+    static constexpr int ITEMS = (Q + NT - 1) / NT;
+    u32x4 v[ITEMS];
+
+    __device__ inline void load(__amdgpu_buffer_rsrc_t rf, uint32_t k0, uint32_t jb, uint32_t co_pad)
+    {
+#pragma unroll
+        for (int j = 0; j < ITEMS; ++j) {
+            const uint32_t g = threadIdx.x + j * NT;
+            const uint32_t row = (g / (CW / 4)) % KC, c4 = g % (CW / 4);
+            const uint32_t col = jb + 4 * c4;
+            const bool ok = g < (uint32_t)Q && col < co_pad;
+            v[j] = ld_b128(rf, ok ? ((k0 + row) * co_pad + col) * 4u : kOOB);
+        }
+    }
+
+    __device__ inline void store(float (*Fs)[CW])
+    {
+#pragma unroll
+        for (int j = 0; j < ITEMS; ++j) {
+            const uint32_t g = threadIdx.x + j * NT;
+            if (g < (uint32_t)Q) {
+                const uint32_t row = g / (CW / 4), c4 = g % (CW / 4);
+                *reinterpret_cast<float4 *>(&Fs[row][4 * c4]) =
+                    make_float4(__uint_as_float(v[j][0]), __uint_as_float(v[j][1]),
+                                __uint_as_float(v[j][2]), __uint_as_float(v[j][3]));
+            }
+        }
+    }
+};
+
 // The packed filter is read through the constant address space: the kernel
 // never writes it, and loads from that space with a uniform address become
 // s_load.
@@ -195,29 +238,83 @@ __device__ inline void read_pixels(float (&x)[TM], const float (*As)[LDA], int k
 // vector-memory loads in flight.
 __device__ inline void wait_lgkm() { __builtin_amdgcn_s_waitcnt(0xc07f); }
 
-// Multiplies one LDS stage of KC taps whose first packed filter row is `fp`.
-// The LDS reads and the filter loads of tap kk+1 are issued before the FMAs
-// of tap kk and waited for after them (scalar loads can return out of order,
-// so the only safe wait is for all of them); the scheduling fence keeps the
-// compiler from hoisting further loads, which would exhaust the SGPRs.
-template <int TM, int TN, int KC, int LDA>
+// Multiplies one LDS stage of KC taps whose first packed filter row is `fp`,
+// TP taps per group.  The LDS reads and the filter loads of group g+1 are
+// issued before the FMAs of group g and waited for after them: scalar loads
+// can return out of order, so the only safe wait is for all of them, and the
+// group size sets how much work covers each wait (the filter rows mostly
+// come from L2, since every wave streams its own column block of F').  The
+// scheduling fence keeps the compiler from hoisting further loads, which
+// would exhaust the SGPRs.
+template <int TM, int TN, int KC, int TP, int LDA>
 __device__ inline void stage_fma(float (&acc)[TM][TN], const float (*As)[LDA], cfloat *fp,
                                  uint32_t row_stride, uint32_t lane)
 {
-    float fc[TN], fn[TN], xc[TM], xn[TM];
-    load_filter<TN>(fc, fp);
-    read_pixels<TM, LDA>(xc, As, 0, lane);
+    static_assert(KC % TP == 0, "taps per group");
+    float fc[TP][TN], fn[TP][TN], xc[TP][TM], xn[TP][TM];
+#pragma unroll
+    for (int q = 0; q < TP; ++q) {
+        load_filter<TN>(fc[q], fp + q * row_stride);
+        read_pixels<TM, LDA>(xc[q], As, q, lane);
+    }
     wait_lgkm();
+#pragma unroll
+    for (int kk = 0; kk < KC; kk += TP) {
+        if (kk + TP < KC) {
+            fp += TP * row_stride;
+#pragma unroll
+            for (int q = 0; q < TP; ++q) {
+                load_filter<TN>(fn[q], fp + q * row_stride);
+                read_pixels<TM, LDA>(xn[q], As, kk + TP + q, lane);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < TP; ++q)
+            tap_fma<TM, TN>(acc, xc[q], fc[q]);
+        wait_lgkm();
+        __builtin_amdgcn_sched_barrier(0);
+        if (kk + TP < KC) {
+#pragma unroll
+            for (int q = 0; q < TP; ++q) {
+#pragma unroll
+                for (int c = 0; c < TN; ++c)
+                    fc[q][c] = fn[q][c];
+#pragma unroll
+                for (int t = 0; t < TM; ++t)
+                    xc[q][t] = xn[q][t];
+            }
+        }
+    }
+}
+
+// LDS-filter variant of stage_fma: the wave's TN filter values of a tap are
+// one LDS row segment at a wave-uniform address (a broadcast read); LDS
+// returns in order, so the compiler's own waits pipeline tap kk+1's reads
+// behind tap kk's FMAs.
+template <int TM, int TN, int KC, int LDA, int CW>
+__device__ inline void stage_fma_lds(float (&acc)[TM][TN], const float (*As)[LDA],
+                                     const float (*Fs)[CW], uint32_t wave, uint32_t lane)
+{
+    float fc[TN], fn[TN], xc[TM], xn[TM];
+    auto read_filter = [&](float (&f)[TN], int kk) {
+#pragma unroll
+        for (int q = 0; q < TN / 4; ++q) {
+            const float4 v = *reinterpret_cast<const float4 *>(&Fs[kk][wave * TN + 4 * q]);
+            f[4 * q + 0] = v.x;
+            f[4 * q + 1] = v.y;
+            f[4 * q + 2] = v.z;
+            f[4 * q + 3] = v.w;
+        }
+    };
+    read_filter(fc, 0);
+    read_pixels<TM, LDA>(xc, As, 0, lane);
 #pragma unroll
     for (int kk = 0; kk < KC; ++kk) {
         if (kk + 1 < KC) {
-            fp += row_stride;
-            load_filter<TN>(fn, fp);
+            read_filter(fn, kk + 1);
             read_pixels<TM, LDA>(xn, As, kk + 1, lane);
         }
         tap_fma<TM, TN>(acc, xc, fc);
-        wait_lgkm();
-        __builtin_amdgcn_sched_barrier(0);
         if (kk + 1 < KC) {
 #pragma unroll
             for (int c = 0; c < TN; ++c)
@@ -229,11 +326,16 @@ __device__ inline void stage_fma(float (&acc)[TM][TN], const float (*As)[LDA], c
     }
 }
 
-template <int TM, int TN, int KC, int WAVES, bool V4>
+// TP = 0 selects the LDS-filter variant; TP >= 1 reads filter rows with
+// scalar loads, TP taps per wait.
+template <int TM, int TN, int KC, int TP, int WAVES, bool V4>
 __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
 {
     using G = Geo<TM, TN, KC, WAVES, V4>;
+    constexpr bool FL = TP == 0;
+    constexpr int CW = TN * WAVES;
     __shared__ __attribute__((aligned(16))) float As[2][KC][G::LDA];
+    __shared__ __attribute__((aligned(16))) float Fs[FL ? 2 : 1][FL ? KC : 1][CW];
     __shared__ uint32_t rowoff[G::BM];
 
     const uint32_t tid = threadIdx.x;
@@ -267,9 +369,18 @@ __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
             acc[t][c] = 0.f;
 
     const uint32_t nst = a.K_pad / KC;
+    const uint32_t jb = blockIdx.y * CW;  // first channel of the workgroup
+    const uint64_t fbytes = (uint64_t)a.K_pad * a.Co_pad * 4;
+    const __amdgpu_buffer_rsrc_t rf =
+        make_rsrc(a.packed, (uint32_t)(fbytes < kMaxRecords ? fbytes : kMaxRecords));
     Stage<TM, TN, KC, WAVES, V4> stg;
+    FStage<TN, KC, WAVES> fst;
     stg.load(rs, rowoff, p0, 0, a);
+    if (FL)
+        fst.load(rf, 0, jb, a.Co_pad);
     stg.store(As[0]);
+    if (FL)
+        fst.store(Fs[0]);
     __syncthreads();
 
     // a wave whose channels all lie past C_o (a ragged last channel block)
@@ -277,13 +388,23 @@ __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
     const bool active = jw < a.Co;
     cfloat *fp = (cfloat *)a.packed + jw;
     for (uint32_t st = 0; st < nst; ++st) {
-        if (st + 1 < nst)
+        if (st + 1 < nst) {
             stg.load(rs, rowoff, p0, (st + 1) * KC, a);
-        if (active)
-            stage_fma<TM, TN, KC, G::LDA>(acc, As[st & 1], fp + (uint64_t)st * KC * a.Co_pad,
-                                         a.Co_pad, lane);
-        if (st + 1 < nst)
+            if (FL)
+                fst.load(rf, (st + 1) * KC, jb, a.Co_pad);
+        }
+        if (active) {
+            if constexpr (FL)
+                stage_fma_lds<TM, TN, KC, G::LDA, CW>(acc, As[st & 1], Fs[st & 1], wave, lane);
+            else
+                stage_fma<TM, TN, KC, TP, G::LDA>(acc, As[st & 1],
+                                                  fp + (uint64_t)st * KC * a.Co_pad, a.Co_pad, lane);
+        }
+        if (st + 1 < nst) {
             stg.store(As[(st + 1) & 1]);
+            if (FL)
+                fst.store(Fs[(st + 1) & 1]);
+        }
         __syncthreads();
     }
 
@@ -311,43 +432,47 @@ __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
 
 // ---------------------------------------------------------------------------
 // Kernel selection.  A tile is (pixels per lane TM, channels per wave TN,
-// taps per stage KC); the number of waves per workgroup is chosen per layer.
+// taps per stage KC, taps per filter-load group TP); the number of waves per
+// workgroup is chosen per layer.
 struct Tile {
     const char *name;
-    int tm, tn, kc;
+    int tm, tn, kc, tp;
 };
 
+// Measured on MI355X: the LDS-filter tiles beat the scalar-load tiles on
+// every layer tried (the scalar cache hits ~25 % of filter rows, so
+// scalar-load waits dominate); the scalar-load tile remains for filters too
+// large for 31-bit LDS-stage offsets.
 const Tile kTiles[] = {
-    {"m4n16", 4, 16, 16},
-    {"m8n16", 8, 16, 8},
-    {"m4n32", 4, 32, 16},
+    {"m4n16f", 4, 16, 16, 0},
+    {"m8n16f", 8, 16, 8, 0},
+    {"m4n16p2", 4, 16, 16, 2},
 };
+constexpr int kScalarTile = 2;
 
-template <int TM, int TN, int KC, int W>
+template <int TM, int TN, int KC, int TP, int W>
 const void *kernel_for(bool v4)
 {
-    return v4 ? (const void *)&conv_fp32_kernel<TM, TN, KC, W, true>
-              : (const void *)&conv_fp32_kernel<TM, TN, KC, W, false>;
+    return v4 ? (const void *)&conv_fp32_kernel<TM, TN, KC, TP, W, true>
+              : (const void *)&conv_fp32_kernel<TM, TN, KC, TP, W, false>;
 }
 
-template <int TM, int TN, int KC>
+template <int TM, int TN, int KC, int TP>
 const void *kernel_for(int waves, bool v4)
 {
     switch (waves) {
-    case 8: return kernel_for<TM, TN, KC, 8>(v4);
-    case 4: return kernel_for<TM, TN, KC, 4>(v4);
-    case 2: return kernel_for<TM, TN, KC, 2>(v4);
-    default: return kernel_for<TM, TN, KC, 1>(v4);
+    case 8: return kernel_for<TM, TN, KC, TP, 8>(v4);
+    case 4: return kernel_for<TM, TN, KC, TP, 4>(v4);
+    case 2: return kernel_for<TM, TN, KC, TP, 2>(v4);
+    default: return kernel_for<TM, TN, KC, TP, 1>(v4);
     }
 }
 
 const void *kernel_for(const Tile &t, int waves, bool v4)
 {
-    if (t.tm == 4 && t.tn == 16)
-        return kernel_for<4, 16, 16>(waves, v4);
-    if (t.tm == 8 && t.tn == 16)
-        return kernel_for<8, 16, 8>(waves, v4);
-    return kernel_for<4, 32, 16>(waves, v4);
+    if (t.tm == 8)
+        return kernel_for<8, 16, 8, 0>(waves, v4);
+    return t.tp == 2 ? kernel_for<4, 16, 16, 2>(waves, v4) : kernel_for<4, 16, 16, 0>(waves, v4);
 }
 
 }  // namespace
@@ -388,6 +513,9 @@ hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed,
             if (strcmp(e, kTiles[t].name) == 0)
                 ti = t;
     }
+    // the LDS-filter tiles address the packed filter with 31-bit offsets
+    if (kTiles[ti].tp == 0 && sh.K_pad32 * sh.Co_pad32 * 4 > (int64_t)kMaxRecords)
+        ti = kScalarTile;
     const Tile &tile = kTiles[ti];
     // Channel groups per workgroup: the largest of 8, 4, 2, 1 waves (TN
     // channels each) that leaves no more idle channels than any smaller one.
