@@ -32,6 +32,27 @@ PEAK_HBM_GBS = 8000.0
 PEAK_FP32_VECTOR_TF = 157.3     # 256 CU x 256 flop/clk x 2.4 GHz
 PEAK_FP16_MFMA_TF = 2516.6      # dense
 
+# HBM-side bytes per launch of the fp32 conv kernel, from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE counters (FETCH_SIZE scaled by 2.0 and WRITE_SIZE by 1.0, the
+# factors a plain 1 GiB copy gives), keyed by layer.  They hold only for the
+# kernel source they were taken on, identified by its SHA-256; after any change
+# to that source the figure is reported as null until measured again.
+# Source: profiles/cfg2_n128_c64_56_3x3.md.
+FP32_CONV_TRAFFIC = {
+    "source_sha256": "5e7e8614f5b13eb79b86443bbfdf47f833dacc77024aac1fbe93c71d86b7ed71",
+    "bytes": {"cfg2": 943.8e6 + 96.0e6},
+}
+
+
+def fp32_conv_traffic(layer_name):
+    import hashlib
+    src = os.path.join(ROOT, "paper_2608_20725_amd", "csrc", "conv_fp32.hip")
+    with open(src, "rb") as f:
+        digest = hashlib.sha256(f.read()).hexdigest()
+    if digest != FP32_CONV_TRAFFIC["source_sha256"]:
+        return None
+    return FP32_CONV_TRAFFIC["bytes"].get(layer_name)
+
 
 def layer_numbers(l, pkg):
     Ho, Wo = pkg.conv_output_dims(l.H, l.W, l.K_h, l.K_w, l.stride)
@@ -218,7 +239,7 @@ def main():
                 "peak": PEAK_FP32_VECTOR_TF,
                 "unit": "TFLOP/s",
                 "frac": round(tf32 / PEAK_FP32_VECTOR_TF, 4),
-                "traffic": None,
+                "traffic": fp32_conv_traffic(l.name),
             },
             "kernels": {
                 "f32_transform": {"ms": round(t32, 5), "GB/s": round(f32["transform_bytes"] / t32 / 1e6, 1),
