@@ -40,7 +40,7 @@ PEAK_FP16_MFMA_TF = 2516.6      # dense
 # Source: profiles/cfg2_n128_c64_56_3x3.md.
 FP32_CONV_TRAFFIC = {
     "source_sha256": "5e7e8614f5b13eb79b86443bbfdf47f833dacc77024aac1fbe93c71d86b7ed71",
-    "bytes": {"cfg2": 943.8e6 + 96.0e6},
+    "bytes": {"cfg2_n128_c64_56_3x3": 943.8e6 + 96.0e6},
 }
 
 

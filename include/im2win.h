@@ -25,8 +25,11 @@
  *                     the buffer
  *     [pad_end, ...)  the filter repacked in window order (tap k = (v*K_h+u)*C_i+r)
  *                     and zero-padded, written by the conv call:
- *                       fp16: [C_o_pad][K_pad] fp16, C_o_pad = round_up(C_o, 128),
- *                             K_pad = round_up(K, 64)
+ *                       fp16: C_o_pad*K_w*T_pad fp16 values, C_o_pad = round_up(C_o, 128),
+ *                             T_pad = round_up(K_h*C_i, 64), holding either
+ *                             [C_o_pad][K_pad] (K_pad = round_up(K, 64)) or one
+ *                             [T_pad] slice per filter column, [C_o_pad][K_w][T_pad],
+ *                             depending on the kernel the layer runs
  *                       fp32: [K_pad32][C_o_pad32] fp32, K_pad32 = round_up(K, 16),
  *                             C_o_pad32 = round_up(C_o, 32)
  *

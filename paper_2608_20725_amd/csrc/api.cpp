@@ -63,13 +63,16 @@ int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_
     r.K_pad = round_up(r.K, 64);
     r.K_pad32 = round_up(r.K, 16);
     r.Co_pad32 = round_up(Co, 32);
+    r.Tp = round_up(Kh * Ci, 64);
     *sh = r;
     return IM2WIN_OK;
 }
 
 int64_t packed_filter_bytes(const Shape &sh, int dt)
 {
-    return dt == IM2WIN_F16 ? sh.Co_pad * sh.K_pad * 2 : sh.K_pad32 * sh.Co_pad32 * 4;
+    // fp16: room for either layout, [C_o_pad][K_pad] or [C_o_pad][K_w][Tp]
+    // (K_pad <= K_w*Tp)
+    return dt == IM2WIN_F16 ? sh.Co_pad * sh.Kw * sh.Tp * 2 : sh.K_pad32 * sh.Co_pad32 * 4;
 }
 
 int64_t workspace_bytes(const Shape &sh, int dt) { return sh.pad_end + packed_filter_bytes(sh, dt); }

@@ -54,6 +54,7 @@ struct Shape {
     int64_t K_pad;      // packed fp16 filter columns
     int64_t K_pad32;    // packed fp32 filter rows (taps)
     int64_t Co_pad32;   // packed fp32 filter columns (channels)
+    int64_t Tp;         // K_h*C_i rounded up to 64 (fp16 per-column filter slices)
 };
 
 inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
@@ -105,4 +106,9 @@ hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed,
 hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed, hipStream_t st);
 hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed, uint16_t *out,
                             hipStream_t st);
+// Column-staged fp16 kernel: the variant for this layer, or -1 when the
+// row-per-pixel kernels run instead.  The filter pack layout follows it.
+int col_plan(const Shape &sh);
+hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const void *packed,
+                                uint16_t *out, hipStream_t st);
 } // namespace im2win

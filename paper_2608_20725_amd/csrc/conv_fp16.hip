@@ -41,31 +41,37 @@ struct C16Args {
 };
 
 // ---------------------------------------------------------------------------
-// Filter repack (window order, zero-padded).  One thread per 16-byte granule
-// of F'.
+// Filter repack (window order, zero-padded): out[j][c][t] = F'[j][c*tlen + t]
+// for t < tlen, 0 for tlen <= t < tpad, 0 for j >= C_o, with nv slices of tpad
+// per row.  F'[j][k] is tap k = (v*K_h + u)*C_i + r of filter column j.  The
+// row-per-pixel kernels use one slice (tlen = K, tpad = K_pad); the
+// column-staged kernel one slice per filter column v (tlen = K_h*C_i).
+// One thread per 16-byte granule.
 struct PackArgs {
     const uint16_t *filt;
     uint16_t *packed;
     uint64_t grans;
-    uint32_t K, K_pad, Co, Ci, Kh, Kw;
+    uint32_t nv, tlen, tpad, Co, Ci, Kh, Kw;
 };
 
 __global__ __launch_bounds__(256) void pack_filter_fp16(PackArgs a)
 {
-    const uint32_t gpr = a.K_pad / 8;  // granules per packed row
+    const uint32_t gpr = a.nv * a.tpad / 8;  // granules per packed row
     for (uint64_t g = (uint64_t)blockIdx.x * 256 + threadIdx.x; g < a.grans;
          g += (uint64_t)gridDim.x * 256) {
         const uint32_t j = (uint32_t)(g / gpr);
-        const uint32_t k0 = (uint32_t)(g % gpr) * 8;
+        const uint32_t i0 = (uint32_t)(g % gpr) * 8;
+        const uint32_t c = i0 / a.tpad, t0 = i0 % a.tpad;
         uint32_t w[4];
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
             uint32_t lo = 0, hi = 0;
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const uint32_t k = k0 + e + h;
+                const uint32_t t = t0 + e + h;
                 uint32_t bits = 0;
-                if (j < a.Co && k < a.K) {
+                if (j < a.Co && t < a.tlen) {
+                    const uint32_t k = c * a.tlen + t;
                     const uint32_t khci = a.Kh * a.Ci;
                     const uint32_t v = k / khci, rem = k % khci;
                     const uint32_t u = rem / a.Ci, r = rem % a.Ci;
@@ -534,9 +540,13 @@ hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed,
     PackArgs a;
     a.filt = filt;
     a.packed = static_cast<uint16_t *>(packed);
-    a.grans = (uint64_t)sh.Co_pad * sh.K_pad / 8;
-    a.K = (uint32_t)sh.K; a.K_pad = (uint32_t)sh.K_pad; a.Co = (uint32_t)sh.Co;
-    a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
+    if (col_plan(sh) >= 0) {
+        a.nv = (uint32_t)sh.Kw; a.tlen = (uint32_t)(sh.Kh * sh.Ci); a.tpad = (uint32_t)sh.Tp;
+    } else {
+        a.nv = 1; a.tlen = (uint32_t)sh.K; a.tpad = (uint32_t)sh.K_pad;
+    }
+    a.grans = (uint64_t)sh.Co_pad * a.nv * a.tpad / 8;
+    a.Co = (uint32_t)sh.Co; a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
     uint64_t blocks = (a.grans + 255) / 256;
     if (blocks > 65536)
         blocks = 65536;
@@ -547,6 +557,9 @@ hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed,
 hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed, uint16_t *out,
                             hipStream_t st)
 {
+    const int plan = col_plan(sh);
+    if (plan >= 0)
+        return launch_conv_fp16_col(sh, plan, ws, packed, out, st);
     C16Args a;
     a.ws = static_cast<const uint16_t *>(ws);
     a.packed = static_cast<const uint16_t *>(packed);

@@ -1,0 +1,442 @@
+// fp16 windowed convolution on the gfx950 matrix cores, staged by input
+// column (Sec. III-B..D, Eq. 3, Alg. 1).
+//
+// A strip of the window tensor is a sequence of W_i input columns, each
+// T = K_h*C_i elements long in (u, r) order, and the window of output column
+// n is the run of columns n*s .. n*s+K_w-1.  Tap k = v*T + t of that window
+// is element t of column n*s + v.  Neighbouring windows share K_w - s
+// columns, so a tile of BN consecutive pixels needs far fewer distinct
+// columns than BN*K_w: this kernel loads every distinct column of its tile
+// once per stage and lets the K_w windows that use a column read it from LDS
+// (the re-use the window layout is built for, applied on chip).
+//
+// Product:  D[j][p] = sum_v sum_t G[j][v][t] * X[col(p, v)][t]
+//   G is the filter packed per filter column v: G[j][v][t] = F[u][v][r][j]
+//   with t = u*C_i + r, zero for t >= T (T padded to Tp, a multiple of 64);
+//   X[c][t] is element t of strip column c.
+//
+// A stage covers BT consecutive t of every column slice:
+//   A rows  (v, j)  K_w*BM rows of BT filter values,
+//   B rows  one per distinct column of the tile (at most NRMAX), BT values,
+// fetched with buffer_load ... lds (each lane's 16 bytes go straight to LDS,
+// one wave instruction fills 1 KiB = 1024/(2*BT) rows) into a two-slot ring:
+// the loads of stage t+1 are in flight while the matrix cores multiply
+// stage t (Alg. 1's double buffering with asynchronous copies).  Every stage
+// does K_w*BT/16 MFMA k-steps; pixel p's B fragment for filter column v is
+// row R(p) + v.
+//
+// Row numbering of the B rows: with ms = min(s, K_w), pixel slot n of the
+// tile gets R(n) = n*ms + k(n)*(K_w - ms), k(n) = strips crossed since the
+// tile's first pixel.  Consecutive pixels of one strip then share K_w - ms
+// rows, and each strip run of the tile starts K_w rows after the previous
+// run's last pixel.
+//
+// LDS rows are XOR-swizzled at 16-byte granularity, chunk c of row r at slot
+// c ^ sw(r), so that the 32 rows one MFMA operand read touches spread over
+// all banks.  The epilogue rounds each fp32 sum to fp16 once (nearest-even).
+#include "common.hpp"
+
+#include <stdlib.h>
+#include <string.h>
+
+namespace im2win {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void *lds_ptr;
+
+struct ColArgs {
+    const uint16_t *ws;      // window tensor (fp16 bits)
+    const uint16_t *packed;  // G [Co_pad][KW][Tp]
+    uint16_t *out;
+    uint64_t win_bytes;
+    uint64_t pk_bytes;       // bytes of G
+    uint32_t P, Co, Wo, L, T, Tp, s, ms, nst;
+    FastDiv div_Wo;
+};
+
+constexpr uint32_t kNoCol = 0xffffffffu;  // B row with no column (past the last pixel)
+
+template <int KW_, int BT_, int WM_, int WN_, int WGM_, int WGN_, int NRMAX_, int NS_>
+struct ColCfg {
+    static constexpr int KW = KW_, BT = BT_, WM = WM_, WN = WN_, WGM = WGM_, WGN = WGN_;
+    static constexpr int NS = NS_;              // ring slots
+    static constexpr int NW = WGM * WGN;        // waves
+    static constexpr int NT = 64 * NW;
+    static constexpr int BM = 32 * WM * WGM;    // channels per tile
+    static constexpr int BN = 32 * WN * WGN;    // pixels per tile
+    static constexpr int NRMAX = NRMAX_;        // B rows a tile may need
+    static constexpr int RB = 2 * BT;           // bytes per LDS row
+    static constexpr int CH = RB / 16;          // 16-byte chunks per row
+    static constexpr int RPI = 1024 / RB;       // rows filled by one wave load
+    static constexpr int AROWS = KW * BM;
+    static constexpr int ROWS = AROWS + NRMAX;
+    static constexpr int NBLK = (ROWS + RPI - 1) / RPI;  // 1 KiB blocks per stage
+    static constexpr int IB = (NBLK + NW - 1) / NW;      // loads per wave per stage
+    // Every wave issues IB loads per stage (those past the stage's rows read
+    // nothing and fill spare LDS with zeros), so outstanding-load counts are
+    // the same for all stages and the ring waits are exact.
+    static constexpr int STAGE = NW * IB * 1024;
+    static_assert(NS >= 2 && NS <= 4, "ring depth");
+    static_assert((NS - 2) * IB <= 63, "vmcnt range");
+    static constexpr int SWS = CH == 4 ? 2 : 3;          // swizzle shift
+    static_assert(BT == 16 || BT == 32 || BT == 64, "stage depth");
+    static_assert(AROWS % RPI == 0, "A and B rows meet at a block boundary");
+};
+
+template <class C>
+__device__ inline uint32_t sw(uint32_t r)
+{
+    return (r ^ (r >> C::SWS)) & (C::CH - 1);
+}
+
+template <int VM>
+__device__ inline void wait_vmcnt()
+{
+    __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier that does not wait for outstanding memory operations
+// (__syncthreads() would also wait for the stage still in flight); the
+// explicit vmcnt wait before it covers the stage about to be read.
+__device__ inline void ring_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <class C>
+struct ColTile {
+    __amdgpu_buffer_rsrc_t rf, rw;
+    uint32_t boff[C::IB];  // byte offset of this lane's chunk at t = 0 (kOOB: none)
+    uint32_t bcm[C::IB];   // B rows: first t of the chunk (t-tail mask); A rows: 0
+    uint32_t Rj[C::WN];    // B row of each of this lane's pixels
+    uint32_t wave, lane, wm, wn, T, nst;
+    floatx16 acc[C::WM][C::WN];
+
+    // Stage st >= nst (past the end of the slices) loads nothing.
+    __device__ inline void issue(uint32_t st, char *slot)
+    {
+        const uint32_t t0 = st * C::BT;
+        const bool past = st >= nst;
+#pragma unroll
+        for (int i = 0; i < C::IB; ++i) {
+            const uint32_t b = wave + C::NW * i;
+            const bool isA = b * C::RPI < (uint32_t)C::AROWS;
+            const uint32_t off = (!past && t0 + bcm[i] < T) ? boff[i] + 2u * t0 : kOOB;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(isA ? rf : rw, (lds_ptr)(slot + 1024 * b), 16, off,
+                                                     0, 0, 0);
+        }
+    }
+
+    // Fragments of k-step ks (filter column v = ks / (BT/16)).
+    __device__ inline void frags(const char *slot, int ks, half8 (&af)[C::WM], half8 (&bf)[C::WN])
+    {
+        const int v = ks / (C::BT / 16), kk = ks % (C::BT / 16);
+        const uint32_t chunk = 2 * kk + (lane >> 5);
+        const uint32_t arow0 = wm * 32 * C::WM + (lane & 31);
+#pragma unroll
+        for (int i = 0; i < C::WM; ++i) {
+            const uint32_t row = v * C::BM + arow0 + 32 * i;
+            af[i] = *reinterpret_cast<const half8 *>(slot + row * C::RB + 16 * (chunk ^ sw<C>(row)));
+        }
+#pragma unroll
+        for (int j = 0; j < C::WN; ++j) {
+            const uint32_t row = C::AROWS + Rj[j] + v;
+            bf[j] = *reinterpret_cast<const half8 *>(slot + row * C::RB + 16 * (chunk ^ sw<C>(row)));
+        }
+    }
+
+    // All k-steps of one stage; the fragments of step ks+1 are read before
+    // the matrix operations of step ks.
+    __device__ inline void compute(const char *slot)
+    {
+        constexpr int KS = C::KW * C::BT / 16;
+        half8 af[2][C::WM], bf[2][C::WN];
+        frags(slot, 0, af[0], bf[0]);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + 1 < KS)
+                frags(slot, ks + 1, af[(ks + 1) & 1], bf[(ks + 1) & 1]);
+#pragma unroll
+            for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+                for (int j = 0; j < C::WN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[ks & 1][i], bf[ks & 1][j],
+                                                                       acc[i][j], 0, 0, 0);
+        }
+    }
+
+    // Stage st sits in slot `cur`: wait for it, then refill the slot freed by
+    // stage st-1 (`next`) with stage st+NS-1, then multiply.  The slots are
+    // separate LDS arrays named at compile time, so the compiler can tell
+    // that reading one does not depend on the loads landing in the others.
+    template <int N>
+    __device__ inline void step(uint32_t st, char (&cur)[N], char (&next)[N])
+    {
+        wait_vmcnt<(C::NS - 2) * C::IB>();
+        ring_barrier();
+        issue(st + C::NS - 1, next);
+        if (st < nst)
+            compute(cur);
+    }
+};
+
+template <class C>
+__global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
+{
+    constexpr int S2 = C::NS > 2 ? C::STAGE : 1024, S3 = C::NS > 3 ? C::STAGE : 1024;
+    __shared__ __attribute__((aligned(1024))) char r0[C::STAGE];
+    __shared__ __attribute__((aligned(1024))) char r1[C::STAGE];
+    __shared__ __attribute__((aligned(1024))) char r2[S2];
+    __shared__ __attribute__((aligned(1024))) char r3[S3];
+    __shared__ uint32_t tbl[C::NRMAX];
+
+    ColTile<C> w;
+    const uint32_t tid = threadIdx.x;
+    w.lane = tid & 63;
+    w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    __builtin_assume(w.wave < (uint32_t)C::NW);
+    w.wm = w.wave / C::WGN;
+    w.wn = w.wave % C::WGN;
+    w.T = a.T;
+    w.nst = a.Tp / C::BT;
+    const uint32_t p0 = blockIdx.x * C::BN;
+    const uint32_t ch0 = blockIdx.y * C::BM;
+    const uint32_t q0 = fdiv(p0, a.div_Wo);
+
+    // B rows address the window tensor from strip q0 on, A rows the filter
+    // from row ch0 on; anything past either buffer reads zero.
+    const uint64_t tb = (uint64_t)q0 * a.L;
+    const uint64_t wleft = a.win_bytes - tb * 2;
+    w.rw = make_rsrc(a.ws + tb, (uint32_t)(wleft < kMaxRecords ? wleft : kMaxRecords));
+    const uint64_t fb = (uint64_t)ch0 * C::KW * a.Tp;
+    const uint64_t fleft = a.pk_bytes > fb * 2 ? a.pk_bytes - fb * 2 : 0;
+    w.rf = make_rsrc(a.packed + fb, (uint32_t)(fleft < kMaxRecords ? fleft : kMaxRecords));
+
+    // Column table: element offset (from strip q0) of the column each B row
+    // holds.  Pixel slot n owns rows R(n) .. R(n)+ms-1; the last pixel of a
+    // strip run also owns the K_w - ms rows after them.
+    for (uint32_t r = tid; r < (uint32_t)C::NRMAX; r += C::NT)
+        tbl[r] = kNoCol;
+    __syncthreads();
+    const uint32_t kwm = C::KW - a.ms;
+    for (uint32_t n = tid; n < (uint32_t)C::BN; n += C::NT) {
+        const uint32_t p = p0 + n;
+        if (p < a.P) {
+            const uint32_t q = fdiv(p, a.div_Wo);
+            const uint32_t c = p - q * a.Wo;
+            const uint32_t k = q - q0;
+            const uint32_t R = n * a.ms + k * kwm;
+            const bool last = n == (uint32_t)C::BN - 1 || p + 1 == a.P || c + 1 == a.Wo;
+            const uint32_t nv = last ? (uint32_t)C::KW : a.ms;
+            for (uint32_t v = 0; v < nv; ++v)
+                tbl[R + v] = k * a.L + (c * a.s + v) * a.T;
+        }
+    }
+    __syncthreads();
+
+    // Per-lane load offsets, fixed for the whole tile.
+#pragma unroll
+    for (int i = 0; i < C::IB; ++i) {
+        const uint32_t b = w.wave + C::NW * i;
+        const uint32_t row = b * C::RPI + w.lane / C::CH;
+        const uint32_t c = (w.lane % C::CH) ^ sw<C>(row);
+        w.boff[i] = kOOB;
+        w.bcm[i] = 0;
+        if (row < (uint32_t)C::AROWS) {
+            const uint32_t v = row / C::BM, jl = row % C::BM;
+            w.boff[i] = ((jl * C::KW + v) * a.Tp + 8 * c) * 2u;
+        } else if (row < (uint32_t)C::ROWS) {
+            const uint32_t e = tbl[row - C::AROWS];
+            if (e != kNoCol)
+                w.boff[i] = (e + 8 * c) * 2u;
+            w.bcm[i] = 8 * c;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < C::WN; ++j) {
+        const uint32_t n = w.wn * 32 * C::WN + 32 * j + (w.lane & 31);
+        const uint32_t p = p0 + n;
+        // a pixel past P reads row 0 (its result is never stored)
+        w.Rj[j] = p < a.P ? n * a.ms + (fdiv(p, a.div_Wo) - q0) * kwm : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::WN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                w.acc[i][j][e] = 0.f;
+
+    // prologue: stages 0 .. NS-2 into slots 0 .. NS-2; stage st then sits
+    // in slot st % NS
+    w.issue(0, r0);
+    if constexpr (C::NS == 2) {
+        for (uint32_t st = 0; st < w.nst; st += 2) {
+            w.step(st, r0, r1);
+            w.step(st + 1, r1, r0);
+        }
+    } else if constexpr (C::NS == 3) {
+        w.issue(1, r1);
+        for (uint32_t st = 0; st < w.nst; st += 3) {
+            w.step(st, r0, r2);
+            w.step(st + 1, r1, r0);
+            w.step(st + 2, r2, r1);
+        }
+    } else {
+        w.issue(1, r1);
+        w.issue(2, r2);
+        for (uint32_t st = 0; st < w.nst; st += 4) {
+            w.step(st, r0, r3);
+            w.step(st + 1, r1, r0);
+            w.step(st + 2, r2, r1);
+            w.step(st + 3, r3, r2);
+        }
+    }
+    // no load may still be writing LDS when the workgroup ends
+    wait_vmcnt<0>();
+
+    // Epilogue: lane holds pixel pb + 32*j + (lane & 31) and, for element e
+    // of block (i, j), channel cb + 32*i + 8*(e/4) + 4*(lane/32) + e%4.
+    const uint32_t pb = p0 + w.wn * 32 * C::WN, cb = ch0 + w.wm * 32 * C::WM;
+#pragma unroll
+    for (int j = 0; j < C::WN; ++j) {
+        const uint32_t p = pb + 32 * j + (w.lane & 31);
+        if (p >= a.P)
+            continue;
+        uint16_t *o = a.out + (uint64_t)p * a.Co;
+#pragma unroll
+        for (int i = 0; i < C::WM; ++i) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const uint32_t c = cb + 32 * i + 8 * g + 4 * (w.lane >> 5);
+                uint32_t h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const _Float16 v = (_Float16)w.acc[i][j][4 * g + e];
+                    h[e] = __builtin_bit_cast(uint16_t, v);
+                }
+                if (c + 3 < a.Co && (a.Co & 3) == 0) {
+                    *reinterpret_cast<uint2 *>(o + c) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (c + e < a.Co)
+                            o[c + e] = (uint16_t)h[e];
+                }
+            }
+        }
+    }
+}
+
+struct ColVariant {
+    const char *name;
+    const void *f;
+    int kw, bm, bn, nrmax;
+};
+
+template <int KW, int BT, int WM, int WN, int WGM, int WGN, int NRMAX, int NS>
+ColVariant col_variant(const char *name)
+{
+    using C = ColCfg<KW, BT, WM, WN, WGM, WGN, NRMAX, NS>;
+    return ColVariant{name, (const void *)&conv_fp16_col<C>, KW, C::BM, C::BN, NRMAX};
+}
+
+const ColVariant *col_variants(int *n)
+{
+    // name: filter width, channels x pixels per tile, taps per stage, ring slots
+    static const ColVariant v[] = {
+        col_variant<3, 32, 2, 2, 1, 4, 288, 2>("k3c64p256t32s2"),
+        col_variant<3, 16, 2, 4, 2, 2, 288, 3>("k3c128p256t16s3"),
+        col_variant<7, 16, 2, 2, 1, 4, 544, 3>("k7c64p256t16s3"),
+    };
+    *n = (int)(sizeof v / sizeof v[0]);
+    return v;
+}
+
+// Rows a tile of bn consecutive pixels needs at most: each strip run of c
+// pixels needs (c-1)*ms + K_w rows, and bn pixels span at most
+// ceil((bn-1)/W_o) + 1 runs.
+int64_t col_rows_needed(const Shape &sh, int bn)
+{
+    const int64_t ms = sh.s < sh.Kw ? sh.s : sh.Kw;
+    int64_t runs = (bn - 1 + sh.Wo - 1) / sh.Wo + 1;
+    if (runs > bn)
+        runs = bn;
+    return (bn - runs) * ms + runs * sh.Kw;
+}
+
+}  // namespace
+
+int col_plan(const Shape &sh)
+{
+    if (sh.Ci % 8 != 0)
+        return -1;  // windows not 16-byte aligned
+    if (const char *e = getenv("IM2WIN_FP16_KERNEL"))
+        if (strcmp(e, "pipe") == 0)
+            return -1;
+    int n;
+    const ColVariant *v = col_variants(&n);
+    int pick = -1;
+    if (const char *e = getenv("IM2WIN_FP16_COL")) {
+        for (int t = 0; t < n; ++t)
+            if (strcmp(e, v[t].name) == 0)
+                pick = t;
+    }
+    if (pick < 0) {
+        // Defaults, measured per layer on MI355X: the column-staged kernel
+        // wins where the window rows dominate a stage (C_o <= 128); with
+        // more channels the K_w*BM filter rows of a stage dominate it and the
+        // row-per-pixel kernel, whose stages hold 64 taps of BM filter rows,
+        // is faster.
+        const char *name = nullptr;
+        if (sh.Kw == 3 && sh.Co <= 128)
+            name = "k3c64p256t32s2";
+        else if (sh.Kw == 7 && sh.Co <= 128)
+            name = "k7c64p256t16s3";
+        else
+            return -1;
+        for (int t = 0; t < n; ++t)
+            if (strcmp(name, v[t].name) == 0)
+                pick = t;
+    }
+    if (pick < 0 || v[pick].kw != sh.Kw)
+        return -1;
+    if (col_rows_needed(sh, v[pick].bn) > v[pick].nrmax)
+        return -1;
+    // the filter rows of one tile are addressed with 31-bit offsets
+    if ((int64_t)v[pick].bm * sh.Kw * sh.Tp * 2 >= (int64_t)kMaxRecords)
+        return -1;
+    // every offset inside a tile must fit 31 bits (checked per layer: the
+    // strips of one tile plus the last column's slice)
+    const int64_t strips_per_tile = (v[pick].bn - 1) / sh.Wo + 2;
+    if ((strips_per_tile * sh.L + sh.Tp) * 2 >= (int64_t)kOOB)
+        return -1;
+    return pick;
+}
+
+hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const void *packed,
+                                uint16_t *out, hipStream_t st)
+{
+    int n;
+    const ColVariant &v = col_variants(&n)[plan];
+    ColArgs a;
+    a.ws = static_cast<const uint16_t *>(ws);
+    a.packed = static_cast<const uint16_t *>(packed);
+    a.out = out;
+    a.win_bytes = (uint64_t)sh.win_bytes;
+    a.pk_bytes = (uint64_t)sh.Co_pad * sh.Kw * sh.Tp * 2;
+    a.P = (uint32_t)sh.P; a.Co = (uint32_t)sh.Co; a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L;
+    a.T = (uint32_t)(sh.Kh * sh.Ci); a.Tp = (uint32_t)sh.Tp; a.s = (uint32_t)sh.s;
+    a.ms = (uint32_t)(sh.s < sh.Kw ? sh.s : sh.Kw);
+    a.nst = 0;
+    a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
+    void *args[] = {&a};
+    dim3 grid((uint32_t)((sh.P + v.bn - 1) / v.bn), (uint32_t)((sh.Co + v.bm - 1) / v.bm));
+    return hipLaunchKernel(v.f, grid, dim3(256), args, 0, st);
+}
+
+}  // namespace im2win

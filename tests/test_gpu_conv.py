@@ -39,6 +39,11 @@ EDGE = list(TINY) + [
     (5, 3, 40, 37, 96, 11, 11, 4),    # stem-like, K = 363
     (1, 130, 6, 6, 20, 3, 3, 1),      # K = 1170
     (300, 1, 3, 3, 5, 2, 2, 1),       # many tiny images: tiles span many strips
+    # column-staged fp16 kernel: strip runs inside a tile, taps past K_h*C_i
+    # inside the last stage, ragged pixel and channel tiles
+    (3, 24, 11, 30, 72, 3, 3, 1),     # K_h*C_i = 72: last stage 8 of 32 taps
+    (2, 16, 21, 40, 40, 3, 3, 1),     # K_h*C_i = 48
+    (1, 8, 13, 120, 20, 7, 7, 2),     # K_w = 7, stride 2: 2 new columns per pixel
 ]
 
 
@@ -59,7 +64,7 @@ def test_conv_edge_shapes(shape, dtype):
 
 
 @pytest.mark.parametrize("dtype", DTYPES, ids=DT_IDS)
-@pytest.mark.parametrize("shape", EDGE[-9:], ids=_id)
+@pytest.mark.parametrize("shape", EDGE[-12:], ids=_id)
 def test_conv_integer_inputs_exact(shape, dtype):
     """Inputs in {-2..2}: every partial sum is an integer below 2^24, so any
     summation order gives the exact result."""
@@ -133,3 +138,19 @@ def test_fp16_rounding_once():
     run = Run(x, w, 1, torch.float16)
     ref = oracle.conv(x.double().numpy(), w.double().numpy(), 1)
     assert np.array_equal(run.out_np(), ref)
+
+
+# The fp16 path has two kernels: windows staged per input column (the
+# default for K_w in {3, 7} with C_o <= 128, when a tile's columns fit) and
+# windows staged per pixel row (every other layer).  IM2WIN_FP16_KERNEL=pipe
+# forces the second, so both are checked on the shapes that select the first.
+@pytest.mark.parametrize("shape", EDGE[-3:] + [(2, 64, 24, 24, 64, 3, 3, 1)], ids=_id)
+def test_fp16_row_kernel_on_column_shapes(shape, monkeypatch):
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    say("conv fp16 row kernel", shape)
+    monkeypatch.setenv("IM2WIN_FP16_KERNEL", "pipe")
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=13)
+    run = Run(x, w, s, torch.float16)
+    check_full(run, x, w)
+    run.check_out_guards()
+
