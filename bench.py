@@ -35,21 +35,27 @@ PEAK_FP16_MFMA_TF = 2516.6      # dense
 # HBM-side bytes per launch of the fp32 conv kernel, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE counters (FETCH_SIZE scaled by 2.0 and WRITE_SIZE by 1.0, the
 # factors a plain 1 GiB copy gives), keyed by layer.  They hold only for the
-# kernel source they were taken on, identified by its SHA-256; after any change
-# to that source the figure is reported as null until measured again.
-# Source: profiles/cfg2_n128_c64_56_3x3.md.
+# kernel sources they were taken on, identified by SHA-256 over FP32_SOURCES;
+# after any change to those sources the figure is reported as null until
+# measured again.  Source: profiles/cfg2_n128_c64_56_3x3.md.
+FP32_SOURCES = ("conv_fp32.hip", "conv_fp32_dma.hip")
 FP32_CONV_TRAFFIC = {
-    "source_sha256": "5e7e8614f5b13eb79b86443bbfdf47f833dacc77024aac1fbe93c71d86b7ed71",
-    "bytes": {"cfg2_n128_c64_56_3x3": 943.8e6 + 96.0e6},
+    "source_sha256": None,
+    "bytes": {},
 }
 
 
-def fp32_conv_traffic(layer_name):
+def fp32_sources_sha256():
     import hashlib
-    src = os.path.join(ROOT, "paper_2608_20725_amd", "csrc", "conv_fp32.hip")
-    with open(src, "rb") as f:
-        digest = hashlib.sha256(f.read()).hexdigest()
-    if digest != FP32_CONV_TRAFFIC["source_sha256"]:
+    h = hashlib.sha256()
+    for name in FP32_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_20725_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def fp32_conv_traffic(layer_name):
+    if fp32_sources_sha256() != FP32_CONV_TRAFFIC["source_sha256"]:
         return None
     return FP32_CONV_TRAFFIC["bytes"].get(layer_name)
 
@@ -233,7 +239,7 @@ def main():
                                                             l.K_w, l.stride, l.dist),
                        "global_batch": l.N, "parallelism": "single GPU"},
             "roofline": {
-                "kernel": "conv_fp32_kernel (fp32 windowed conv, VALU)",
+                "kernel": "conv_fp32_dma (fp32 windowed conv, VALU)",
                 "bound": "alu",
                 "achieved": round(tf32, 3),
                 "peak": PEAK_FP32_VECTOR_TF,

@@ -103,6 +103,11 @@ hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream
 hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hipStream_t st);
 hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed, float *out,
                             hipStream_t st);
+// fp32 kernel with stages loaded straight into LDS: the variant for this
+// layer, or -1 when the register-staged kernel runs instead.
+int dma32_plan(const Shape &sh);
+hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const void *ws, const void *packed,
+                                float *out, hipStream_t st);
 hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed, hipStream_t st);
 hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed, uint16_t *out,
                             hipStream_t st);

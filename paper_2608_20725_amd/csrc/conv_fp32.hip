@@ -495,6 +495,9 @@ hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hi
 hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed, float *out,
                             hipStream_t st)
 {
+    const int plan = dma32_plan(sh);
+    if (plan >= 0)
+        return launch_conv_fp32_dma(sh, plan, ws, packed, out, st);
     C32Args a;
     a.ws = static_cast<const float *>(ws);
     a.packed = static_cast<const float *>(packed);

@@ -1,0 +1,332 @@
+// fp32 windowed convolution on the gfx950 vector ALUs, stages loaded straight
+// into LDS (Sec. III-C, Eq. 3).
+//
+//   O[p][j] = sum_{k<K} Wn[p][k] * F'[k][j]
+//
+// Wn[p][.] is the window of output pixel p (a contiguous span of its strip,
+// Eq. 3) and F' the filter repacked into window tap order, [K_pad32][C_o_pad32]
+// (pack_filter_fp32).
+//
+// Work split (wave64, four waves):
+//   * a lane keeps a TM x TN block of fp32 accumulators (TM pixels, TN
+//     channels); LC lanes of a wave share pixels and split channels, so a
+//     wave covers (64/LC)*TM pixels x LC*TN channels, and the four waves lie
+//     along channels or pixels so that a workgroup covers 64 channels; lane
+//     group g of a wave owns pixels g, g + 64/LC, g + 2*64/LC, ...;
+//   * a stage is 16 taps.  The windows of the workgroup's pixels for those
+//     taps (64 bytes per pixel) and the stage's 16 x 64 filter slab are
+//     fetched with buffer_load ... lds, which writes each lane's 16 bytes
+//     straight to LDS: no staging registers and no transposing stores, and
+//     the ring of NS slots keeps NS-1 stages in flight;
+//   * per group of 4 taps a lane reads its TM pixels' 4-tap quads (TM 16-byte
+//     reads) and, per tap, its TN filter values (TN/4 16-byte reads), then
+//     does 4*TM*TN FMAs with every operand in VGPRs: (TM + TN) LDS reads per
+//     4*TM*TN FMAs.  LDS read instructions, not FMAs, bound the simpler
+//     tilings on this part, so the tile trades them against registers.
+// Window rows in LDS are [pixel][16 taps] = 64 bytes; quad q of pixel p sits
+// at slot q ^ (p & 3), so the 16 lanes that read quad q of 16 consecutive
+// pixels hit all 64 banks.  Taps past K read zero (masked loads) against zero
+// filter rows (padding), so they add exactly 0.
+#include "common.hpp"
+
+#include <stdlib.h>
+#include <string.h>
+
+namespace im2win {
+namespace {
+
+typedef __attribute__((address_space(3))) void *lds_ptr;
+
+struct D32Args {
+    const float *ws;
+    const float *packed;  // F' [K_pad32][Co_pad32]
+    float *out;
+    uint64_t win_bytes;
+    uint32_t P, K, K_pad, Co, Co_pad, Wo, L, S;
+    FastDiv div_Wo;
+};
+
+// Lane tile TM pixels x TN channels; LC lanes of a wave share pixels and
+// split channels, so a wave covers (64/LC)*TM pixels x LC*TN channels; WCH of
+// the four waves lie along channels and the rest along pixels.
+template <int TM_, int TN_, int LC_, int WCH_, int NS_>
+struct DCfg {
+    static constexpr int TM = TM_, TN = TN_, LC = LC_, WCH = WCH_, NS = NS_, KC = 16;
+    static constexpr int NW = 4, NT = 256;
+    static constexpr int WPX = NW / WCH;          // waves along pixels
+    static constexpr int LP = 64 / LC;            // lane groups along pixels
+    static constexpr int WBM = LP * TM;           // pixels per wave
+    static constexpr int BM = WPX * WBM;          // pixels per workgroup
+    static constexpr int CW = WCH * LC * TN;      // channels per workgroup
+    static_assert(TN % 4 == 0 && NW % WCH == 0, "tile");
+    static_assert(CW == 64, "the filter slab loads cover 64 channels");
+    static constexpr int WBYTES = BM * KC * 4;    // window part of a stage
+    static constexpr int FBYTES = KC * CW * 4;    // filter part of a stage
+    static constexpr int STAGE = WBYTES + FBYTES;
+    static constexpr int IW = WBYTES / 1024 / NW;  // window loads per wave per stage
+    static constexpr int IF = FBYTES / 1024 / NW;  // filter loads per wave per stage
+    static constexpr int IB = IW + IF;
+    static_assert(WBYTES % (1024 * NW) == 0 && FBYTES % (1024 * NW) == 0, "even split over waves");
+    static_assert(NS >= 2 && NS <= 3, "ring depth");
+    static_assert((NS - 2) * IB <= 63, "vmcnt range");
+};
+
+template <int VM>
+__device__ inline void wait_vmcnt()
+{
+    __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier that leaves the stages in flight alone (__syncthreads()
+// would also wait for them); the explicit vmcnt wait covers the stage read.
+__device__ inline void ring_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <class C>
+struct DTile {
+    __amdgpu_buffer_rsrc_t rw, rf;
+    uint32_t woff[C::IW];  // window byte offset at tap 0 (kOOB: no pixel)
+    uint32_t wk[C::IW];    // first tap of the quad within the stage
+    uint32_t foff[C::IF];  // filter byte offset at tap 0 (kOOB: column past the pad)
+    uint32_t wave, lane, K, Co_pad, nst;
+    float acc[C::TM][C::TN];
+
+    __device__ inline void issue(uint32_t st, char *slot)
+    {
+        const uint32_t k0 = st * C::KC;
+        const bool past = st >= nst;
+#pragma unroll
+        for (int i = 0; i < C::IW; ++i) {
+            const uint32_t b = wave + C::NW * i;
+            const uint32_t off = (!past && k0 + wk[i] < K) ? woff[i] + 4u * k0 : kOOB;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(slot + 1024 * b), 16, off, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < C::IF; ++i) {
+            const uint32_t b = wave + C::NW * i;
+            const uint32_t off = past ? kOOB : foff[i] + 4u * k0 * Co_pad;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rf, (lds_ptr)(slot + C::WBYTES + 1024 * b), 16, off,
+                                                     0, 0, 0);
+        }
+    }
+
+    __device__ inline void compute(const char *slot)
+    {
+        // this lane's channels of tap 0, and its first pixel
+        const char *fs = slot + C::WBYTES + ((wave % C::WCH) * C::LC + lane % C::LC) * C::TN * 4;
+        const uint32_t pl0 = (wave / C::WCH) * C::WBM + lane / C::LC;
+#pragma unroll
+        for (int q = 0; q < C::KC / 4; ++q) {
+            float x[C::TM][4];
+#pragma unroll
+            for (int t = 0; t < C::TM; ++t) {
+                const uint32_t p = pl0 + C::LP * t;
+                const float4 v = *reinterpret_cast<const float4 *>(slot + p * 64 + 16 * (q ^ (p & 3)));
+                x[t][0] = v.x;
+                x[t][1] = v.y;
+                x[t][2] = v.z;
+                x[t][3] = v.w;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                float f[C::TN];
+#pragma unroll
+                for (int c = 0; c < C::TN; c += 4) {
+                    const float4 v =
+                        *reinterpret_cast<const float4 *>(fs + (4 * q + e) * C::CW * 4 + 4 * c);
+                    f[c] = v.x;
+                    f[c + 1] = v.y;
+                    f[c + 2] = v.z;
+                    f[c + 3] = v.w;
+                }
+#pragma unroll
+                for (int t = 0; t < C::TM; ++t)
+#pragma unroll
+                    for (int c = 0; c < C::TN; ++c)
+                        acc[t][c] = __builtin_fmaf(x[t][e], f[c], acc[t][c]);
+            }
+        }
+    }
+
+    template <int N>
+    __device__ inline void step(uint32_t st, char (&cur)[N], char (&next)[N])
+    {
+        wait_vmcnt<(C::NS - 2) * C::IB>();
+        ring_barrier();
+        issue(st + C::NS - 1, next);
+        if (st < nst)
+            compute(cur);
+    }
+};
+
+template <class C>
+__global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
+{
+    constexpr int S2 = C::NS > 2 ? C::STAGE : 1024;
+    __shared__ __attribute__((aligned(1024))) char r0[C::STAGE];
+    __shared__ __attribute__((aligned(1024))) char r1[C::STAGE];
+    __shared__ __attribute__((aligned(1024))) char r2[S2];
+
+    DTile<C> w;
+    const uint32_t tid = threadIdx.x;
+    w.lane = tid & 63;
+    w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    __builtin_assume(w.wave < (uint32_t)C::NW);
+    w.K = a.K;
+    w.Co_pad = a.Co_pad;
+    w.nst = a.K_pad / C::KC;
+    const uint32_t p0 = blockIdx.x * C::BM;
+    const uint32_t jb = blockIdx.y * C::CW;  // first channel of the workgroup
+
+    // windows are addressed from the strip of p0 on
+    const uint32_t q0 = fdiv(p0, a.div_Wo);
+    const uint64_t tb = (uint64_t)q0 * a.L;
+    const uint64_t left = a.win_bytes - tb * 4;
+    w.rw = make_rsrc(a.ws + tb, (uint32_t)(left < kMaxRecords ? left : kMaxRecords));
+    const uint64_t fbytes = (uint64_t)a.K_pad * a.Co_pad * 4;
+    w.rf = make_rsrc(a.packed, (uint32_t)(fbytes < kMaxRecords ? fbytes : kMaxRecords));
+
+    // Window load i of this wave fills pixels 16*b .. 16*b+15 (b = wave + 4i),
+    // lane -> pixel 16*b + lane/4, LDS slot lane%4, which holds quad
+    // (lane%4) ^ (pixel & 3) of the pixel's 16 stage taps.
+#pragma unroll
+    for (int i = 0; i < C::IW; ++i) {
+        const uint32_t b = w.wave + C::NW * i;
+        const uint32_t pl = 16 * b + w.lane / 4;
+        const uint32_t qd = (w.lane % 4) ^ (pl & 3);
+        const uint32_t p = p0 + pl;
+        w.wk[i] = 4 * qd;
+        w.woff[i] = kOOB;
+        if (p < a.P) {
+            const uint32_t q = fdiv(p, a.div_Wo);
+            w.woff[i] = ((q - q0) * a.L + (p - q * a.Wo) * a.S + 4 * qd) * 4u;
+        }
+    }
+    // Filter load i fills taps 4*b .. 4*b+3 of the slab (b = wave + 4i): lane
+    // -> tap 4*b + lane/16, channels jb + 4*(lane%16) .. +3.
+#pragma unroll
+    for (int i = 0; i < C::IF; ++i) {
+        const uint32_t b = w.wave + C::NW * i;
+        const uint32_t row = 4 * b + w.lane / 16, col = jb + 4 * (w.lane % 16);
+        w.foff[i] = col < a.Co_pad ? (row * a.Co_pad + col) * 4u : kOOB;
+    }
+#pragma unroll
+    for (int t = 0; t < C::TM; ++t)
+#pragma unroll
+        for (int c = 0; c < C::TN; ++c)
+            w.acc[t][c] = 0.f;
+
+    w.issue(0, r0);
+    if constexpr (C::NS == 2) {
+        for (uint32_t st = 0; st < w.nst; st += 2) {
+            w.step(st, r0, r1);
+            w.step(st + 1, r1, r0);
+        }
+    } else {
+        w.issue(1, r1);
+        for (uint32_t st = 0; st < w.nst; st += 3) {
+            w.step(st, r0, r2);
+            w.step(st + 1, r1, r0);
+            w.step(st + 2, r2, r1);
+        }
+    }
+    // no load may still be writing LDS when the workgroup ends
+    wait_vmcnt<0>();
+
+    // first channel of this lane
+    const uint32_t jw = jb + ((w.wave % C::WCH) * C::LC + w.lane % C::LC) * C::TN;
+    if (jw >= a.Co)
+        return;
+    const uint32_t pl0 = (w.wave / C::WCH) * C::WBM + w.lane / C::LC;
+#pragma unroll
+    for (int t = 0; t < C::TM; ++t) {
+        const uint32_t p = p0 + pl0 + C::LP * t;
+        if (p >= a.P)
+            continue;
+        float *o = a.out + (uint64_t)p * a.Co + jw;
+        if (jw + C::TN <= a.Co && (a.Co & 3) == 0) {
+#pragma unroll
+            for (int c = 0; c < C::TN; c += 4)
+                *reinterpret_cast<float4 *>(o + c) =
+                    make_float4(w.acc[t][c], w.acc[t][c + 1], w.acc[t][c + 2], w.acc[t][c + 3]);
+        } else {
+#pragma unroll
+            for (int c = 0; c < C::TN; ++c)
+                if (jw + c < a.Co)
+                    o[c] = w.acc[t][c];
+        }
+    }
+}
+
+struct DVariant {
+    const char *name;
+    const void *f;
+    int bm, cw;
+};
+
+template <int TM, int TN, int LC, int WCH, int NS>
+DVariant d_variant(const char *name)
+{
+    using C = DCfg<TM, TN, LC, WCH, NS>;
+    return DVariant{name, (const void *)&conv_fp32_dma<C>, C::BM, C::CW};
+}
+
+const DVariant *d_variants(int *n)
+{
+    // name: pixels x channels per lane, lanes along channels, ring slots
+    static const DVariant v[] = {
+        d_variant<4, 16, 1, 4, 2>("p4c16l1s2"),
+        d_variant<8, 8, 8, 1, 2>("p8c8l8s2"),
+        d_variant<8, 8, 8, 1, 3>("p8c8l8s3"),
+        d_variant<8, 16, 4, 1, 2>("p8c16l4s2"),
+    };
+    *n = (int)(sizeof v / sizeof v[0]);
+    return v;
+}
+
+}  // namespace
+
+int dma32_plan(const Shape &sh)
+{
+    if (sh.Ci % 4 != 0)
+        return -1;  // windows not 16-byte aligned
+    if (sh.K_pad32 * sh.Co_pad32 * 4 > (int64_t)kMaxRecords)
+        return -1;  // filter offsets need 31 bits
+    int n;
+    const DVariant *v = d_variants(&n);
+    const char *name = "p8c8l8s2";
+    if (const char *e = getenv("IM2WIN_FP32_KERNEL")) {
+        if (strcmp(e, "regs") == 0)
+            return -1;
+        name = e;
+    }
+    for (int t = 0; t < n; ++t)
+        if (strcmp(name, v[t].name) == 0)
+            return t;
+    return 0;
+}
+
+hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const void *ws, const void *packed,
+                                float *out, hipStream_t st)
+{
+    int n;
+    const DVariant &v = d_variants(&n)[plan];
+    D32Args a;
+    a.ws = static_cast<const float *>(ws);
+    a.packed = static_cast<const float *>(packed);
+    a.out = out;
+    a.win_bytes = (uint64_t)sh.win_bytes;
+    a.P = (uint32_t)sh.P; a.K = (uint32_t)sh.K; a.K_pad = (uint32_t)sh.K_pad32;
+    a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
+    a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.S = (uint32_t)sh.S;
+    a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
+    void *args[] = {&a};
+    dim3 grid((uint32_t)((sh.P + v.bm - 1) / v.bm), (uint32_t)((sh.Co + v.cw - 1) / v.cw));
+    return hipLaunchKernel(v.f, grid, dim3(256), args, 0, st);
+}
+
+}  // namespace im2win
