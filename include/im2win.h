@@ -111,7 +111,10 @@ int64_t conv_im2col_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
  *            the window tensor and the zero pad are written, the rest of the
  *            workspace is left alone
  * The copy is bit-exact and does not depend on the element type beyond its
- * size.  C_o and K_w only size the workspace check.
+ * size.  C_o and K_w only size the workspace check.  Besides the ranges of
+ * conv_workspace_bytes, the window tensor must hold fewer than 2^32 16-byte
+ * granules when C_i*elt is a multiple of 16 bytes, else fewer than 2^32
+ * elements (IM2WIN_ERANGE).
  */
 int conv_im2win_transform(const void *in_nhwc, void *ws, int64_t ws_bytes,
                           int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,

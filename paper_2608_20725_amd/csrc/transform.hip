@@ -6,8 +6,9 @@
 // a 16-byte store; the K_h/s-fold re-reads of input rows are served by L2 and
 // the Infinity Cache.  Two kernels:
 //   * vec:    C_i*elt is a multiple of 16 bytes.  A thread copies whole
-//             16-byte granules; one workgroup covers a contiguous run of one
-//             strip, so the stores of a wave are one contiguous 1 KiB run.
+//             16-byte granules; a workgroup covers a contiguous run of the
+//             window tensor (possibly across strips), so the stores of a wave
+//             are one contiguous 1 KiB run, in an XCD-aware block order.
 //   * gather: any other C_i (e.g. the 3-channel stem layers).  A thread
 //             assembles one 16-byte granule of the flat window tensor element
 //             by element; granules may straddle strips.
@@ -30,7 +31,7 @@ struct TArgs {
     uint64_t win_elems;
     uint64_t win_bytes, pad_end;
     uint64_t grans;          // gather: 16-byte granules of the window tensor
-    FastDiv div_Ci, div_Kh, div_Wi, div_Ho, div_L;
+    FastDiv div_Ci, div_Kh, div_Wi, div_Ho, div_L, div_gps;
 };
 
 __device__ inline void zero_pad(const TArgs &a)
@@ -40,33 +41,43 @@ __device__ inline void zero_pad(const TArgs &a)
         a.ws[b] = 0;
 }
 
+// XCD-aware block order: the hardware deals the blocks of a launch to the 8
+// XCDs round-robin (block b to XCD b % 8), and each XCD has its own L2.  Block
+// b works on logical block xcd_block(b), so that every XCD walks one
+// contiguous run of the window tensor: strips that share input rows are then
+// copied by the same XCD at about the same time and the re-reads hit its L2.
+// A bijection on [0, nb).
+__device__ inline uint32_t xcd_block(uint32_t b, uint32_t nb)
+{
+    const uint32_t x = b % 8, j = b / 8;
+    const uint32_t per = nb / 8, rem = nb % 8;
+    return x * per + (x < rem ? x : rem) + j;
+}
+
 template <int ELT>
 __global__ __launch_bounds__(kThreads) void transform_vec(TArgs a)
 {
     constexpr uint32_t V = 16 / ELT;  // elements per granule
-    // strip index q over gridDim.y * gridDim.z
-    const uint32_t q = blockIdx.y + blockIdx.z * gridDim.y;
-    if (q >= a.strips)
-        return;
-    if (q == 0 && blockIdx.x == 0)
+    if (blockIdx.x == 0)
         zero_pad(a);
-    const uint32_t i = fdiv(q, a.div_Ho);
-    const uint32_t m = q - i * a.Ho;
-    const char *img = a.in + (uint64_t)i * a.Hi * a.Wi * a.Ci * ELT;
-    char *strip = a.ws + (uint64_t)q * a.L * ELT;
-    const uint32_t g0 = blockIdx.x * (kThreads * kGranPerThread) + threadIdx.x;
+    // granules of the whole window tensor, numbered strip by strip
+    // (granule counts fit 32 bits: transform_range_ok)
+    const uint32_t gb = xcd_block(blockIdx.x, gridDim.x) * (kThreads * kGranPerThread);
 #pragma unroll
     for (int t = 0; t < kGranPerThread; ++t) {
-        const uint32_t g = g0 + t * kThreads;
-        if (g < a.gran_per_strip) {
-            const uint32_t pos = g * V;                // element within the strip
+        const uint32_t g = gb + t * kThreads + threadIdx.x;
+        if (g < a.grans) {
+            const uint32_t q = fdiv(g, a.div_gps);  // strip
+            const uint32_t pos = (g - q * a.gran_per_strip) * V;
+            const uint32_t i = fdiv(q, a.div_Ho);
+            const uint32_t m = q - i * a.Ho;
             const uint32_t seg = fdiv(pos, a.div_Ci);  // k*K_h + u
             const uint32_t r = pos - seg * a.Ci;
             const uint32_t k = fdiv(seg, a.div_Kh);
             const uint32_t u = seg - k * a.Kh;
-            const uint64_t src = ((uint64_t)(m * a.s + u) * a.Wi + k) * a.Ci + r;
-            const uint4 v = *reinterpret_cast<const uint4 *>(img + src * ELT);
-            *reinterpret_cast<uint4 *>(strip + (uint64_t)pos * ELT) = v;
+            const uint64_t src = (((uint64_t)i * a.Hi + m * a.s + u) * a.Wi + k) * a.Ci + r;
+            const uint4 v = *reinterpret_cast<const uint4 *>(a.in + src * ELT);
+            *reinterpret_cast<uint4 *>(a.ws + (uint64_t)g * 16) = v;
         }
     }
 }
@@ -136,8 +147,8 @@ __global__ __launch_bounds__(kThreads) void transform_gather(TArgs a)
 
 bool transform_range_ok(const Shape &sh)
 {
-    if ((sh.Ci * sh.elt) % 16 == 0)
-        return true;
+    if ((sh.Ci * sh.elt) % 16 == 0)  // granule indices fit 32 bits
+        return (uint64_t)sh.win_bytes / 16 + kThreads * kGranPerThread < (1ull << 32);
     return (uint64_t)sh.win_elems + 16 < (1ull << 32);
 }
 
@@ -162,15 +173,14 @@ hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream
     const bool vec = (sh.Ci * sh.elt) % 16 == 0;
     if (vec) {
         a.gran_per_strip = (uint32_t)(sh.L * sh.elt / 16);
-        a.grans = 0;
-        const uint32_t per_block = kThreads * kGranPerThread;
-        dim3 grid((a.gran_per_strip + per_block - 1) / per_block, 1, 1);
-        // strips over y (<= 65535) and z
-        uint32_t gy = a.strips < 65535u ? a.strips : 65535u;
-        grid.y = gy;
-        grid.z = (a.strips + gy - 1) / gy;
+        a.div_gps = make_fastdiv(a.gran_per_strip);
+        a.grans = (uint64_t)sh.win_bytes / 16;
+        const uint64_t per_block = kThreads * kGranPerThread;
+        const uint64_t blocks = (a.grans + per_block - 1) / per_block;
+        if (blocks > 0x7fffffffull)
+            return hipErrorInvalidValue;
         const void *f = sh.elt == 4 ? (const void *)&transform_vec<4> : (const void *)&transform_vec<2>;
-        return hipLaunchKernel(f, grid, dim3(kThreads), args, 0, st);
+        return hipLaunchKernel(f, dim3((uint32_t)blocks), dim3(kThreads), args, 0, st);
     }
     // gather: element indices fit 32 bits (transform_range_ok)
     a.gran_per_strip = 0;
