@@ -49,9 +49,11 @@ struct D32Args {
 // Lane tile TM pixels x TN channels; LC lanes of a wave share pixels and
 // split channels, so a wave covers (64/LC)*TM pixels x LC*TN channels; WCH of
 // the four waves lie along channels and the rest along pixels.
-template <int TM_, int TN_, int LC_, int WCH_, int NS_>
+template <int TM_, int TN_, int LC_, int WCH_, int NS_, int KC_ = 16>
 struct DCfg {
-    static constexpr int TM = TM_, TN = TN_, LC = LC_, WCH = WCH_, NS = NS_, KC = 16;
+    static constexpr int TM = TM_, TN = TN_, LC = LC_, WCH = WCH_, NS = NS_, KC = KC_;
+    static constexpr int QPR = KC / 4;            // 16-byte quads per window row
+    static constexpr int PPI = 64 / QPR;          // pixels per window load
     static constexpr int NW = 4, NT = 256;
     static constexpr int WPX = NW / WCH;          // waves along pixels
     static constexpr int LP = 64 / LC;            // lane groups along pixels
@@ -62,11 +64,14 @@ struct DCfg {
     static_assert(CW == 64, "the filter slab loads cover 64 channels");
     static constexpr int WBYTES = BM * KC * 4;    // window part of a stage
     static constexpr int FBYTES = KC * CW * 4;    // filter part of a stage
-    static constexpr int STAGE = WBYTES + FBYTES;
     static constexpr int IW = WBYTES / 1024 / NW;  // window loads per wave per stage
-    static constexpr int IF = FBYTES / 1024 / NW;  // filter loads per wave per stage
+    // filter loads per wave per stage; loads past the slab read nothing into
+    // a spare 1 KiB block, so every wave issues the same count
+    static constexpr int IF = (FBYTES / 1024 + NW - 1) / NW;
     static constexpr int IB = IW + IF;
-    static_assert(WBYTES % (1024 * NW) == 0 && FBYTES % (1024 * NW) == 0, "even split over waves");
+    static constexpr int STAGE_ALLOC = WBYTES + NW * IF * 1024;
+    static_assert(WBYTES % (1024 * NW) == 0, "even split over waves");
+    static_assert(KC == 8 || KC == 16, "stage depth");
     static_assert(NS >= 2 && NS <= 3, "ring depth");
     static_assert((NS - 2) * IB <= 63, "vmcnt range");
 };
@@ -108,10 +113,16 @@ struct DTile {
 #pragma unroll
         for (int i = 0; i < C::IF; ++i) {
             const uint32_t b = wave + C::NW * i;
-            const uint32_t off = past ? kOOB : foff[i] + 4u * k0 * Co_pad;
+            const uint32_t off = past ? kOOB : foff[i] + 4u * k0 * Co_pad;  // foff is kOOB past the slab
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rf, (lds_ptr)(slot + C::WBYTES + 1024 * b), 16, off,
                                                      0, 0, 0);
         }
+    }
+
+    // Window quad q of local pixel p sits at slot q ^ swz(p) of its row.
+    __device__ static inline uint32_t wslot(uint32_t p, uint32_t q)
+    {
+        return C::QPR == 4 ? q ^ (p & 3) : q ^ ((p >> 3) & 1);
     }
 
     __device__ inline void compute(const char *slot)
@@ -120,34 +131,30 @@ struct DTile {
         const char *fs = slot + C::WBYTES + ((wave % C::WCH) * C::LC + lane % C::LC) * C::TN * 4;
         const uint32_t pl0 = (wave / C::WCH) * C::WBM + lane / C::LC;
 #pragma unroll
-        for (int q = 0; q < C::KC / 4; ++q) {
-            float x[C::TM][4];
+        for (int q = 0; q < C::QPR; ++q) {
+            // filter values of the quad's 4 taps
+            float f[4][C::TN];
 #pragma unroll
-            for (int t = 0; t < C::TM; ++t) {
-                const uint32_t p = pl0 + C::LP * t;
-                const float4 v = *reinterpret_cast<const float4 *>(slot + p * 64 + 16 * (q ^ (p & 3)));
-                x[t][0] = v.x;
-                x[t][1] = v.y;
-                x[t][2] = v.z;
-                x[t][3] = v.w;
-            }
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                float f[C::TN];
+            for (int e = 0; e < 4; ++e)
 #pragma unroll
                 for (int c = 0; c < C::TN; c += 4) {
                     const float4 v =
                         *reinterpret_cast<const float4 *>(fs + (4 * q + e) * C::CW * 4 + 4 * c);
-                    f[c] = v.x;
-                    f[c + 1] = v.y;
-                    f[c + 2] = v.z;
-                    f[c + 3] = v.w;
+                    f[e][c] = v.x;
+                    f[e][c + 1] = v.y;
+                    f[e][c + 2] = v.z;
+                    f[e][c + 3] = v.w;
                 }
 #pragma unroll
-                for (int t = 0; t < C::TM; ++t)
+            for (int t = 0; t < C::TM; ++t) {
+                const uint32_t p = pl0 + C::LP * t;
+                const float4 v = *reinterpret_cast<const float4 *>(slot + p * (C::KC * 4) + 16 * wslot(p, q));
+                const float x[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
 #pragma unroll
                     for (int c = 0; c < C::TN; ++c)
-                        acc[t][c] = __builtin_fmaf(x[t][e], f[c], acc[t][c]);
+                        acc[t][c] = __builtin_fmaf(x[e], f[e][c], acc[t][c]);
             }
         }
     }
@@ -166,9 +173,9 @@ struct DTile {
 template <class C>
 __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
 {
-    constexpr int S2 = C::NS > 2 ? C::STAGE : 1024;
-    __shared__ __attribute__((aligned(1024))) char r0[C::STAGE];
-    __shared__ __attribute__((aligned(1024))) char r1[C::STAGE];
+    constexpr int S2 = C::NS > 2 ? C::STAGE_ALLOC : 1024;
+    __shared__ __attribute__((aligned(1024))) char r0[C::STAGE_ALLOC];
+    __shared__ __attribute__((aligned(1024))) char r1[C::STAGE_ALLOC];
     __shared__ __attribute__((aligned(1024))) char r2[S2];
 
     DTile<C> w;
@@ -190,14 +197,14 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
     const uint64_t fbytes = (uint64_t)a.K_pad * a.Co_pad * 4;
     w.rf = make_rsrc(a.packed, (uint32_t)(fbytes < kMaxRecords ? fbytes : kMaxRecords));
 
-    // Window load i of this wave fills pixels 16*b .. 16*b+15 (b = wave + 4i),
-    // lane -> pixel 16*b + lane/4, LDS slot lane%4, which holds quad
-    // (lane%4) ^ (pixel & 3) of the pixel's 16 stage taps.
+    // Window load i of this wave fills pixels PPI*b .. PPI*b+PPI-1 (b = wave
+    // + 4i): lane -> pixel PPI*b + lane/QPR, LDS slot lane%QPR, which holds
+    // quad wslot(pixel, lane%QPR) of the pixel's stage taps.
 #pragma unroll
     for (int i = 0; i < C::IW; ++i) {
         const uint32_t b = w.wave + C::NW * i;
-        const uint32_t pl = 16 * b + w.lane / 4;
-        const uint32_t qd = (w.lane % 4) ^ (pl & 3);
+        const uint32_t pl = C::PPI * b + w.lane / C::QPR;
+        const uint32_t qd = DTile<C>::wslot(pl, w.lane % C::QPR);
         const uint32_t p = p0 + pl;
         w.wk[i] = 4 * qd;
         w.woff[i] = kOOB;
@@ -212,7 +219,7 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
     for (int i = 0; i < C::IF; ++i) {
         const uint32_t b = w.wave + C::NW * i;
         const uint32_t row = 4 * b + w.lane / 16, col = jb + 4 * (w.lane % 16);
-        w.foff[i] = col < a.Co_pad ? (row * a.Co_pad + col) * 4u : kOOB;
+        w.foff[i] = (row < (uint32_t)C::KC && col < a.Co_pad) ? (row * a.Co_pad + col) * 4u : kOOB;
     }
 #pragma unroll
     for (int t = 0; t < C::TM; ++t)
@@ -268,21 +275,24 @@ struct DVariant {
     int bm, cw;
 };
 
-template <int TM, int TN, int LC, int WCH, int NS>
+template <int TM, int TN, int LC, int WCH, int NS, int KC>
 DVariant d_variant(const char *name)
 {
-    using C = DCfg<TM, TN, LC, WCH, NS>;
+    using C = DCfg<TM, TN, LC, WCH, NS, KC>;
     return DVariant{name, (const void *)&conv_fp32_dma<C>, C::BM, C::CW};
 }
 
 const DVariant *d_variants(int *n)
 {
-    // name: pixels x channels per lane, lanes along channels, ring slots
+    // name: pixels x channels per lane, lanes along channels, ring slots,
+    // taps per stage
+    // Measured on MI355X over the benchmark layers: 8 x 8 lane tiles with
+    // 16-tap stages beat 4 x 16, 8 x 16, 12 x 8 and 16 x 8 tiles and 8-tap
+    // stages on every layer but one (larger tiles lose occupancy, 8-tap
+    // stages add barriers); 4 x 16 stays for comparison.
     static const DVariant v[] = {
-        d_variant<4, 16, 1, 4, 2>("p4c16l1s2"),
-        d_variant<8, 8, 8, 1, 2>("p8c8l8s2"),
-        d_variant<8, 8, 8, 1, 3>("p8c8l8s3"),
-        d_variant<8, 16, 4, 1, 2>("p8c16l4s2"),
+        d_variant<8, 8, 8, 1, 2, 16>("p8c8l8s2k16"),
+        d_variant<4, 16, 1, 4, 2, 16>("p4c16l1s2k16"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
@@ -298,7 +308,7 @@ int dma32_plan(const Shape &sh)
         return -1;  // filter offsets need 31 bits
     int n;
     const DVariant *v = d_variants(&n);
-    const char *name = "p8c8l8s2";
+    const char *name = "p8c8l8s2k16";
     if (const char *e = getenv("IM2WIN_FP32_KERNEL")) {
         if (strcmp(e, "regs") == 0)
             return -1;
