@@ -40,8 +40,8 @@ PEAK_FP16_MFMA_TF = 2516.6      # dense
 # measured again.  Source: profiles/cfg2_n128_c64_56_3x3.md.
 FP32_SOURCES = ("conv_fp32.hip", "conv_fp32_dma.hip")
 FP32_CONV_TRAFFIC = {
-    "source_sha256": None,
-    "bytes": {},
+    "source_sha256": "865c0f91a264997fc21a95e25821d9886a1b9f7a133fef97e9c19f3d7dfdb68f",
+    "bytes": {"cfg2_n128_c64_56_3x3": 1003.4e6 + 95.6e6},
 }
 
 
