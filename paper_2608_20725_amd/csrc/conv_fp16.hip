@@ -32,6 +32,13 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int BK = 64;       // taps per stage
 constexpr int LDK = BK + 8;  // halves per LDS row: 144 bytes, offsets rows across banks
 
+// How the row-per-pixel register-staged kernel (the one for windows that are
+// not 16-byte aligned) loads a 16-byte granule of window taps: one unaligned
+// load or eight element loads.  The unaligned load measured faster for long
+// windows (K = 363: 248 vs 195 TFLOP/s) and slower for short ones (K = 27:
+// 32 vs 41), so the element loads stay for K < 128.
+constexpr int kLoadUnaligned = 1, kLoadElems = 2;
+
 struct C16Args {
     const uint16_t *ws;      // window tensor (fp16 bits)
     const uint16_t *packed;  // F' [Co_pad][K_pad]
@@ -129,7 +136,7 @@ __device__ inline void store_tile(const floatx16 (&acc)[WM][WN], const C16Args &
 }
 
 // ---------------------------------------------------------------------------
-template <int WM, int WN, int WGM, int WGN, bool ALIGNED>
+template <int WM, int WN, int WGM, int WGN, int LM>
 struct Cfg {
     static constexpr int NT = 64 * WGM * WGN;
     static constexpr int BMc = 32 * WM * WGM;  // channels per workgroup
@@ -142,13 +149,13 @@ struct Cfg {
 };
 
 // One K stage in flight: global -> registers (load), registers -> LDS (store).
-template <int WM, int WN, int WGM, int WGN, bool ALIGNED>
+template <int WM, int WN, int WGM, int WGN, int LM>
 struct Stage16 {
-    using C = Cfg<WM, WN, WGM, WGN, ALIGNED>;
+    using C = Cfg<WM, WN, WGM, WGN, LM>;
     u32x4 fr[C::FPT], wr[C::WPT];
 
-    __device__ inline void load(__amdgpu_buffer_rsrc_t rs, const uint32_t *rowoff, const uint16_t *fb,
-                                uint32_t p0, uint32_t k0, const C16Args &a)
+    __device__ inline void load(__amdgpu_buffer_rsrc_t rs, const uint16_t *wsb, const uint32_t *rowoff,
+                                const uint16_t *fb, uint32_t p0, uint32_t k0, const C16Args &a)
     {
         const uint32_t tid = threadIdx.x;
         // filter rows: always inside the zero-padded packed filter
@@ -167,15 +174,28 @@ struct Stage16 {
             const uint32_t k = k0 + 8 * c8;
             const bool ok = p0 + row < a.P;
             const uint32_t base = (rowoff[row] + k) * 2u;
-            if (ALIGNED) {
-                wr[j] = ld_b128(rs, (ok && k < a.K) ? base : kOOB);
-            } else {
+            if (LM == kLoadElems) {
                 uint32_t h[8];
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
                     h[e] = ld_b16(rs, (ok && k + e < a.K) ? base + 2u * e : kOOB);
                 wr[j] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
                               h[6] | (h[7] << 16)};
+            } else {
+                // One unaligned 16-byte load (gfx950 runs with unaligned
+                // global access enabled; the zero pad after the window tensor
+                // keeps the last load inside the workspace), then the taps
+                // past K are cleared.
+                u32x4 v = {0u, 0u, 0u, 0u};
+                if (ok && k < a.K) {
+                    __builtin_memcpy(&v, reinterpret_cast<const char *>(wsb) + base, 16);
+                    const uint32_t nv = a.K - k;  // taps of this granule inside K
+#pragma unroll
+                    for (int d = 0; d < 4; ++d)
+                        v[d] &= ((uint32_t)(2 * d) < nv ? 0xffffu : 0u) |
+                                ((uint32_t)(2 * d + 1) < nv ? 0xffff0000u : 0u);
+                }
+                wr[j] = v;
             }
         }
     }
@@ -196,10 +216,10 @@ struct Stage16 {
     }
 };
 
-template <int WM, int WN, int WGM, int WGN, bool ALIGNED>
+template <int WM, int WN, int WGM, int WGN, int LM>
 __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
 {
-    using C = Cfg<WM, WN, WGM, WGN, ALIGNED>;
+    using C = Cfg<WM, WN, WGM, WGN, LM>;
     __shared__ __attribute__((aligned(16))) _Float16 Fs[2][C::BMc][LDK];
     __shared__ __attribute__((aligned(16))) _Float16 Ws[2][C::BNp][LDK];
     __shared__ uint32_t rowoff[C::BNp];
@@ -214,8 +234,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
     const uint32_t q0 = fdiv(p0, a.div_Wo);
     const uint64_t tb_elem = (uint64_t)q0 * a.L;
     const uint64_t left = a.win_bytes - tb_elem * 2;
-    const __amdgpu_buffer_rsrc_t rs =
-        make_rsrc(a.ws + tb_elem, (uint32_t)(left < kMaxRecords ? left : kMaxRecords));
+    const uint16_t *wsb = a.ws + tb_elem;
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(wsb, (uint32_t)(left < kMaxRecords ? left : kMaxRecords));
     for (uint32_t t = tid; t < C::BNp; t += C::NT) {
         const uint32_t p = p0 + t;
         uint32_t off = 0;
@@ -228,7 +248,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
     __syncthreads();
 
     const uint16_t *fb = a.packed + (uint64_t)ch0 * a.K_pad;
-    Stage16<WM, WN, WGM, WGN, ALIGNED> stg;
+    Stage16<WM, WN, WGM, WGN, LM> stg;
 
     floatx16 acc[WM][WN];
 #pragma unroll
@@ -240,7 +260,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
                 acc[i][j][e] = 0.f;
 
     const uint32_t nst = a.K_pad / BK;
-    stg.load(rs, rowoff, fb, p0, 0, a);
+    stg.load(rs, wsb, rowoff, fb, p0, 0, a);
     stg.store(Fs[0], Ws[0]);
     __syncthreads();
 
@@ -250,7 +270,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
     for (uint32_t st = 0; st < nst; ++st) {
         const int buf = st & 1;
         if (st + 1 < nst)
-            stg.load(rs, rowoff, fb, p0, (st + 1) * BK, a);
+            stg.load(rs, wsb, rowoff, fb, p0, (st + 1) * BK, a);
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
             half8 af[WM], bf[WN];
@@ -503,10 +523,10 @@ __global__ __launch_bounds__(256) void conv_fp16_pipe(C16Args a)
 }
 
 template <int WM, int WN, int WGM, int WGN>
-void pick_regs(bool aligned, const void **f, int *bm, int *bn)
+void pick_regs(bool unaligned_loads, const void **f, int *bm, int *bn)
 {
-    *f = aligned ? (const void *)&conv_fp16_kernel<WM, WN, WGM, WGN, true>
-                 : (const void *)&conv_fp16_kernel<WM, WN, WGM, WGN, false>;
+    *f = unaligned_loads ? (const void *)&conv_fp16_kernel<WM, WN, WGM, WGN, kLoadUnaligned>
+                         : (const void *)&conv_fp16_kernel<WM, WN, WGM, WGN, kLoadElems>;
     *bm = 32 * WM * WGM;
     *bn = 32 * WN * WGN;
 }
@@ -598,12 +618,13 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
     }
     const void *f;
     int bm, bn;
+    const bool unal = sh.K >= 128;
     if (sh.Co <= 32)
-        pick_regs<1, 2, 1, 4>(false, &f, &bm, &bn);
+        pick_regs<1, 2, 1, 4>(unal, &f, &bm, &bn);
     else if (sh.Co <= 64)
-        pick_regs<2, 2, 1, 4>(false, &f, &bm, &bn);
+        pick_regs<2, 2, 1, 4>(unal, &f, &bm, &bn);
     else
-        pick_regs<2, 2, 2, 2>(false, &f, &bm, &bn);
+        pick_regs<2, 2, 2, 2>(unal, &f, &bm, &bn);
     dim3 grid((uint32_t)((sh.P + bn - 1) / bn), (uint32_t)((sh.Co + bm - 1) / bm));
     return hipLaunchKernel(f, grid, dim3(256), args, 0, st);
 }
