@@ -312,19 +312,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
 // compared with one stage of MFMA work).  Rows past the last pixel and taps
 // past K use an out-of-range offset, for which the load writes zeros.
 //
-// LDS rows are XOR-swizzled: 16-byte chunk c of row r sits in slot c ^ (r & 7),
-// so the 8 lanes that read one chunk of 8 consecutive rows for an MFMA
-// operand touch 8 different slots (all 32 banks).
+// LDS rows are XOR-swizzled: 16-byte chunk c of row r sits in slot
+// c ^ rsw(r), rsw(r) = (r ^ (r >> 3)) & 7, so the 16 lanes that read one
+// chunk of 16 consecutive rows for an MFMA operand touch 16 different 16-byte
+// slots of the 64 banks.  (With c ^ (r & 7), rows r and r+8 collided: bank
+// conflicts measured at 3.8x the LDS instruction cycles.)
 template <int WM, int WN, int WGM, int WGN, int NSTAGE>
 struct PipeCfg {
-    static_assert(WGM * WGN == 4, "four waves per workgroup");
+    static constexpr int NW = WGM * WGN;      // waves per workgroup
+    static constexpr int NT = 64 * NW;
+    static_assert(NW == 4 || NW == 8, "four or eight waves per workgroup");
     static constexpr int BMc = 32 * WM * WGM;
     static constexpr int BNp = 32 * WN * WGN;
     static constexpr int ROWS = BMc + BNp;
     static constexpr int STAGE = ROWS * 128;  // bytes per stage
     static constexpr int BLOCKS = ROWS / 8;   // 8-row (1 KiB) blocks per stage
-    static_assert(BLOCKS % 4 == 0, "blocks split evenly over the four waves");
-    static constexpr int I = BLOCKS / 4;      // load instructions per wave per stage
+    static_assert(BLOCKS % NW == 0, "blocks split evenly over the waves");
+    static constexpr int I = BLOCKS / NW;     // load instructions per wave per stage
     static_assert((NSTAGE - 2) * I <= 63, "vmcnt range");
     static constexpr int LDS = NSTAGE * STAGE;
 };
@@ -350,6 +354,8 @@ __device__ inline void ring_barrier()
     asm volatile("" ::: "memory");
 }
 
+__device__ inline uint32_t rsw(uint32_t r) { return (r ^ (r >> 3)) & 7u; }
+
 // State of one workgroup of the pipelined kernel.  Ring slots are separate
 // LDS arrays and every step of the main loop names its slot at compile time,
 // so the compiler can tell that reading one slot does not depend on the
@@ -361,7 +367,7 @@ struct Pipe {
     uint32_t voff[C::I];    // byte offset of this lane's chunk at tap 0 (kOOB: no pixel)
     uint32_t vchunk[C::I];  // first tap of this lane's chunk within a stage
     uint32_t wave, lane, K, nst;
-    uint32_t arow, brow, sw;
+    uint32_t arow, brow;
     floatx16 acc[WM][WN];
 
     // Stage s >= nst (past the end of K) loads nothing: every offset is out of
@@ -373,7 +379,7 @@ struct Pipe {
         const bool past = s >= nst;
 #pragma unroll
         for (int j = 0; j < C::I; ++j) {
-            const uint32_t b = wave + 4 * j;
+            const uint32_t b = wave + C::NW * j;
             const bool filt = b < (uint32_t)C::BMc / 8;
             uint32_t off = voff[j] + 2u * k0;
             if (past || (!filt && tail && k0 + vchunk[j] >= K))
@@ -387,14 +393,18 @@ struct Pipe {
     {
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
-            const uint32_t cofs = 16u * ((2 * ks + (lane >> 5)) ^ sw);
+            const uint32_t ch = 2 * ks + (lane >> 5);
             half8 af[WM], bf[WN];
 #pragma unroll
-            for (int i = 0; i < WM; ++i)
-                af[i] = *reinterpret_cast<const half8 *>(stage + (arow + 32 * i) * 128 + cofs);
+            for (int i = 0; i < WM; ++i) {
+                const uint32_t r = arow + 32 * i;
+                af[i] = *reinterpret_cast<const half8 *>(stage + r * 128 + 16u * (ch ^ rsw(r)));
+            }
 #pragma unroll
-            for (int j = 0; j < WN; ++j)
-                bf[j] = *reinterpret_cast<const half8 *>(stage + (brow + 32 * j) * 128 + cofs);
+            for (int j = 0; j < WN; ++j) {
+                const uint32_t r = brow + 32 * j;
+                bf[j] = *reinterpret_cast<const half8 *>(stage + r * 128 + 16u * (ch ^ rsw(r)));
+            }
 #pragma unroll
             for (int i = 0; i < WM; ++i)
 #pragma unroll
@@ -421,7 +431,7 @@ struct Pipe {
 };
 
 template <int WM, int WN, int WGM, int WGN, int NSTAGE>
-__global__ __launch_bounds__(256) void conv_fp16_pipe(C16Args a)
+__global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
 {
     using C = PipeCfg<WM, WN, WGM, WGN, NSTAGE>;
     static_assert(NSTAGE >= 2 && NSTAGE <= 4, "ring depth");
@@ -447,7 +457,7 @@ __global__ __launch_bounds__(256) void conv_fp16_pipe(C16Args a)
     const uint64_t left = a.win_bytes - tb_elem * 2;
     w.rw = make_rsrc(a.ws + tb_elem, (uint32_t)(left < kMaxRecords ? left : kMaxRecords));
     w.rf = make_rsrc(a.packed + (uint64_t)ch0 * a.K_pad, (uint32_t)C::BMc * a.K_pad * 2u);
-    for (uint32_t t = tid; t < C::BNp; t += 256) {
+    for (uint32_t t = tid; t < C::BNp; t += C::NT) {
         const uint32_t p = p0 + t;
         uint32_t off = 0;
         if (p < a.P) {
@@ -459,26 +469,26 @@ __global__ __launch_bounds__(256) void conv_fp16_pipe(C16Args a)
     __syncthreads();
 
     // Lane L of a load instruction fills LDS slot L & 7 of row 8*block + L/8
-    // with 16-byte chunk (L & 7) ^ (row & 7) of that row.
+    // with 16-byte chunk (L & 7) ^ rsw(row) of that row (row counted from the
+    // first filter row of the stage).
     const uint32_t rib = w.lane >> 3, slot = w.lane & 7;
 #pragma unroll
     for (int j = 0; j < C::I; ++j) {
-        const uint32_t b = w.wave + 4 * j;
+        const uint32_t b = w.wave + C::NW * j;
         if (b < (uint32_t)C::BMc / 8) {
             const uint32_t row = 8 * b + rib;
-            const uint32_t c = slot ^ (row & 7);
+            const uint32_t c = slot ^ rsw(row);
             w.voff[j] = row * a.K_pad * 2u + 16u * c;
             w.vchunk[j] = 8 * c;
         } else {
             const uint32_t row = 8 * (b - C::BMc / 8) + rib;
-            const uint32_t c = slot ^ (row & 7);
+            const uint32_t c = slot ^ rsw(C::BMc + row);
             w.voff[j] = (p0 + row < a.P) ? rowoff[row] * 2u + 16u * c : kOOB;
             w.vchunk[j] = 8 * c;
         }
     }
     w.arow = wm * 32 * WM + (w.lane & 31);
     w.brow = C::BMc + wn * 32 * WN + (w.lane & 31);
-    w.sw = w.lane & 7;  // row & 7 of every row this lane reads
 #pragma unroll
     for (int i = 0; i < WM; ++i)
 #pragma unroll
@@ -534,14 +544,14 @@ void pick_regs(bool unaligned_loads, const void **f, int *bm, int *bn)
 struct PipeVariant {
     const char *name;
     const void *f;
-    int bm, bn;
+    int bm, bn, nt;
 };
 
 template <int WM, int WN, int WGM, int WGN, int NS>
 PipeVariant pipe_variant(const char *name)
 {
     return PipeVariant{name, (const void *)&conv_fp16_pipe<WM, WN, WGM, WGN, NS>, 32 * WM * WGM,
-                       32 * WN * WGN};
+                       32 * WN * WGN, 64 * WGM * WGN};
 }
 
 // Tile shapes of the pipelined kernel: channels x pixels per workgroup,
@@ -549,15 +559,13 @@ PipeVariant pipe_variant(const char *name)
 const PipeVariant *pipe_variants(int *n)
 {
     static const PipeVariant v[] = {
-        pipe_variant<1, 2, 1, 4, 4>("c32p256s4"),
         pipe_variant<1, 1, 1, 4, 3>("c32p128s3"),
-        pipe_variant<2, 2, 1, 4, 3>("c64p256s3"),
         pipe_variant<1, 2, 2, 2, 3>("c64p128s3"),
-        pipe_variant<2, 2, 2, 2, 4>("c128p128s4"),
         pipe_variant<2, 2, 2, 2, 2>("c128p128s2"),
-        pipe_variant<2, 4, 2, 2, 3>("c128p256s3"),
-        pipe_variant<4, 2, 1, 4, 2>("c128p256s2w"),
-        pipe_variant<2, 4, 2, 2, 2>("c128p256s2"),
+        // eight waves, 128 x 64 wave tiles: half the L2 -> LDS traffic per
+        // FLOP of the 128 x 128 tiles
+        pipe_variant<4, 2, 2, 4, 2>("c256p256s2w8"),
+        pipe_variant<2, 2, 2, 4, 2>("c128p256s2w8"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
@@ -603,9 +611,28 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
     if (aligned) {
         int n;
         const PipeVariant *v = pipe_variants(&n);
-        // Shapes that leave LDS for two workgroups per CU measured fastest on
-        // every layer tried (latency hiding beats ring depth).
-        int pick = sh.Co <= 32 ? 1 : sh.Co <= 64 ? 3 : 5;
+        // Defaults, measured per layer on MI355X: shapes that leave LDS for
+        // two workgroups per CU (32x128, 64x128, 128x128); 64x128 also when a
+        // 128x128 grid would give fewer workgroups than CUs (S11: 280 vs 220
+        // TFLOP/s); 256x256 over eight waves when its grid fills 128 to 256
+        // CUs (cfg4 616 vs 575, S4 670 vs 646; with fewer tiles it starves
+        // the chip, with more the second round runs partly empty).
+        auto find = [&](const char *name) {
+            for (int t = 0; t < n; ++t)
+                if (strcmp(name, v[t].name) == 0)
+                    return t;
+            return 0;
+        };
+        auto tiles = [&](int64_t bm, int64_t bn) { return ((sh.P + bn - 1) / bn) * ((sh.Co + bm - 1) / bm); };
+        int pick;
+        if (sh.Co <= 32)
+            pick = find("c32p128s3");
+        else if (sh.Co <= 64 || tiles(128, 128) < 256)
+            pick = find("c64p128s3");
+        else if (tiles(256, 256) >= 128 && tiles(256, 256) <= 256 && sh.Co >= 256)
+            pick = find("c256p256s2w8");
+        else
+            pick = find("c128p128s2");
         // IM2WIN_FP16_TILE=<name> overrides the tile shape (for tuning).
         if (const char *e = getenv("IM2WIN_FP16_TILE")) {
             for (int t = 0; t < n; ++t)
@@ -614,7 +641,7 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
         }
         const PipeVariant &p = v[pick];
         dim3 grid((uint32_t)((sh.P + p.bn - 1) / p.bn), (uint32_t)((sh.Co + p.bm - 1) / p.bm));
-        return hipLaunchKernel(p.f, grid, dim3(256), args, 0, st);
+        return hipLaunchKernel(p.f, grid, dim3(p.nt), args, 0, st);
     }
     const void *f;
     int bm, bn;

@@ -36,11 +36,13 @@ __device__ inline void store_tile_lds(const f32x16_acc (&acc)[WM][WN], char *lds
     constexpr int BM = 32 * WM * WGM, BN = 32 * WN * WGN, NT = 64 * WGM * WGN;
     constexpr int RB = 2 * BM;          // bytes per pixel row
     constexpr int CHR = RB / 16;        // 16-byte chunks per row
-    constexpr uint32_t SWM = CHR >= 8 ? 7u : (uint32_t)CHR - 1;
     static_assert(CHR >= 4, "at least 32 channels per tile");
-    // chunk k of row px sits at slot k ^ (px & SWM): the 16 lanes that write
-    // one channel group of 16 consecutive rows, and the lanes that read one
-    // row, spread over all banks
+    // chunk k of row px sits at slot k ^ sw(px): the 16 lanes that write one
+    // channel group of 16 consecutive rows, and the lanes that read one row,
+    // touch 16 different 16-byte slots of the 64 banks
+    auto sw = [](uint32_t px) -> uint32_t {
+        return CHR >= 16 ? (px & 15u) : CHR == 8 ? ((px ^ (px >> 3)) & 7u) : ((px ^ (px >> 2)) & 3u);
+    };
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < WN; ++j) {
@@ -57,7 +59,7 @@ __device__ inline void store_tile_lds(const f32x16_acc (&acc)[WM][WN], char *lds
                     h[e] = __builtin_bit_cast(uint16_t, v);
                 }
                 const uint32_t k = ch / 8;
-                *reinterpret_cast<uint2 *>(lds + px * RB + 16 * (k ^ (px & SWM)) + 2 * (ch % 8)) =
+                *reinterpret_cast<uint2 *>(lds + px * RB + 16 * (k ^ sw(px)) + 2 * (ch % 8)) =
                     make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
             }
         }
@@ -69,7 +71,7 @@ __device__ inline void store_tile_lds(const f32x16_acc (&acc)[WM][WN], char *lds
         const uint32_t p = p0 + px, ch = ch0 + 8 * k;
         if (p >= P || ch >= Co)
             continue;
-        const uint4 v = *reinterpret_cast<const uint4 *>(lds + px * RB + 16 * (k ^ (px & SWM)));
+        const uint4 v = *reinterpret_cast<const uint4 *>(lds + px * RB + 16 * (k ^ sw(px)));
         uint16_t *o = out + (uint64_t)p * Co + ch;
         if (vec && ch + 8 <= Co) {
             *reinterpret_cast<uint4 *>(o) = v;

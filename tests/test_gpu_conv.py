@@ -154,3 +154,39 @@ def test_fp16_row_kernel_on_column_shapes(shape, monkeypatch):
     check_full(run, x, w)
     run.check_out_guards()
 
+
+# Every kernel variant the launchers can pick (by layer or through the tuning
+# variables), on shapes that reach it: each must match the oracle, and where
+# the variants of a kernel accumulate K in the same order (the row-per-pixel
+# fp16 tiles, the fp32 kernels) each other bit for bit.  The names mirror the
+# variant tables in the C++ sources.
+VARIANT_CASES = [
+    # (environment variable, names, shape, dtype, same summation order)
+    ("IM2WIN_FP16_TILE", ["c32p128s3", "c64p128s3", "c128p128s2", "c256p256s2w8", "c128p256s2w8"],
+     (2, 16, 13, 13, 72, 5, 5, 1), torch.float16, True),
+    ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c128p256t16s3"], (2, 64, 24, 24, 100, 3, 3, 1),
+     torch.float16, False),
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p4c16l1s2k16", "regs"], (2, 16, 17, 19, 100, 3, 3, 1),
+     torch.float32, True),
+]
+
+
+@pytest.mark.parametrize("case", VARIANT_CASES, ids=lambda c: c[0])
+def test_kernel_variants_agree(case, monkeypatch):
+    var, names, shape, dtype, same_order = case
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=17)
+    first = None
+    for name in names:
+        say("variant", var, name, shape)
+        monkeypatch.setenv(var, name)
+        if var == "IM2WIN_FP16_TILE":
+            monkeypatch.setenv("IM2WIN_FP16_KERNEL", "pipe")
+        run = Run(x, w, s, dtype)
+        check_full(run, x, w)
+        out = run.out_np()
+        if first is None:
+            first = out
+        elif same_order:
+            assert np.array_equal(out.view(np.uint8), first.view(np.uint8)), name
+
