@@ -25,11 +25,12 @@
  *                     the buffer
  *     [pad_end, ...)  the filter repacked in window order (tap k = (v*K_h+u)*C_i+r)
  *                     and zero-padded, written by the conv call:
- *                       fp16: C_o_pad*K_w*T_pad fp16 values, C_o_pad = round_up(C_o, 128),
- *                             T_pad = round_up(K_h*C_i, 64), holding either
- *                             [C_o_pad][K_pad] (K_pad = round_up(K, 64)) or one
- *                             [T_pad] slice per filter column, [C_o_pad][K_w][T_pad],
- *                             depending on the kernel the layer runs
+ *                       fp16: C_o_pad*K_w*T_pad fp16 values, C_o_pad = round_up(C_o, 256),
+ *                             T_pad = round_up(K_h*C_i, 64): tiles of TB taps, each
+ *                             holding C_o_pad rows per slice, either one slice of
+ *                             K_pad = round_up(K, 64) taps or one slice of T_pad taps
+ *                             per filter column; TB depends on the kernel the layer
+ *                             runs (an internal layout, rewritten by every conv call)
  *                       fp32: [K_pad32][C_o_pad32] fp32, K_pad32 = round_up(K, 16),
  *                             C_o_pad32 = round_up(C_o, 32)
  *
@@ -89,8 +90,8 @@ int conv_output_dims(int64_t H_i, int64_t W_i, int64_t K_h, int64_t K_w, int64_t
  *
  * Index ranges the kernels support (else IM2WIN_ERANGE): one strip
  * W_i*K_h*C_i < 2^20 elements, K = K_h*K_w*C_i < 2^24, C_o < 2^19,
- * N*H_o*W_o < 2^31 output pixels, N*H_o < 2^31 strips, and every byte count
- * below 2^62.
+ * N*H_o*W_o < 2^31 output pixels, N*H_o < 2^31 strips, for IM2WIN_F16 a packed
+ * filter (above) below 2^31 bytes, and every byte count below 2^62.
  */
 int64_t conv_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
                              int64_t K_h, int64_t K_w, int64_t stride, im2win_dtype_t dt);

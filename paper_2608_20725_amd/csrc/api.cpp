@@ -59,19 +59,21 @@ int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_
         !mul_ok(r.win_elems, r.elt, kMaxBytes, &r.win_bytes))
         return IM2WIN_ERANGE;
     r.pad_end = round_up(r.win_bytes, kPad) + kPad;
-    r.Co_pad = round_up(Co, 128);
+    r.Co_pad = round_up(Co, 256);
     r.K_pad = round_up(r.K, 64);
     r.K_pad32 = round_up(r.K, 16);
     r.Co_pad32 = round_up(Co, 32);
     r.Tp = round_up(Kh * Ci, 64);
+    // the fp16 kernels address the packed filter with 31-bit offsets
+    if (dt == IM2WIN_F16 && r.Co_pad * r.Kw * r.Tp * 2 >= (int64_t)kMaxRecords)
+        return IM2WIN_ERANGE;
     *sh = r;
     return IM2WIN_OK;
 }
 
 int64_t packed_filter_bytes(const Shape &sh, int dt)
 {
-    // fp16: room for either layout, [C_o_pad][K_pad] or [C_o_pad][K_w][Tp]
-    // (K_pad <= K_w*Tp)
+    // fp16: room for every packed layout (C_o_pad*K_pad <= C_o_pad*K_w*Tp)
     return dt == IM2WIN_F16 ? sh.Co_pad * sh.Kw * sh.Tp * 2 : sh.K_pad32 * sh.Co_pad32 * 4;
 }
 

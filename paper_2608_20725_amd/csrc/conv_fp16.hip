@@ -44,32 +44,44 @@ struct C16Args {
     const uint16_t *packed;  // F' [Co_pad][K_pad]
     uint16_t *out;
     uint64_t win_bytes;
-    uint32_t P, K, K_pad, Co, Wo, L, S;
+    uint32_t P, K, K_pad, Co, Co_pad, Wo, L, S;
+    uint32_t pk_bytes;       // bytes of the packed filter
     FastDiv div_Wo;
 };
 
 // ---------------------------------------------------------------------------
-// Filter repack (window order, zero-padded): out[j][c][t] = F'[j][c*tlen + t]
-// for t < tlen, 0 for tlen <= t < tpad, 0 for j >= C_o, with nv slices of tpad
-// per row.  F'[j][k] is tap k = (v*K_h + u)*C_i + r of filter column j.  The
-// row-per-pixel kernels use one slice (tlen = K, tpad = K_pad); the
-// column-staged kernel one slice per filter column v (tlen = K_h*C_i).
-// One thread per 16-byte granule.
+// Filter repack (window order, zero-padded).  Element (j, c, t) of the packed
+// filter is F'[j][c*tlen + t] (tap k = (v*K_h + u)*C_i + r of filter column
+// j) for t < tlen and j < C_o, else 0, stored at
+//     ((t / TB * nv + c) * C_o_pad + j) * TB + t % TB:
+// tiles of TB taps, and within a tile all C_o_pad rows of slice c one after
+// the other.  A stage of a kernel that consumes TB taps at a time then finds
+// its filter rows as one contiguous run, which buffer_load ... lds streams
+// about twice as fast as rows scattered K_pad apart.  Layouts in use:
+//   row-per-pixel pipelined kernel: nv = 1, tlen = K, tpad = K_pad, TB = 64;
+//   column-staged kernel: nv = K_w, tlen = K_h*C_i, tpad = T_pad, TB = its
+//     stage depth;
+//   register-staged kernel: nv = 1, tlen = K, TB = tpad = K_pad, i.e. plain
+//     [C_o_pad][K_pad].
+// One thread per 16-byte granule, in output order.
 struct PackArgs {
     const uint16_t *filt;
     uint16_t *packed;
     uint64_t grans;
-    uint32_t nv, tlen, tpad, Co, Ci, Kh, Kw;
+    uint32_t nv, tlen, tpad, tb, Co, Co_pad, Ci, Kh, Kw;
 };
 
 __global__ __launch_bounds__(256) void pack_filter_fp16(PackArgs a)
 {
-    const uint32_t gpr = a.nv * a.tpad / 8;  // granules per packed row
     for (uint64_t g = (uint64_t)blockIdx.x * 256 + threadIdx.x; g < a.grans;
          g += (uint64_t)gridDim.x * 256) {
-        const uint32_t j = (uint32_t)(g / gpr);
-        const uint32_t i0 = (uint32_t)(g % gpr) * 8;
-        const uint32_t c = i0 / a.tpad, t0 = i0 % a.tpad;
+        const uint64_t e0 = g * 8;
+        const uint32_t r0 = (uint32_t)(e0 % a.tb);
+        const uint64_t q = e0 / a.tb;
+        const uint32_t j = (uint32_t)(q % a.Co_pad);
+        const uint64_t q2 = q / a.Co_pad;
+        const uint32_t c = (uint32_t)(q2 % a.nv);
+        const uint32_t t0 = (uint32_t)(q2 / a.nv) * a.tb + r0;
         uint32_t w[4];
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
@@ -366,7 +378,7 @@ struct Pipe {
     __amdgpu_buffer_rsrc_t rf, rw;
     uint32_t voff[C::I];    // byte offset of this lane's chunk at tap 0 (kOOB: no pixel)
     uint32_t vchunk[C::I];  // first tap of this lane's chunk within a stage
-    uint32_t wave, lane, K, nst;
+    uint32_t wave, lane, K, nst, apitch;
     uint32_t arow, brow;
     floatx16 acc[WM][WN];
 
@@ -381,7 +393,9 @@ struct Pipe {
         for (int j = 0; j < C::I; ++j) {
             const uint32_t b = wave + C::NW * j;
             const bool filt = b < (uint32_t)C::BMc / 8;
-            uint32_t off = voff[j] + 2u * k0;
+            // filter rows: stage s is tile s of the packed filter (apitch
+            // bytes each); window rows: taps k0 .. k0+63 of the window
+            uint32_t off = voff[j] + (filt ? s * apitch : 2u * k0);
             if (past || (!filt && tail && k0 + vchunk[j] >= K))
                 off = kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(filt ? rf : rw, (lds_ptr)(stage + 1024 * b), 16, off,
@@ -456,7 +470,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
     const uint64_t tb_elem = (uint64_t)q0 * a.L;
     const uint64_t left = a.win_bytes - tb_elem * 2;
     w.rw = make_rsrc(a.ws + tb_elem, (uint32_t)(left < kMaxRecords ? left : kMaxRecords));
-    w.rf = make_rsrc(a.packed + (uint64_t)ch0 * a.K_pad, (uint32_t)C::BMc * a.K_pad * 2u);
+    // the packed filter in 64-tap tiles of C_o_pad rows: row ch0 of tile 0 on
+    w.rf = make_rsrc(a.packed + (uint64_t)ch0 * BK, a.pk_bytes - ch0 * (uint32_t)BK * 2u);
+    w.apitch = a.Co_pad * (uint32_t)BK * 2u;
     for (uint32_t t = tid; t < C::BNp; t += C::NT) {
         const uint32_t p = p0 + t;
         uint32_t off = 0;
@@ -478,7 +494,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
         if (b < (uint32_t)C::BMc / 8) {
             const uint32_t row = 8 * b + rib;
             const uint32_t c = slot ^ rsw(row);
-            w.voff[j] = row * a.K_pad * 2u + 16u * c;
+            w.voff[j] = row * (uint32_t)BK * 2u + 16u * c;
             w.vchunk[j] = 8 * c;
         } else {
             const uint32_t row = 8 * (b - C::BMc / 8) + rib;
@@ -578,13 +594,17 @@ hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed,
     PackArgs a;
     a.filt = filt;
     a.packed = static_cast<uint16_t *>(packed);
-    if (col_plan(sh) >= 0) {
+    const int plan = col_plan(sh);
+    if (plan >= 0) {
         a.nv = (uint32_t)sh.Kw; a.tlen = (uint32_t)(sh.Kh * sh.Ci); a.tpad = (uint32_t)sh.Tp;
+        a.tb = (uint32_t)col_stage_taps(plan);
     } else {
         a.nv = 1; a.tlen = (uint32_t)sh.K; a.tpad = (uint32_t)sh.K_pad;
+        a.tb = (sh.Ci % 8) == 0 ? (uint32_t)BK : a.tpad;  // pipelined or register-staged kernel
     }
     a.grans = (uint64_t)sh.Co_pad * a.nv * a.tpad / 8;
-    a.Co = (uint32_t)sh.Co; a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
+    a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad;
+    a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
     uint64_t blocks = (a.grans + 255) / 256;
     if (blocks > 65536)
         blocks = 65536;
@@ -604,6 +624,8 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
     a.out = out;
     a.win_bytes = (uint64_t)sh.win_bytes;
     a.P = (uint32_t)sh.P; a.K = (uint32_t)sh.K; a.K_pad = (uint32_t)sh.K_pad;
+    a.Co_pad = (uint32_t)sh.Co_pad;
+    a.pk_bytes = (uint32_t)(sh.Co_pad * sh.K_pad * 2);  // < 2^31 (checked with the shape)
     a.Co = (uint32_t)sh.Co; a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.S = (uint32_t)sh.S;
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     void *args[] = {&a};

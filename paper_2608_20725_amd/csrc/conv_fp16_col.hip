@@ -49,11 +49,11 @@ typedef __attribute__((address_space(3))) void *lds_ptr;
 
 struct ColArgs {
     const uint16_t *ws;      // window tensor (fp16 bits)
-    const uint16_t *packed;  // G [Co_pad][KW][Tp]
+    const uint16_t *packed;  // G in BT-tap tiles: [Tp/BT][KW][Co_pad][BT]
     uint16_t *out;
     uint64_t win_bytes;
     uint64_t pk_bytes;       // bytes of G
-    uint32_t P, Co, Wo, L, T, Tp, s, ms, nst;
+    uint32_t P, Co, Co_pad, Wo, L, T, Tp, s, ms, nst;
     FastDiv div_Wo;
 };
 
@@ -114,7 +114,7 @@ struct ColTile {
     uint32_t boff[C::IB];  // byte offset of this lane's chunk at t = 0 (kOOB: none)
     uint32_t bcm[C::IB];   // B rows: first t of the chunk (t-tail mask); A rows: 0
     uint32_t Rj[C::WN];    // B row of each of this lane's pixels
-    uint32_t wave, lane, wm, wn, T, nst;
+    uint32_t wave, lane, wm, wn, T, nst, apitch;
     floatx16 acc[C::WM][C::WN];
 
     // Stage st >= nst (past the end of the slices) loads nothing.
@@ -126,7 +126,7 @@ struct ColTile {
         for (int i = 0; i < C::IB; ++i) {
             const uint32_t b = wave + C::NW * i;
             const bool isA = b * C::RPI < (uint32_t)C::AROWS;
-            const uint32_t off = (!past && t0 + bcm[i] < T) ? boff[i] + 2u * t0 : kOOB;
+            const uint32_t off = (!past && t0 + bcm[i] < T) ? boff[i] + (isA ? st * apitch : 2u * t0) : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(isA ? rf : rw, (lds_ptr)(slot + 1024 * b), 16, off,
                                                      0, 0, 0);
         }
@@ -213,9 +213,11 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
     const uint64_t tb = (uint64_t)q0 * a.L;
     const uint64_t wleft = a.win_bytes - tb * 2;
     w.rw = make_rsrc(a.ws + tb, (uint32_t)(wleft < kMaxRecords ? wleft : kMaxRecords));
-    const uint64_t fb = (uint64_t)ch0 * C::KW * a.Tp;
-    const uint64_t fleft = a.pk_bytes > fb * 2 ? a.pk_bytes - fb * 2 : 0;
-    w.rf = make_rsrc(a.packed + fb, (uint32_t)(fleft < kMaxRecords ? fleft : kMaxRecords));
+    // the packed filter in BT-tap tiles: tile st holds, for each filter column
+    // v, the C_o_pad rows of slice v; addressed from row ch0 of (tile 0, v 0)
+    const uint64_t fb = (uint64_t)ch0 * C::BT;
+    w.rf = make_rsrc(a.packed + fb, (uint32_t)(a.pk_bytes - fb * 2));
+    w.apitch = (uint32_t)C::KW * a.Co_pad * C::BT * 2u;
 
     // Column table: element offset (from strip q0) of the column each B row
     // holds.  Pixel slot n owns rows R(n) .. R(n)+ms-1; the last pixel of a
@@ -249,7 +251,7 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
         w.bcm[i] = 0;
         if (row < (uint32_t)C::AROWS) {
             const uint32_t v = row / C::BM, jl = row % C::BM;
-            w.boff[i] = ((jl * C::KW + v) * a.Tp + 8 * c) * 2u;
+            w.boff[i] = ((v * a.Co_pad + jl) * C::BT + 8 * c) * 2u;
         } else if (row < (uint32_t)C::ROWS) {
             const uint32_t e = tbl[row - C::AROWS];
             if (e != kNoCol)
@@ -343,14 +345,14 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
 struct ColVariant {
     const char *name;
     const void *f;
-    int kw, bm, bn, nrmax;
+    int kw, bm, bn, nrmax, bt;
 };
 
 template <int KW, int BT, int WM, int WN, int WGM, int WGN, int NRMAX, int NS>
 ColVariant col_variant(const char *name)
 {
     using C = ColCfg<KW, BT, WM, WN, WGM, WGN, NRMAX, NS>;
-    return ColVariant{name, (const void *)&conv_fp16_col<C>, KW, C::BM, C::BN, NRMAX};
+    return ColVariant{name, (const void *)&conv_fp16_col<C>, KW, C::BM, C::BN, NRMAX, BT};
 }
 
 const ColVariant *col_variants(int *n)
@@ -415,8 +417,8 @@ int col_plan(const Shape &sh)
         return -1;
     if (col_rows_needed(sh, v[pick].bn) > v[pick].nrmax)
         return -1;
-    // the filter rows of one tile are addressed with 31-bit offsets
-    if ((int64_t)v[pick].bm * sh.Kw * sh.Tp * 2 >= (int64_t)kMaxRecords)
+    // the packed filter is addressed with 31-bit offsets
+    if (sh.Co_pad * sh.Kw * sh.Tp * 2 >= (int64_t)kMaxRecords)
         return -1;
     // every offset inside a tile must fit 31 bits (checked per layer: the
     // strips of one tile plus the last column's slice)
@@ -424,6 +426,12 @@ int col_plan(const Shape &sh)
     if ((strips_per_tile * sh.L + sh.Tp) * 2 >= (int64_t)kOOB)
         return -1;
     return pick;
+}
+
+int col_stage_taps(int plan)
+{
+    int n;
+    return col_variants(&n)[plan].bt;
 }
 
 hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const void *packed,
@@ -437,6 +445,7 @@ hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const
     a.out = out;
     a.win_bytes = (uint64_t)sh.win_bytes;
     a.pk_bytes = (uint64_t)sh.Co_pad * sh.Kw * sh.Tp * 2;
+    a.Co_pad = (uint32_t)sh.Co_pad;
     a.P = (uint32_t)sh.P; a.Co = (uint32_t)sh.Co; a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L;
     a.T = (uint32_t)(sh.Kh * sh.Ci); a.Tp = (uint32_t)sh.Tp; a.s = (uint32_t)sh.s;
     a.ms = (uint32_t)(sh.s < sh.Kw ? sh.s : sh.Kw);

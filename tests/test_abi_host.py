@@ -57,9 +57,9 @@ def _closed_form(l, elt, fp16):
     win = l.N * Ho * l.W * l.K_h * l.C_i * elt
     pad_end = (win + 255) // 256 * 256 + 256
     K = l.K_h * l.K_w * l.C_i
-    if fp16:   # packed filter round_up(C_o,128) x K_w x round_up(K_h*C_i,64) fp16
-        packed = ((l.C_o + 127) // 128 * 128) * l.K_w * ((l.K_h * l.C_i + 63) // 64 * 64) * 2
-        assert packed >= ((l.C_o + 127) // 128 * 128) * ((K + 63) // 64 * 64) * 2
+    if fp16:   # packed filter round_up(C_o,256) x K_w x round_up(K_h*C_i,64) fp16
+        packed = ((l.C_o + 255) // 256 * 256) * l.K_w * ((l.K_h * l.C_i + 63) // 64 * 64) * 2
+        assert packed >= ((l.C_o + 255) // 256 * 256) * ((K + 63) // 64 * 64) * 2
     else:      # packed filter [round_up(K,16)][round_up(C_o,32)] fp32
         packed = ((K + 15) // 16 * 16) * ((l.C_o + 31) // 32 * 32) * 4
     im2col = l.N * Ho * Wo * K * elt
@@ -115,6 +115,9 @@ def test_ranges(lib):
     assert lib.conv_workspace_bytes(1, 3, 8, 8, 1 << 19, 3, 3, 1, pkg.F32) == ERANGE
     # more than 2^31 output pixels
     assert lib.conv_workspace_bytes(1 << 20, 1, 64, 64, 1, 1, 1, 1, pkg.F32) == ERANGE
+    # fp16 packed filter of 2^31 bytes or more (fp32 has no such limit)
+    assert lib.conv_workspace_bytes(1, 1 << 12, 1, 64, 1 << 16, 1, 64, 1, pkg.F16) == ERANGE
+    assert lib.conv_workspace_bytes(1, 1 << 12, 1, 64, 1 << 16, 1, 64, 1, pkg.F32) > 0
 
 
 def test_output_dims_rejects(lib):
