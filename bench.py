@@ -109,6 +109,31 @@ class Path:
         self.conv(self.ws, self.w, self.out, l.N, l.C_i, l.H, l.W, l.stride)
 
 
+def measure_minibatch(l, paths, pkg, torch, n_chunk=32, reps=10):
+    """The mini-batch entry point on the same layer and buffers: chunks of
+    `n_chunk` images alternating between two streams.
+    Outside the timed step; reports its time per batch (HIP events on the main
+    stream, which waits for every transform) and its workspace."""
+    res = {"n_chunk": n_chunk, "two_streams": True}
+    aux = torch.cuda.Stream()
+    for name, p in paths.items():
+        need = pkg.conv_chunked_workspace_bytes(l.N, l.C_i, l.H, l.W, l.C_o, l.K_h, l.K_w, l.stride,
+                                                n_chunk, True, p.x.dtype)
+        ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        for _ in range(2):
+            pkg.conv_im2win_chunked(p.x, p.w, p.out, ws, l.stride, n_chunk, aux_stream=aux)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            pkg.conv_im2win_chunked(p.x, p.w, p.out, ws, l.stride, n_chunk, aux_stream=aux)
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = {"ms": round(e0.elapsed_time(e1) / reps, 5), "workspace_bytes": need,
+                     "full_batch_workspace_bytes": p.ws.numel()}
+        del ws
+    return res
+
+
 def cpu_baseline(l, x, w, budget_s=10.0):
     """The fp64 oracle on the host cores over whole images of the same layer,
     a few images at a time, cycling through the batch until `budget_s` has
@@ -276,6 +301,13 @@ def main():
                 "allocator_peak_bytes": peak_alloc,
             },
         }
+        if not args.sweep:
+            mb = measure_minibatch(l, paths, pkg, torch)
+            for name in ("f32", "f16"):
+                full_ms = k[name + "_transform_ms"][0] + k[name + "_conv_ms"][0]
+                mb[name]["TFLOP/s"] = round(flops / (mb[name]["ms"] * 1e-3) / 1e12, 3)
+                mb[name]["full_batch_ms"] = round(full_ms, 5)
+            rec["minibatch"] = mb
         if not args.no_cpu_baseline and not args.sweep:
             rec["cpu_baseline"] = cpu_baseline(l, x, w)
         print(json.dumps(rec), flush=True)

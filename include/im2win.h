@@ -155,6 +155,50 @@ int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream);
 
 /* A static, human-readable name for a status code. */
+/*
+ * Mini-batch im2win: bytes of workspace conv_im2win_chunked needs for chunks
+ * of n_chunk images (n_chunk is clamped to N), with one window-tensor slot, or
+ * two when two_streams is non-zero:
+ *   nslots * round_up(pad_end(n_chunk), 256) + packed filter bytes,
+ * where pad_end(n) is the pad end of an n-image window tensor (layout above).
+ * Host only.  Returns a negative status for invalid arguments.
+ */
+int64_t conv_chunked_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
+                                     int64_t K_h, int64_t K_w, int64_t stride, int64_t n_chunk,
+                                     int two_streams, im2win_dtype_t dt);
+
+/*
+ * Transform + windowed convolution of the whole batch in chunks of n_chunk
+ * images (the mini-batch strategy of Sec. IV-C, against the full-batch
+ * conv_im2win_transform + conv_im2win_fp32/fp16 pair): the workspace holds the
+ * window tensor of one chunk, or of two when a second stream is given.
+ *   in_nhwc         device, input I (fp32 or fp16 bits per `dt`), read only
+ *   filt_khkwcico   device, filter F, read only
+ *   out_nhwc        device, output O, written once per element
+ *   ws              device, ws_bytes >= conv_chunked_workspace_bytes(...,
+ *                   hip_stream_aux != NULL, dt); slot layout as above, the
+ *                   packed filter after the slots
+ *   hip_stream      the filter pack and the chunks (transform, then conv) are
+ *                   enqueued here
+ *   hip_stream_aux  NULL, or a second stream: chunks then alternate between
+ *                   the two streams (chunk c on hip_stream_aux when c is odd),
+ *                   each stream using its own workspace slot, so two chunks
+ *                   are in flight and one's transform overlaps the other's
+ *                   conv.  The aux stream first waits for the work already on
+ *                   hip_stream and hip_stream finally waits for the aux
+ *                   stream, so all of the call is ordered before later work on
+ *                   hip_stream.  The ordering uses two HIP events that the
+ *                   library creates on first use per host thread and device
+ *                   and keeps (no device memory is allocated).
+ * The output is bit-identical to conv_im2win_fp32/fp16 on the full batch.
+ * Errors as for the other calls; input, filter, output and workspace must not
+ * overlap, and the two streams must differ.
+ */
+int conv_im2win_chunked(const void *in_nhwc, const void *filt_khkwcico, void *out_nhwc, void *ws,
+                        int64_t ws_bytes, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
+                        int64_t K_h, int64_t K_w, int64_t stride, int64_t n_chunk, im2win_dtype_t dt,
+                        void *hip_stream, void *hip_stream_aux);
+
 const char *conv_im2win_strerror(int status);
 
 #ifdef __cplusplus

@@ -68,6 +68,10 @@ def load_library():
     lib.conv_im2win_fp32.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
     lib.conv_im2win_fp16.restype = ctypes.c_int
     lib.conv_im2win_fp16.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
+    lib.conv_chunked_workspace_bytes.restype = _i64
+    lib.conv_chunked_workspace_bytes.argtypes = [_i64] * 9 + [ctypes.c_int, ctypes.c_int]
+    lib.conv_im2win_chunked.restype = ctypes.c_int
+    lib.conv_im2win_chunked.argtypes = [_vp, _vp, _vp, _vp, _i64] + [_i64] * 9 + [ctypes.c_int, _vp, _vp]
     lib.conv_im2win_strerror.restype = ctypes.c_char_p
     lib.conv_im2win_strerror.argtypes = [ctypes.c_int]
     _lib = lib
@@ -190,3 +194,33 @@ def im2win_conv2d(x, w, stride: int, ws=None, out=None, stream=None):
     else:
         conv_im2win_fp16(ws, w, out, N, C_i, H_i, W_i, stride, stream)
     return out, ws
+
+
+def conv_chunked_workspace_bytes(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, n_chunk, two_streams,
+                                 dtype) -> int:
+    n = load_library().conv_chunked_workspace_bytes(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, n_chunk,
+                                                    1 if two_streams else 0, _dtype_code(dtype))
+    if n < 0:
+        raise Im2winError(int(n), "conv_chunked_workspace_bytes")
+    return int(n)
+
+
+def conv_im2win_chunked(x, w, out, ws, stride: int, n_chunk: int, stream=None, aux_stream=None):
+    """Transform + conv of NHWC ``x`` in chunks of ``n_chunk`` images into
+    ``out``; with ``aux_stream`` the transform of the next chunk overlaps the
+    conv of the current one."""
+    import torch
+    if x.dim() != 4 or not x.is_contiguous() or w.dim() != 4 or not w.is_contiguous():
+        raise ValueError("x must be contiguous NHWC, w contiguous [K_h][K_w][C_i][C_o]")
+    if not out.is_contiguous() or x.dtype != w.dtype or x.dtype != out.dtype:
+        raise ValueError("out must be contiguous, with the dtype of x and w")
+    N, H_i, W_i, C_i = x.shape
+    K_h, K_w, C_i2, C_o = w.shape
+    if C_i2 != C_i:
+        raise ValueError("filter has %d input channels, layer has %d" % (C_i2, C_i))
+    aux = ctypes.c_void_p(None) if aux_stream is None else _stream(aux_stream)
+    rc = load_library().conv_im2win_chunked(
+        _ptr(x), _ptr(w), _ptr(out), _ptr(ws), _nbytes(ws), N, C_i, H_i, W_i, C_o, K_h, K_w,
+        stride, n_chunk, _dtype_code(x.dtype), _stream(stream), aux)
+    _check(rc, "conv_im2win_chunked")
+

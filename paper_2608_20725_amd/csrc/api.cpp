@@ -1,6 +1,7 @@
 // Host side of the C interface: argument checks, workspace accounting,
 // device check and kernel dispatch.  The operations themselves run in the
-// gfx950 kernels of transform.hip, conv_fp32.hip and conv_fp16.hip.
+// gfx950 kernels of transform.hip, conv_fp32*.hip and conv_fp16*.hip; the
+// mini-batch entry points are in chunked.cpp.
 #include "../../include/im2win.h"
 #include "common.hpp"
 
@@ -26,6 +27,11 @@ bool mul_ok(int64_t a, int64_t b, int64_t lim, int64_t *out)
     *out = a * b;
     return true;
 }
+
+}  // namespace
+
+// Shared with the chunked entry points (chunked.cpp).
+namespace im2win {
 
 // Fills `sh` from the user's arguments; returns a status.
 int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_t Kh,
@@ -135,7 +141,7 @@ int launch_status(hipError_t e)
     return IM2WIN_OK;
 }
 
-}  // namespace
+}  // namespace im2win
 
 extern "C" {
 

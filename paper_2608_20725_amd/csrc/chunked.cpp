@@ -1,0 +1,193 @@
+// Mini-batch (N-chunked) im2win: the transform and the windowed convolution
+// run on chunks of n_chunk images, so the workspace holds the window tensor of
+// one chunk (or two, double-buffered) instead of the whole batch.  The paper
+// processes the full batch at once and notes the memory this costs next to
+// mini-batch methods (Sec. IV-C); this entry point bounds it.  With a second
+// stream, alternate chunks run on the two streams, so two chunks are in flight
+// and the transform of one overlaps the convolution of the other.
+//
+// Every chunk is convolved by the same kernels, in the same summation order, as
+// the full batch would be, so the output is bit-identical to the full-batch
+// entry points.
+#include "common.hpp"
+
+#include "../../include/im2win.h"
+
+#include <string.h>
+
+namespace im2win {
+namespace {
+
+constexpr int64_t kSlotAlign = 256;
+
+struct Plan {
+    Shape chunk;        // shape of a full chunk (n_chunk images)
+    int64_t n_chunk;
+    int64_t nslots;
+    int64_t slot_bytes;
+    int64_t packed_off;
+    int64_t ws_bytes;
+};
+
+int make_plan(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+              int64_t stride, int64_t n_chunk, int two_streams, int dt, Plan *p)
+{
+    if (n_chunk <= 0 || N <= 0)
+        return IM2WIN_EINVAL;
+    Shape full;
+    int rc = make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dt, &full);
+    if (rc != IM2WIN_OK)
+        return rc;
+    p->n_chunk = n_chunk < N ? n_chunk : N;
+    if ((rc = make_shape(p->n_chunk, C_i, H_i, W_i, C_o, K_h, K_w, stride, dt, &p->chunk)) != IM2WIN_OK)
+        return rc;
+    if (!transform_range_ok(p->chunk))
+        return IM2WIN_ERANGE;
+    p->nslots = two_streams ? 2 : 1;
+    p->slot_bytes = round_up(p->chunk.pad_end, kSlotAlign);
+    p->packed_off = p->nslots * p->slot_bytes;
+    p->ws_bytes = p->packed_off + packed_filter_bytes(p->chunk, dt);
+    return IM2WIN_OK;
+}
+
+// Events for ordering the two streams, kept per host thread and device
+// (created on first use, reused by every later call from that thread).
+struct Events {
+    hipEvent_t start = nullptr, done = nullptr;
+    bool ready = false;
+};
+
+int events_for_device(Events **out)
+{
+    constexpr int kMaxDev = 64;
+    static thread_local Events ev[kMaxDev];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev)
+        return IM2WIN_ENODEV;
+    Events &e = ev[dev];
+    if (!e.ready) {
+        if (hipEventCreateWithFlags(&e.start, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&e.done, hipEventDisableTiming) != hipSuccess)
+            return IM2WIN_ELAUNCH;
+        e.ready = true;
+    }
+    *out = &e;
+    return IM2WIN_OK;
+}
+
+int run_chunked(const void *in, const void *filt, void *out, void *ws, int64_t ws_bytes, int64_t N,
+                int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+                int64_t stride, int64_t n_chunk, int dt, hipStream_t st, hipStream_t aux)
+{
+    if (!in || !filt || !out || !ws)
+        return IM2WIN_EINVAL;
+    Plan p;
+    int rc = make_plan(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, n_chunk, aux != nullptr, dt, &p);
+    if (rc != IM2WIN_OK)
+        return rc;
+    if (aux != nullptr && aux == st)
+        return IM2WIN_EINVAL;
+    if (!aligned16(in) || !aligned16(filt) || !aligned16(out) || !aligned16(ws))
+        return IM2WIN_EALIGN;
+    Shape full;
+    make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dt, &full);
+    const int64_t elt = full.elt;
+    const int64_t in_bytes = N * H_i * W_i * C_i * elt, f_bytes = full.K * C_o * elt,
+                  o_bytes = full.P * C_o * elt;
+    if (ws_bytes < 0)
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_extent(in, in_bytes)) != IM2WIN_OK || (rc = check_extent(filt, f_bytes)) != IM2WIN_OK ||
+        (rc = check_extent(out, o_bytes)) != IM2WIN_OK || (rc = check_extent(ws, ws_bytes)) != IM2WIN_OK)
+        return rc;
+    if (overlaps(in, in_bytes, ws, ws_bytes) || overlaps(in, in_bytes, out, o_bytes) ||
+        overlaps(filt, f_bytes, ws, ws_bytes) || overlaps(filt, f_bytes, out, o_bytes) ||
+        overlaps(out, o_bytes, ws, ws_bytes))
+        return IM2WIN_EOVERLAP;
+    if (ws_bytes < p.ws_bytes)
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_device()) != IM2WIN_OK)
+        return rc;
+    Events *ev = nullptr;
+    if (aux != nullptr && (rc = events_for_device(&ev)) != IM2WIN_OK)
+        return rc;
+
+    char *wsb = static_cast<char *>(ws);
+    void *packed = wsb + p.packed_off;
+    // the filter is packed once; its layout does not depend on the batch size
+    if (dt == IM2WIN_F32)
+        rc = launch_status(launch_pack_fp32(p.chunk, static_cast<const float *>(filt), packed, st));
+    else
+        rc = launch_status(launch_pack_fp16(p.chunk, static_cast<const uint16_t *>(filt), packed, st));
+    if (rc != IM2WIN_OK)
+        return rc;
+    // With two streams, chunk c runs (transform, then conv) on stream c % 2
+    // in slot c % 2: two chunks are in flight at once, the transform of one
+    // overlapping the conv of the other, and a slot is reused only by later
+    // work on the same stream.  The aux stream starts after everything already
+    // queued on `st` (the input, the packed filter, earlier users of this
+    // workspace) and `st` finally waits for the aux stream.
+    if (aux != nullptr) {
+        if (hipEventRecord(ev->start, st) != hipSuccess || hipStreamWaitEvent(aux, ev->start, 0) != hipSuccess)
+            return IM2WIN_ELAUNCH;
+    }
+    const int64_t in_img = H_i * W_i * C_i * elt, out_img = full.Ho * full.Wo * C_o * elt;
+    const int64_t nchunks = (N + p.n_chunk - 1) / p.n_chunk;
+    for (int64_t c = 0; c < nchunks; ++c) {
+        const int64_t i0 = c * p.n_chunk;
+        const int64_t n = N - i0 < p.n_chunk ? N - i0 : p.n_chunk;
+        Shape sh = p.chunk;
+        if (n != p.n_chunk)
+            make_shape(n, C_i, H_i, W_i, C_o, K_h, K_w, stride, dt, &sh);
+        const int slot = (int)(c % p.nslots);
+        char *wsl = wsb + slot * p.slot_bytes;
+        const char *inc = static_cast<const char *>(in) + i0 * in_img;
+        char *outc = static_cast<char *>(out) + i0 * out_img;
+        hipStream_t cs = (aux != nullptr && slot == 1) ? aux : st;
+        if ((rc = launch_status(launch_transform(sh, inc, wsl, cs))) != IM2WIN_OK)
+            return rc;
+        if (dt == IM2WIN_F32)
+            rc = launch_status(launch_conv_fp32(sh, wsl, packed, reinterpret_cast<float *>(outc), cs));
+        else
+            rc = launch_status(launch_conv_fp16(sh, wsl, packed, reinterpret_cast<uint16_t *>(outc), cs));
+        if (rc != IM2WIN_OK)
+            return rc;
+    }
+    if (aux != nullptr) {
+        if (hipEventRecord(ev->done, aux) != hipSuccess || hipStreamWaitEvent(st, ev->done, 0) != hipSuccess)
+            return IM2WIN_ELAUNCH;
+    }
+    return IM2WIN_OK;
+}
+
+}  // namespace
+}  // namespace im2win
+
+using namespace im2win;
+
+extern "C" {
+
+int64_t conv_chunked_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
+                                     int64_t K_h, int64_t K_w, int64_t stride, int64_t n_chunk,
+                                     int two_streams, im2win_dtype_t dt)
+{
+    if (dt != IM2WIN_F32 && dt != IM2WIN_F16)
+        return IM2WIN_EINVAL;
+    Plan p;
+    int rc = make_plan(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, n_chunk, two_streams, (int)dt, &p);
+    if (rc != IM2WIN_OK)
+        return rc;
+    return p.ws_bytes;
+}
+
+int conv_im2win_chunked(const void *in_nhwc, const void *filt_khkwcico, void *out_nhwc, void *ws,
+                        int64_t ws_bytes, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
+                        int64_t K_h, int64_t K_w, int64_t stride, int64_t n_chunk, im2win_dtype_t dt,
+                        void *hip_stream, void *hip_stream_aux)
+{
+    if (dt != IM2WIN_F32 && dt != IM2WIN_F16)
+        return IM2WIN_EINVAL;
+    return run_chunked(in_nhwc, filt_khkwcico, out_nhwc, ws, ws_bytes, N, C_i, H_i, W_i, C_o, K_h, K_w, stride,
+                       n_chunk, (int)dt, (hipStream_t)hip_stream, (hipStream_t)hip_stream_aux);
+}
+
+}  // extern "C"

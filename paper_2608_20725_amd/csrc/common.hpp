@@ -94,6 +94,19 @@ __device__ inline uint32_t ld_b16(__amdgpu_buffer_rsrc_t r, uint32_t off)
 
 } // namespace im2win
 
+// Host helpers of the C interface (api.cpp), shared with the chunked entry
+// points (chunked.cpp).
+namespace im2win {
+int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_t Kh, int64_t Kw,
+               int64_t s, int dt, Shape *sh);
+int64_t packed_filter_bytes(const Shape &sh, int dt);
+bool aligned16(const void *p);
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb);
+int check_extent(const void *p, int64_t bytes);
+int check_device();
+int launch_status(hipError_t e);
+}  // namespace im2win
+
 // Kernel launchers (one per translation unit).  Each returns a hipError_t from
 // the launch itself; the shape has been validated.
 namespace im2win {

@@ -164,3 +164,36 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(pkg, "_LIB_PATH", str(tmp_path / "nope.so"))
     with pytest.raises(RuntimeError, match="not built"):
         pkg.load_library()
+
+
+@pytest.mark.parametrize("layer", [workloads.CFG2, workloads.CFG3, workloads.CFG4], ids=lambda l: l.name)
+def test_chunked_workspace_bytes(lib, layer):
+    l = layer
+    for dt, elt in ((pkg.F32, 4), (pkg.F16, 2)):
+        full, _, _ = _closed_form(l, elt, dt == pkg.F16)
+        for n_chunk in (1, 7, l.N, l.N + 5):
+            for two in (0, 1):
+                nc = min(n_chunk, l.N)
+                Ho = (l.H - l.K_h) // l.stride + 1
+                win = nc * Ho * l.W * l.K_h * l.C_i * elt
+                pad_end = (win + 255) // 256 * 256 + 256
+                slot = (pad_end + 255) // 256 * 256
+                packed = full - ((l.N * Ho * l.W * l.K_h * l.C_i * elt + 255) // 256 * 256 + 256)
+                want = (2 if two else 1) * slot + packed
+                got = pkg.conv_chunked_workspace_bytes(l.N, l.C_i, l.H, l.W, l.C_o, l.K_h, l.K_w,
+                                                       l.stride, n_chunk, two, dt)
+                assert got == want
+        # the window-tensor slots of one-image chunks are 2/N of the full batch's
+        one = pkg.conv_chunked_workspace_bytes(l.N, l.C_i, l.H, l.W, l.C_o, l.K_h, l.K_w, l.stride,
+                                               1, 1, dt)
+        assert one - packed < (full - packed) // 16
+
+
+def test_chunked_rejects(lib):
+    assert lib.conv_chunked_workspace_bytes(4, 8, 10, 10, 16, 3, 3, 1, 0, 0, pkg.F32) == EINVAL
+    assert lib.conv_chunked_workspace_bytes(4, 8, 10, 10, 16, 3, 3, 1, -3, 1, pkg.F32) == EINVAL
+    assert lib.conv_chunked_workspace_bytes(4, 8, 10, 10, 16, 3, 3, 1, 2, 0, 9) == EINVAL
+    v = ctypes.c_void_p
+    # null pointers first
+    assert lib.conv_im2win_chunked(None, v(256), v(512), v(1024), 1 << 20, 4, 8, 10, 10, 16, 3, 3, 1, 2,
+                                   pkg.F32, None, None) == EINVAL

@@ -63,7 +63,10 @@ def test_host_pointer_refused():
 
 
 def test_buffer_smaller_than_layer():
-    # an output allocation too small for the layer is refused, not overrun
+    # an output allocation too small for the layer is refused, not overrun:
+    # EBUFFER when the block ends before the output would, or EOVERLAP when
+    # torch's caching allocator carved the block out of the segment that also
+    # holds the workspace (the output range then runs into the workspace)
     x, w, ws, out, need = _bufs()
     lib = pkg.load_library()
     small = torch.cuda.caching_allocator_alloc(256)
@@ -71,6 +74,6 @@ def test_buffer_smaller_than_layer():
         rc = lib.conv_im2win_fp32(ctypes.c_void_p(ws.data_ptr()), need,
                                   ctypes.c_void_p(w.data_ptr()), ctypes.c_void_p(small),
                                   64, Ci, H, W, Co, Kh, Kw, s, None)
-        assert rc in (EBUFFER, EWORKSPACE)
+        assert rc in (EBUFFER, EWORKSPACE, EOVERLAP)
     finally:
         torch.cuda.caching_allocator_delete(small)
