@@ -345,14 +345,14 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
 struct ColVariant {
     const char *name;
     const void *f;
-    int kw, bm, bn, nrmax, bt;
+    int kw, bm, bn, nrmax, bt, nt;
 };
 
 template <int KW, int BT, int WM, int WN, int WGM, int WGN, int NRMAX, int NS>
 ColVariant col_variant(const char *name)
 {
     using C = ColCfg<KW, BT, WM, WN, WGM, WGN, NRMAX, NS>;
-    return ColVariant{name, (const void *)&conv_fp16_col<C>, KW, C::BM, C::BN, NRMAX, BT};
+    return ColVariant{name, (const void *)&conv_fp16_col<C>, KW, C::BM, C::BN, NRMAX, BT, C::NT};
 }
 
 const ColVariant *col_variants(int *n)
@@ -362,6 +362,8 @@ const ColVariant *col_variants(int *n)
         col_variant<3, 32, 2, 2, 1, 4, 288, 2>("k3c64p256t32s2"),
         col_variant<3, 16, 2, 4, 2, 2, 288, 3>("k3c128p256t16s3"),
         col_variant<7, 16, 2, 2, 1, 4, 544, 3>("k7c64p256t16s3"),
+        // eight waves, 256 x 256 tiles (large C_o)
+        col_variant<3, 32, 4, 2, 2, 4, 320, 2>("k3c256p256t32s2w8"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
@@ -402,11 +404,18 @@ int col_plan(const Shape &sh)
         // more channels the K_w*BM filter rows of a stage dominate it and the
         // row-per-pixel kernel, whose stages hold 64 taps of BM filter rows,
         // is faster.
+        // With C_o > 128 and a 256 x 256 grid of 128 to 256 tiles, the
+        // eight-wave 256 x 256 variant (whose filter rows now arrive as one
+        // contiguous run per stage) beats the row kernel (cfg4: 722 vs 663
+        // TFLOP/s); with fewer tiles it leaves too many CUs idle.
+        const int64_t tiles256 = ((sh.P + 255) / 256) * ((sh.Co + 255) / 256);
         const char *name = nullptr;
         if (sh.Kw == 3 && sh.Co <= 128)
             name = "k3c64p256t32s2";
         else if (sh.Kw == 7 && sh.Co <= 128)
             name = "k7c64p256t16s3";
+        else if (sh.Kw == 3 && tiles256 >= 128 && tiles256 <= 256)
+            name = "k3c256p256t32s2w8";
         else
             return -1;
         for (int t = 0; t < n; ++t)
@@ -453,7 +462,7 @@ hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     void *args[] = {&a};
     dim3 grid((uint32_t)((sh.P + v.bn - 1) / v.bn), (uint32_t)((sh.Co + v.bm - 1) / v.bm));
-    return hipLaunchKernel(v.f, grid, dim3(256), args, 0, st);
+    return hipLaunchKernel(v.f, grid, dim3(v.nt), args, 0, st);
 }
 
 }  // namespace im2win
