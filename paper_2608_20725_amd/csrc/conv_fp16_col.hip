@@ -364,6 +364,7 @@ const ColVariant *col_variants(int *n)
         col_variant<7, 16, 2, 2, 1, 4, 544, 3>("k7c64p256t16s3"),
         // eight waves, 256 x 256 tiles (large C_o)
         col_variant<3, 32, 4, 2, 2, 4, 320, 2>("k3c256p256t32s2w8"),
+        col_variant<3, 32, 2, 3, 4, 2, 256, 2>("k3c256p192t32s2w8"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
@@ -404,17 +405,20 @@ int col_plan(const Shape &sh)
         // more channels the K_w*BM filter rows of a stage dominate it and the
         // row-per-pixel kernel, whose stages hold 64 taps of BM filter rows,
         // is faster.
-        // With C_o > 128 and a 256 x 256 grid of 128 to 256 tiles, the
-        // eight-wave 256 x 256 variant (whose filter rows now arrive as one
-        // contiguous run per stage) beats the row kernel (cfg4: 722 vs 663
-        // TFLOP/s); with fewer tiles it leaves too many CUs idle.
-        const int64_t tiles256 = ((sh.P + 255) / 256) * ((sh.Co + 255) / 256);
+        // With C_o > 128 the eight-wave 256-channel variants (whose filter
+        // rows arrive as one contiguous run per stage) beat the row kernel
+        // when their grid fills most of the 256 CUs in one round: cfg4 (192
+        // tiles of 256 x 192) 808 vs 633 TFLOP/s; with ~100-130 tiles they
+        // lose (S5: 536 vs 636), so those layers keep the row kernel.
+        auto tiles = [&](int64_t bn) { return ((sh.P + bn - 1) / bn) * ((sh.Co + 255) / 256); };
         const char *name = nullptr;
         if (sh.Kw == 3 && sh.Co <= 128)
             name = "k3c64p256t32s2";
         else if (sh.Kw == 7 && sh.Co <= 128)
             name = "k7c64p256t16s3";
-        else if (sh.Kw == 3 && tiles256 >= 128 && tiles256 <= 256)
+        else if (sh.Kw == 3 && tiles(192) >= 160 && tiles(192) <= 256)
+            name = "k3c256p192t32s2w8";
+        else if (sh.Kw == 3 && tiles(256) >= 160 && tiles(256) <= 256)
             name = "k3c256p256t32s2w8";
         else
             return -1;

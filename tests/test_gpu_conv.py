@@ -164,7 +164,7 @@ VARIANT_CASES = [
     # (environment variable, names, shape, dtype, same summation order)
     ("IM2WIN_FP16_TILE", ["c32p128s3", "c64p128s3", "c128p128s2", "c256p256s2w8", "c128p256s2w8"],
      (2, 16, 13, 13, 72, 5, 5, 1), torch.float16, True),
-    ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c128p256t16s3", "k3c256p256t32s2w8"],
+    ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c128p256t16s3", "k3c256p256t32s2w8", "k3c256p192t32s2w8"],
      (2, 64, 24, 24, 300, 3, 3, 1), torch.float16, False),
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p4c16l1s2k16", "regs"], (2, 16, 17, 19, 100, 3, 3, 1),
      torch.float32, True),
