@@ -128,6 +128,11 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
 // row-per-pixel kernels run instead.  The filter pack layout follows it.
 int col_plan(const Shape &sh);
 int col_stage_taps(int plan);  // taps per stage of that variant (packed-filter tile)
+// Segment-staged fp16 kernel for windows that are not 16-byte aligned: the
+// variant for this layer, or -1 when the register-staged kernel runs.
+int seg_plan(const Shape &sh);
+hipError_t launch_conv_fp16_seg(const Shape &sh, int plan, const void *ws, const void *packed,
+                                uint16_t *out, hipStream_t st);
 hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const void *packed,
                                 uint16_t *out, hipStream_t st);
 } // namespace im2win

@@ -600,7 +600,9 @@ hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed,
         a.tb = (uint32_t)col_stage_taps(plan);
     } else {
         a.nv = 1; a.tlen = (uint32_t)sh.K; a.tpad = (uint32_t)sh.K_pad;
-        a.tb = (sh.Ci % 8) == 0 ? (uint32_t)BK : a.tpad;  // pipelined or register-staged kernel
+        // pipelined and segment-staged kernels: 64-tap tiles; register-staged
+        // kernel: one tile of K_pad taps
+        a.tb = ((sh.Ci % 8) == 0 || seg_plan(sh) >= 0) ? (uint32_t)BK : a.tpad;
     }
     a.grans = (uint64_t)sh.Co_pad * a.nv * a.tpad / 8;
     a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad;
@@ -665,6 +667,9 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
         dim3 grid((uint32_t)((sh.P + p.bn - 1) / p.bn), (uint32_t)((sh.Co + p.bm - 1) / p.bm));
         return hipLaunchKernel(p.f, grid, dim3(p.nt), args, 0, st);
     }
+    const int sp = seg_plan(sh);
+    if (sp >= 0)
+        return launch_conv_fp16_seg(sh, sp, ws, packed, out, st);
     const void *f;
     int bm, bn;
     const bool unal = sh.K >= 128;

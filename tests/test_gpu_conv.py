@@ -39,6 +39,15 @@ EDGE = list(TINY) + [
     (5, 3, 40, 37, 96, 11, 11, 4),    # stem-like, K = 363
     (1, 130, 6, 6, 20, 3, 3, 1),      # K = 1170
     (300, 1, 3, 3, 5, 2, 2, 1),       # many tiny images: tiles span many strips
+    # segment-staged fp16 kernel (windows not 16-byte aligned): tiles over
+    # several strips and images, taps past K in the last 64-tap stage
+    (2, 3, 30, 70, 20, 3, 3, 1),      # tile spans an image boundary
+    (1, 5, 19, 150, 100, 5, 5, 2),    # K = 125: second stage ragged; C_o ragged in 128
+    (3, 3, 40, 61, 70, 11, 11, 4),    # 11 strips per 128-pixel tile, segments near the LDS limit
+    (2, 3, 9, 80, 40, 1, 1, 2),       # s > K_w: window step longer than the window
+    (2, 1, 50, 50, 8, 3, 3, 1),       # C_i = 1
+    (1, 20, 20, 100, 64, 3, 3, 1),    # C_i = 20: 8-byte aligned windows, K = 180
+    (2, 6, 13, 90, 200, 3, 5, 1),     # two channel tiles, the second ragged
     # column-staged fp16 kernel: strip runs inside a tile, taps past K_h*C_i
     # inside the last stage, ragged pixel and channel tiles
     (3, 24, 11, 30, 72, 3, 3, 1),     # K_h*C_i = 72: last stage 8 of 32 taps
@@ -64,7 +73,7 @@ def test_conv_edge_shapes(shape, dtype):
 
 
 @pytest.mark.parametrize("dtype", DTYPES, ids=DT_IDS)
-@pytest.mark.parametrize("shape", EDGE[-12:], ids=_id)
+@pytest.mark.parametrize("shape", EDGE[-19:], ids=_id)
 def test_conv_integer_inputs_exact(shape, dtype):
     """Inputs in {-2..2}: every partial sum is an integer below 2^24, so any
     summation order gives the exact result."""
@@ -155,6 +164,25 @@ def test_fp16_row_kernel_on_column_shapes(shape, monkeypatch):
     run.check_out_guards()
 
 
+# Windows that are not 16-byte aligned (C_i not a multiple of 8) go to the
+# segment-staged fp16 kernel when a tile's strip segments fit in LDS, else to
+# the register-staged one; IM2WIN_FP16_KERNEL=regs forces the latter, so both
+# are checked on the shapes that select the former.
+SEG_SHAPES = [(1, 3, 32, 32, 16, 3, 3, 1), (2, 3, 30, 70, 20, 3, 3, 1), (3, 3, 40, 61, 70, 11, 11, 4),
+              (2, 6, 13, 90, 200, 3, 5, 1)]
+
+
+@pytest.mark.parametrize("shape", SEG_SHAPES, ids=_id)
+def test_fp16_register_kernel_on_segment_shapes(shape, monkeypatch):
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    say("conv fp16 register-staged kernel", shape)
+    monkeypatch.setenv("IM2WIN_FP16_KERNEL", "regs")
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=19)
+    run = Run(x, w, s, torch.float16)
+    check_full(run, x, w)
+    run.check_out_guards()
+
+
 # Every kernel variant the launchers can pick (by layer or through the tuning
 # variables), on shapes that reach it: each must match the oracle, and where
 # the variants of a kernel accumulate K in the same order (the row-per-pixel
@@ -168,6 +196,8 @@ VARIANT_CASES = [
      (2, 64, 24, 24, 300, 3, 3, 1), torch.float16, False),
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p4c16l1s2k16", "regs"], (2, 16, 17, 19, 100, 3, 3, 1),
      torch.float32, True),
+    ("IM2WIN_FP16_SEG", ["s64p256", "s96p128", "s128p128"], (2, 6, 13, 90, 200, 3, 5, 1), torch.float16,
+     True),
 ]
 
 
@@ -190,3 +220,42 @@ def test_kernel_variants_agree(case, monkeypatch):
         elif same_order:
             assert np.array_equal(out.view(np.uint8), first.view(np.uint8)), name
 
+
+
+# Non-finite inputs stay inside the windows that hold them: an output is
+# finite exactly where the oracle's is (a kernel that multiplied the zero
+# filter padding past K by a neighbouring window's Inf would turn an
+# unrelated output into NaN), and the finite outputs meet the usual bar.
+# One shape per kernel path: fp32 DMA-staged and register-staged, fp16
+# pixel-row, column, segment and register-staged.
+NONFINITE_CASES = [
+    ((2, 16, 12, 14, 40, 3, 3, 1), torch.float32),
+    ((2, 3, 12, 14, 40, 3, 3, 1), torch.float32),
+    ((2, 16, 12, 14, 40, 5, 5, 1), torch.float16),
+    ((2, 16, 12, 40, 40, 3, 3, 1), torch.float16),
+    ((2, 3, 30, 70, 20, 3, 3, 1), torch.float16),
+    ((1, 12, 30, 30, 48, 5, 4, 2), torch.float16),
+]
+
+
+@pytest.mark.parametrize("case", NONFINITE_CASES, ids=lambda c: _id(c[0]) + ("-f32" if c[1] == torch.float32 else "-f16"))
+def test_nonfinite_inputs_stay_in_their_windows(case):
+    shape, dtype = case
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    say("non-finite", shape, dtype)
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=23)
+    rng = np.random.default_rng(23)
+    for v in (float("inf"), float("-inf"), float("inf"), float("nan")):
+        x[rng.integers(N), rng.integers(H), rng.integers(W), rng.integers(Ci)] = v
+    run = Run(x, w, s, dtype)
+    xo, wo = oracle_inputs(x, w, dtype)
+    with np.errstate(invalid="ignore", over="ignore"):
+        ref, absref = oracle.conv(xo, wo, s, with_abs=True)
+    y = run.out_np()
+    fin = np.isfinite(ref)
+    assert (~fin).any() and fin.any()
+    assert np.array_equal(np.isfinite(y), fin), "%d outputs differ in finiteness" % int(
+        (np.isfinite(y) != fin).sum())
+    r = rel_err(y[fin], ref[fin], absref[fin])
+    assert r <= TOL[dtype], "max |err|/sum|x||w| = %.3g" % r
+    run.check_out_guards()
