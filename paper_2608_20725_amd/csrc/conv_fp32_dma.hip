@@ -49,11 +49,15 @@ struct D32Args {
 // Lane tile TM pixels x TN channels; LC lanes of a wave share pixels and
 // split channels, so a wave covers (64/LC)*TM pixels x LC*TN channels; WCH of
 // the four waves lie along channels and the rest along pixels.
-template <int TM_, int TN_, int LC_, int WCH_, int NS_, int KC_ = 16>
+template <int TM_, int TN_, int LC_, int WCH_, int NS_, int KC_ = 16, int GR_ = 16>
 struct DCfg {
     static constexpr int TM = TM_, TN = TN_, LC = LC_, WCH = WCH_, NS = NS_, KC = KC_;
+    // bytes one lane moves per window load: 16 when every window starts on a
+    // 16-byte boundary (C_i a multiple of 4), else 4 (any fp32 window)
+    static constexpr int GR = GR_;
     static constexpr int QPR = KC / 4;            // 16-byte quads per window row
-    static constexpr int PPI = 64 / QPR;          // pixels per window load
+    static constexpr int LPR = KC * 4 / GR;       // lanes per window row in a load
+    static constexpr int PPI = 64 / LPR;          // pixels per window load
     static constexpr int NW = 4, NT = 256;
     static constexpr int WPX = NW / WCH;          // waves along pixels
     static constexpr int LP = 64 / LC;            // lane groups along pixels
@@ -64,13 +68,14 @@ struct DCfg {
     static_assert(CW == 64, "the filter slab loads cover 64 channels");
     static constexpr int WBYTES = BM * KC * 4;    // window part of a stage
     static constexpr int FBYTES = KC * CW * 4;    // filter part of a stage
-    static constexpr int IW = WBYTES / 1024 / NW;  // window loads per wave per stage
+    static constexpr int IW = WBYTES / (64 * GR) / NW;  // window loads per wave per stage
     // filter loads per wave per stage; loads past the slab read nothing into
     // a spare 1 KiB block, so every wave issues the same count
     static constexpr int IF = (FBYTES / 1024 + NW - 1) / NW;
     static constexpr int IB = IW + IF;
     static constexpr int STAGE_ALLOC = WBYTES + NW * IF * 1024;
-    static_assert(WBYTES % (1024 * NW) == 0, "even split over waves");
+    static_assert(WBYTES % (64 * GR * NW) == 0, "even split over waves");
+    static_assert(GR == 16 || GR == 4, "window load granule");
     static_assert(KC == 8 || KC == 16, "stage depth");
     static_assert(NS >= 2 && NS <= 3, "ring depth");
     static_assert((NS - 2) * IB <= 63, "vmcnt range");
@@ -95,7 +100,7 @@ template <class C>
 struct DTile {
     __amdgpu_buffer_rsrc_t rw, rf;
     uint32_t woff[C::IW];  // window byte offset at tap 0 (kOOB: no pixel)
-    uint32_t wk[C::IW];    // first tap of the quad within the stage
+    uint32_t wk;           // first tap of the lane's granule within the stage
     uint32_t foff[C::IF];  // filter byte offset at tap 0 (kOOB: column past the pad)
     uint32_t wave, lane, K, Co_pad, nst;
     float acc[C::TM][C::TN];
@@ -107,8 +112,8 @@ struct DTile {
 #pragma unroll
         for (int i = 0; i < C::IW; ++i) {
             const uint32_t b = wave + C::NW * i;
-            const uint32_t off = (!past && k0 + wk[i] < K) ? woff[i] + 4u * k0 : kOOB;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(slot + 1024 * b), 16, off, 0, 0, 0);
+            const uint32_t off = (!past && k0 + wk < K) ? woff[i] + 4u * k0 : kOOB;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(slot + 64 * C::GR * b), C::GR, off, 0, 0, 0);
         }
 #pragma unroll
         for (int i = 0; i < C::IF; ++i) {
@@ -198,19 +203,28 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
     w.rf = make_rsrc(a.packed, (uint32_t)(fbytes < kMaxRecords ? fbytes : kMaxRecords));
 
     // Window load i of this wave fills pixels PPI*b .. PPI*b+PPI-1 (b = wave
-    // + 4i): lane -> pixel PPI*b + lane/QPR, LDS slot lane%QPR, which holds
-    // quad wslot(pixel, lane%QPR) of the pixel's stage taps.
+    // + 4i): lane -> pixel PPI*b + lane/LPR and granule g = lane%LPR of its
+    // LDS row, in LDS quad g*GR/16; that quad holds quad wslot(pixel, .) of
+    // the pixel's stage taps (with 4-byte granules, element g%4 of it).  The
+    // tap depends on the pixel only through the swizzle bits of pl, which
+    // are the same for every load of a lane (PPI*b is a multiple of 16 when
+    // the swizzle uses pl & 3 and of 32 when it uses bit 3), so it is kept
+    // once per lane.
+    {
+        const uint32_t pl = w.lane / C::LPR;
+        const uint32_t g = w.lane % C::LPR;
+        w.wk = C::GR == 16 ? 4 * DTile<C>::wslot(pl, g) : 4 * DTile<C>::wslot(pl, g / 4) + g % 4;
+    }
+    static_assert(C::PPI % (C::QPR == 4 ? 4 : 16) == 0, "swizzle bits of pl fixed per lane");
 #pragma unroll
     for (int i = 0; i < C::IW; ++i) {
         const uint32_t b = w.wave + C::NW * i;
-        const uint32_t pl = C::PPI * b + w.lane / C::QPR;
-        const uint32_t qd = DTile<C>::wslot(pl, w.lane % C::QPR);
+        const uint32_t pl = C::PPI * b + w.lane / C::LPR;
         const uint32_t p = p0 + pl;
-        w.wk[i] = 4 * qd;
         w.woff[i] = kOOB;
         if (p < a.P) {
             const uint32_t q = fdiv(p, a.div_Wo);
-            w.woff[i] = ((q - q0) * a.L + (p - q * a.Wo) * a.S + 4 * qd) * 4u;
+            w.woff[i] = ((q - q0) * a.L + (p - q * a.Wo) * a.S + w.wk) * 4u;
         }
     }
     // Filter load i fills taps 4*b .. 4*b+3 of the slab (b = wave + 4i): lane
@@ -272,14 +286,14 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
 struct DVariant {
     const char *name;
     const void *f;
-    int bm, cw;
+    int bm, cw, gr;
 };
 
-template <int TM, int TN, int LC, int WCH, int NS, int KC>
+template <int TM, int TN, int LC, int WCH, int NS, int KC, int GR = 16>
 DVariant d_variant(const char *name)
 {
-    using C = DCfg<TM, TN, LC, WCH, NS, KC>;
-    return DVariant{name, (const void *)&conv_fp32_dma<C>, C::BM, C::CW};
+    using C = DCfg<TM, TN, LC, WCH, NS, KC, GR>;
+    return DVariant{name, (const void *)&conv_fp32_dma<C>, C::BM, C::CW, GR};
 }
 
 const DVariant *d_variants(int *n)
@@ -293,6 +307,8 @@ const DVariant *d_variants(int *n)
     static const DVariant v[] = {
         d_variant<8, 8, 8, 1, 2, 16>("p8c8l8s2k16"),
         d_variant<4, 16, 1, 4, 2, 16>("p4c16l1s2k16"),
+        // 4-byte window loads: windows that start anywhere (C_i % 4 != 0)
+        d_variant<8, 8, 8, 1, 2, 16, 4>("p8c8l8s2k16g4"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
@@ -302,22 +318,28 @@ const DVariant *d_variants(int *n)
 
 int dma32_plan(const Shape &sh)
 {
-    if (sh.Ci % 4 != 0)
-        return -1;  // windows not 16-byte aligned
     if (sh.K_pad32 * sh.Co_pad32 * 4 > (int64_t)kMaxRecords)
         return -1;  // filter offsets need 31 bits
+    // 16-byte window loads need every window on a 16-byte boundary
+    const bool aligned = sh.Ci % 4 == 0;
     int n;
     const DVariant *v = d_variants(&n);
-    const char *name = "p8c8l8s2k16";
+    const char *name = aligned ? "p8c8l8s2k16" : "p8c8l8s2k16g4";
     if (const char *e = getenv("IM2WIN_FP32_KERNEL")) {
         if (strcmp(e, "regs") == 0)
             return -1;
         name = e;
     }
-    for (int t = 0; t < n; ++t)
+    int pick = -1;
+    for (int t = 0; t < n; ++t) {
+        if (v[t].gr == 16 && !aligned)
+            continue;
+        if (pick < 0 && v[t].gr == (aligned ? 16 : 4))
+            pick = t;  // the first that fits, if the name matches none
         if (strcmp(name, v[t].name) == 0)
             return t;
-    return 0;
+    }
+    return pick;
 }
 
 hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const void *ws, const void *packed,

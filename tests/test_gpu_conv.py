@@ -194,14 +194,15 @@ VARIANT_CASES = [
      (2, 16, 13, 13, 72, 5, 5, 1), torch.float16, True),
     ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c128p256t16s3", "k3c256p256t32s2w8", "k3c256p192t32s2w8"],
      (2, 64, 24, 24, 300, 3, 3, 1), torch.float16, False),
-    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p4c16l1s2k16", "regs"], (2, 16, 17, 19, 100, 3, 3, 1),
-     torch.float32, True),
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16g4", "regs"],
+     (2, 16, 17, 19, 100, 3, 3, 1), torch.float32, True),
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16g4", "regs"], (3, 3, 40, 61, 70, 11, 11, 4), torch.float32, True),
     ("IM2WIN_FP16_SEG", ["s64p256", "s96p128", "s128p128"], (2, 6, 13, 90, 200, 3, 5, 1), torch.float16,
      True),
 ]
 
 
-@pytest.mark.parametrize("case", VARIANT_CASES, ids=lambda c: c[0])
+@pytest.mark.parametrize("case", VARIANT_CASES, ids=lambda c: c[0] + "-" + _id(c[2]))
 def test_kernel_variants_agree(case, monkeypatch):
     var, names, shape, dtype, same_order = case
     N, Ci, H, W, Co, Kh, Kw, s = shape
