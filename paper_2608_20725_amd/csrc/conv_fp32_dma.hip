@@ -47,33 +47,41 @@ struct D32Args {
 };
 
 // Lane tile TM pixels x TN channels; LC lanes of a wave share pixels and
-// split channels, so a wave covers (64/LC)*TM pixels x LC*TN channels; WCH of
-// the four waves lie along channels and the rest along pixels.
-template <int TM_, int TN_, int LC_, int WCH_, int NS_, int KC_ = 16, int GR_ = 16>
+// split channels, so a wave covers (64/LC)*TM pixels x LC*TN channels; of the
+// four waves, KS split the taps of a stage (each takes KC of them, and their
+// sums are added at the end), WCH lie along channels and the rest along
+// pixels.
+template <int TM_, int TN_, int LC_, int WCH_, int NS_, int KC_ = 16, int GR_ = 16, int KS_ = 1>
 struct DCfg {
     static constexpr int TM = TM_, TN = TN_, LC = LC_, WCH = WCH_, NS = NS_, KC = KC_;
     // bytes one lane moves per window load: 16 when every window starts on a
     // 16-byte boundary (C_i a multiple of 4), else 4 (any fp32 window)
     static constexpr int GR = GR_;
-    static constexpr int QPR = KC / 4;            // 16-byte quads per window row
-    static constexpr int LPR = KC * 4 / GR;       // lanes per window row in a load
+    static constexpr int KS = KS_;                // waves along the taps
+    static constexpr int KT = KS * KC;            // taps per stage
+    static constexpr int QPR = KC / 4;            // 16-byte quads per wave per stage
+    static constexpr int LPR = KT * 4 / GR;       // lanes per window row in a load
     static constexpr int PPI = 64 / LPR;          // pixels per window load
     static constexpr int NW = 4, NT = 256;
-    static constexpr int WPX = NW / WCH;          // waves along pixels
+    static constexpr int WPX = NW / (WCH * KS);   // waves along pixels
     static constexpr int LP = 64 / LC;            // lane groups along pixels
     static constexpr int WBM = LP * TM;           // pixels per wave
     static constexpr int BM = WPX * WBM;          // pixels per workgroup
     static constexpr int CW = WCH * LC * TN;      // channels per workgroup
-    static_assert(TN % 4 == 0 && NW % WCH == 0, "tile");
+    static_assert(TN % 4 == 0 && NW % (WCH * KS) == 0, "tile");
     static_assert(CW == 64, "the filter slab loads cover 64 channels");
-    static constexpr int WBYTES = BM * KC * 4;    // window part of a stage
-    static constexpr int FBYTES = KC * CW * 4;    // filter part of a stage
+    static_assert(KS == 1 || (KC == 16 && GR == 16), "tap split: 16-tap quads groups, 16-byte loads");
+    static constexpr int WBYTES = BM * KT * 4;    // window part of a stage
+    static constexpr int FBYTES = KT * CW * 4;    // filter part of a stage
     static constexpr int IW = WBYTES / (64 * GR) / NW;  // window loads per wave per stage
     // filter loads per wave per stage; loads past the slab read nothing into
     // a spare 1 KiB block, so every wave issues the same count
     static constexpr int IF = (FBYTES / 1024 + NW - 1) / NW;
     static constexpr int IB = IW + IF;
     static constexpr int STAGE_ALLOC = WBYTES + NW * IF * 1024;
+    // every wave's sums, for the final add of the tap slices
+    static constexpr int PART_BYTES = KS > 1 ? NW * TM * TN * 64 * 4 : 0;
+    static constexpr int RING = NS * STAGE_ALLOC > PART_BYTES ? NS * STAGE_ALLOC : PART_BYTES;
     static_assert(WBYTES % (64 * GR * NW) == 0, "even split over waves");
     static_assert(GR == 16 || GR == 4, "window load granule");
     static_assert(KC == 8 || KC == 16, "stage depth");
@@ -107,7 +115,7 @@ struct DTile {
 
     __device__ inline void issue(uint32_t st, char *slot)
     {
-        const uint32_t k0 = st * C::KC;
+        const uint32_t k0 = st * C::KT;
         const bool past = st >= nst;
 #pragma unroll
         for (int i = 0; i < C::IW; ++i) {
@@ -124,17 +132,24 @@ struct DTile {
         }
     }
 
-    // Window quad q of local pixel p sits at slot q ^ swz(p) of its row.
+    // Window quad q of local pixel p sits at slot q ^ swz(p) of its row (the
+    // swizzle stays inside each group of 4 quads).
     __device__ static inline uint32_t wslot(uint32_t p, uint32_t q)
     {
         return C::QPR == 4 ? q ^ (p & 3) : q ^ ((p >> 3) & 1);
     }
 
+    // this wave's place: tap slice, pixel group, channel group
+    __device__ inline uint32_t wks() const { return wave / (C::WCH * C::WPX); }
+    __device__ inline uint32_t wpx() const { return (wave / C::WCH) % C::WPX; }
+    __device__ inline uint32_t wch() const { return wave % C::WCH; }
+
     __device__ inline void compute(const char *slot)
     {
-        // this lane's channels of tap 0, and its first pixel
-        const char *fs = slot + C::WBYTES + ((wave % C::WCH) * C::LC + lane % C::LC) * C::TN * 4;
-        const uint32_t pl0 = (wave / C::WCH) * C::WBM + lane / C::LC;
+        // this lane's channels of the slice's first tap, and its first pixel
+        const uint32_t q0 = wks() * C::QPR;
+        const char *fs = slot + C::WBYTES + q0 * 4 * C::CW * 4 + (wch() * C::LC + lane % C::LC) * C::TN * 4;
+        const uint32_t pl0 = wpx() * C::WBM + lane / C::LC;
 #pragma unroll
         for (int q = 0; q < C::QPR; ++q) {
             // filter values of the quad's 4 taps
@@ -153,7 +168,10 @@ struct DTile {
 #pragma unroll
             for (int t = 0; t < C::TM; ++t) {
                 const uint32_t p = pl0 + C::LP * t;
-                const float4 v = *reinterpret_cast<const float4 *>(slot + p * (C::KC * 4) + 16 * wslot(p, q));
+                // q0 is a multiple of 4 and the swizzle stays inside groups of
+                // 4 quads: quad q0 + q of the row sits at slot q0 + wslot(p, q)
+                const float4 v =
+                    *reinterpret_cast<const float4 *>(slot + 16 * q0 + p * (C::KT * 4) + 16 * wslot(p, q));
                 const float x[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
@@ -164,8 +182,7 @@ struct DTile {
         }
     }
 
-    template <int N>
-    __device__ inline void step(uint32_t st, char (&cur)[N], char (&next)[N])
+    __device__ inline void step(uint32_t st, char *cur, char *next)
     {
         wait_vmcnt<(C::NS - 2) * C::IB>();
         ring_barrier();
@@ -178,10 +195,8 @@ struct DTile {
 template <class C>
 __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
 {
-    constexpr int S2 = C::NS > 2 ? C::STAGE_ALLOC : 1024;
-    __shared__ __attribute__((aligned(1024))) char r0[C::STAGE_ALLOC];
-    __shared__ __attribute__((aligned(1024))) char r1[C::STAGE_ALLOC];
-    __shared__ __attribute__((aligned(1024))) char r2[S2];
+    __shared__ __attribute__((aligned(1024))) char ring[C::RING];
+    char *const r0 = ring, *const r1 = ring + C::STAGE_ALLOC, *const r2 = ring + 2 * C::STAGE_ALLOC;
 
     DTile<C> w;
     const uint32_t tid = threadIdx.x;
@@ -190,7 +205,7 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
     __builtin_assume(w.wave < (uint32_t)C::NW);
     w.K = a.K;
     w.Co_pad = a.Co_pad;
-    w.nst = a.K_pad / C::KC;
+    w.nst = (a.K_pad + C::KT - 1) / C::KT;  // taps past K_pad read zero (masked, or past the filter)
     const uint32_t p0 = blockIdx.x * C::BM;
     const uint32_t jb = blockIdx.y * C::CW;  // first channel of the workgroup
 
@@ -233,7 +248,7 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
     for (int i = 0; i < C::IF; ++i) {
         const uint32_t b = w.wave + C::NW * i;
         const uint32_t row = 4 * b + w.lane / 16, col = jb + 4 * (w.lane % 16);
-        w.foff[i] = (row < (uint32_t)C::KC && col < a.Co_pad) ? (row * a.Co_pad + col) * 4u : kOOB;
+        w.foff[i] = (row < (uint32_t)C::KT && col < a.Co_pad) ? (row * a.Co_pad + col) * 4u : kOOB;
     }
 #pragma unroll
     for (int t = 0; t < C::TM; ++t)
@@ -258,11 +273,69 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
     // no load may still be writing LDS when the workgroup ends
     wait_vmcnt<0>();
 
-    // first channel of this lane
-    const uint32_t jw = jb + ((w.wave % C::WCH) * C::LC + w.lane % C::LC) * C::TN;
+    // first channel of this lane, and its first pixel
+    const uint32_t jw = jb + (w.wch() * C::LC + w.lane % C::LC) * C::TN;
+    const uint32_t pl0 = w.wpx() * C::WBM + w.lane / C::LC;
+    if constexpr (C::KS > 1) {
+        // Every wave stores its sums in LDS; then the KS waves with the same
+        // pixels and channels each finish TM/KS of the lane's pixel rows,
+        // adding the tap slices' sums in slice order (a fixed order: the
+        // result does not depend on timing).
+        constexpr int WAVE_PART = C::TM * C::TN * 64 * 4;
+        const uint32_t ks = w.wks(), grp = w.wpx() * C::WCH + w.wch();
+        auto part = [&](uint32_t k) {
+            return reinterpret_cast<float4 *>(ring + (k * (C::NW / C::KS) + grp) * WAVE_PART);
+        };
+        __syncthreads();  // every wave is done with the ring
+        float4 *mine = part(ks);
+#pragma unroll
+        for (int t = 0; t < C::TM; ++t)
+#pragma unroll
+            for (int c = 0; c < C::TN; c += 4)
+                mine[(t * (C::TN / 4) + c / 4) * 64 + w.lane] =
+                    make_float4(w.acc[t][c], w.acc[t][c + 1], w.acc[t][c + 2], w.acc[t][c + 3]);
+        __syncthreads();
+        if (jw >= a.Co)
+            return;
+        for (int r = 0; r < C::TM / C::KS; ++r) {
+            const uint32_t t = r * C::KS + ks;
+            const uint32_t p = p0 + pl0 + C::LP * t;
+            if (p >= a.P)
+                continue;
+            float v[C::TN];
+#pragma unroll
+            for (int c = 0; c < C::TN; c += 4) {
+                float4 sum = part(0)[(t * (C::TN / 4) + c / 4) * 64 + w.lane];
+#pragma unroll
+                for (int k = 1; k < C::KS; ++k) {
+                    const float4 u = part(k)[(t * (C::TN / 4) + c / 4) * 64 + w.lane];
+                    sum.x += u.x;
+                    sum.y += u.y;
+                    sum.z += u.z;
+                    sum.w += u.w;
+                }
+                v[c] = sum.x;
+                v[c + 1] = sum.y;
+                v[c + 2] = sum.z;
+                v[c + 3] = sum.w;
+            }
+            float *o = a.out + (uint64_t)p * a.Co + jw;
+            if (jw + C::TN <= a.Co && (a.Co & 3) == 0) {
+#pragma unroll
+                for (int c = 0; c < C::TN; c += 4)
+                    *reinterpret_cast<float4 *>(o + c) = make_float4(v[c], v[c + 1], v[c + 2], v[c + 3]);
+            } else {
+#pragma unroll
+                for (int c = 0; c < C::TN; ++c)
+                    if (jw + c < a.Co)
+                        o[c] = v[c];
+            }
+        }
+        return;
+    }
+
     if (jw >= a.Co)
         return;
-    const uint32_t pl0 = (w.wave / C::WCH) * C::WBM + w.lane / C::LC;
 #pragma unroll
     for (int t = 0; t < C::TM; ++t) {
         const uint32_t p = p0 + pl0 + C::LP * t;
@@ -289,26 +362,37 @@ struct DVariant {
     int bm, cw, gr;
 };
 
-template <int TM, int TN, int LC, int WCH, int NS, int KC, int GR = 16>
+template <int TM, int TN, int LC, int WCH, int NS, int KC, int GR = 16, int KS = 1>
 DVariant d_variant(const char *name)
 {
-    using C = DCfg<TM, TN, LC, WCH, NS, KC, GR>;
+    using C = DCfg<TM, TN, LC, WCH, NS, KC, GR, KS>;
     return DVariant{name, (const void *)&conv_fp32_dma<C>, C::BM, C::CW, GR};
 }
 
 const DVariant *d_variants(int *n)
 {
     // name: pixels x channels per lane, lanes along channels, ring slots,
-    // taps per stage
-    // Measured on MI355X over the benchmark layers: 8 x 8 lane tiles with
-    // 16-tap stages beat 4 x 16, 8 x 16, 12 x 8 and 16 x 8 tiles and 8-tap
-    // stages on every layer but one (larger tiles lose occupancy, 8-tap
-    // stages add barriers); 4 x 16 stays for comparison.
+    // taps per wave per stage, then g4 (4-byte window loads) or tN (the
+    // waves split a stage's taps N ways).
+    // Measured on MI355X over the benchmark layers, each conv right after
+    // its transform: 8 x 8 lane tiles with 16-tap stages beat 4 x 16,
+    // 8 x 16, 12 x 8 and 16 x 8 tiles and 8-tap stages (larger tiles lose
+    // occupancy, 8-tap stages add barriers).  With the taps split four ways
+    // (a 32- or 64-pixel tile, 64 taps per stage, 2 workgroups per CU)
+    // layers whose 256-pixel grid is small gain: 3x3 C=512 at 7x7 (104
+    // tiles) 18.5 -> 54.1 TFLOP/s with 64-pixel tiles, 3x3 C=256 at 14x14
+    // (288) 46.9 -> 62.8, 3x3 C=512 at 14x14 (576) 62.7 -> 73.3, 5x5 C_o=256
+    // at 24x24 (800) 65.9 -> 69.3 with 32-pixel tiles; from about 1500 tiles
+    // on (the 56x56 C=64 and 1x1 C=1024 layers) the 256-pixel tile is ahead
+    // again (69.8 vs 63.9, 70.7 vs 67.5).  Two-way splits, a 3-slot ring and
+    // the 256-pixel tile held to 2 workgroups per CU measured lower.
     static const DVariant v[] = {
         d_variant<8, 8, 8, 1, 2, 16>("p8c8l8s2k16"),
         d_variant<4, 16, 1, 4, 2, 16>("p4c16l1s2k16"),
         // 4-byte window loads: windows that start anywhere (C_i % 4 != 0)
         d_variant<8, 8, 8, 1, 2, 16, 4>("p8c8l8s2k16g4"),
+        d_variant<8, 8, 8, 1, 2, 16, 16, 4>("p8c8l8s2k16t4"),
+        d_variant<4, 8, 8, 1, 2, 16, 16, 4>("p4c8l8s2k16t4"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
@@ -318,13 +402,18 @@ const DVariant *d_variants(int *n)
 
 int dma32_plan(const Shape &sh)
 {
-    if (sh.K_pad32 * sh.Co_pad32 * 4 > (int64_t)kMaxRecords)
-        return -1;  // filter offsets need 31 bits
+    // filter offsets, up to one 64-tap stage past K_pad32, need 31 bits
+    if ((sh.K_pad32 + 64) * sh.Co_pad32 * 4 > (int64_t)kMaxRecords)
+        return -1;
     // 16-byte window loads need every window on a 16-byte boundary
     const bool aligned = sh.Ci % 4 == 0;
     int n;
     const DVariant *v = d_variants(&n);
-    const char *name = aligned ? "p8c8l8s2k16" : "p8c8l8s2k16g4";
+    const int64_t tiles256 = ((sh.P + 255) / 256) * ((sh.Co + 63) / 64);
+    const char *name = !aligned          ? "p8c8l8s2k16g4"
+                       : tiles256 <= 128  ? "p8c8l8s2k16t4"
+                       : tiles256 <= 1024 ? "p4c8l8s2k16t4"
+                                          : "p8c8l8s2k16";
     if (const char *e = getenv("IM2WIN_FP32_KERNEL")) {
         if (strcmp(e, "regs") == 0)
             return -1;

@@ -197,6 +197,10 @@ VARIANT_CASES = [
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16g4", "regs"],
      (2, 16, 17, 19, 100, 3, 3, 1), torch.float32, True),
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16g4", "regs"], (3, 3, 40, 61, 70, 11, 11, 4), torch.float32, True),
+    # taps split over the waves: another summation order, K = 144 ragged in
+    # 64-tap stages
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16t4", "p4c8l8s2k16t4"], (2, 16, 17, 19, 100, 3, 3, 1), torch.float32,
+     True),
     ("IM2WIN_FP16_SEG", ["s64p256", "s96p128", "s128p128"], (2, 6, 13, 90, 200, 3, 5, 1), torch.float16,
      True),
 ]
