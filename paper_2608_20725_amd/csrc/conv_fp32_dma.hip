@@ -51,7 +51,7 @@ struct D32Args {
 // four waves, KS split the taps of a stage (each takes KC of them, and their
 // sums are added at the end), WCH lie along channels and the rest along
 // pixels.
-template <int TM_, int TN_, int LC_, int WCH_, int NS_, int KC_ = 16, int GR_ = 16, int KS_ = 1>
+template <int TM_, int TN_, int LC_, int WCH_, int NS_, int KC_ = 16, int GR_ = 16, int KS_ = 1, int NW_ = 4>
 struct DCfg {
     static constexpr int TM = TM_, TN = TN_, LC = LC_, WCH = WCH_, NS = NS_, KC = KC_;
     // bytes one lane moves per window load: 16 when every window starts on a
@@ -62,7 +62,7 @@ struct DCfg {
     static constexpr int QPR = KC / 4;            // 16-byte quads per wave per stage
     static constexpr int LPR = KT * 4 / GR;       // lanes per window row in a load
     static constexpr int PPI = 64 / LPR;          // pixels per window load
-    static constexpr int NW = 4, NT = 256;
+    static constexpr int NW = NW_, NT = 64 * NW;  // waves, threads
     static constexpr int WPX = NW / (WCH * KS);   // waves along pixels
     static constexpr int LP = 64 / LC;            // lane groups along pixels
     static constexpr int WBM = LP * TM;           // pixels per wave
@@ -359,14 +359,14 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
 struct DVariant {
     const char *name;
     const void *f;
-    int bm, cw, gr;
+    int bm, cw, gr, nt;
 };
 
-template <int TM, int TN, int LC, int WCH, int NS, int KC, int GR = 16, int KS = 1>
+template <int TM, int TN, int LC, int WCH, int NS, int KC, int GR = 16, int KS = 1, int NW = 4>
 DVariant d_variant(const char *name)
 {
-    using C = DCfg<TM, TN, LC, WCH, NS, KC, GR, KS>;
-    return DVariant{name, (const void *)&conv_fp32_dma<C>, C::BM, C::CW, GR};
+    using C = DCfg<TM, TN, LC, WCH, NS, KC, GR, KS, NW>;
+    return DVariant{name, (const void *)&conv_fp32_dma<C>, C::BM, C::CW, GR, C::NT};
 }
 
 const DVariant *d_variants(int *n)
@@ -384,8 +384,10 @@ const DVariant *d_variants(int *n)
     // (288) 46.9 -> 62.8, 3x3 C=512 at 14x14 (576) 62.7 -> 73.3, 5x5 C_o=256
     // at 24x24 (800) 65.9 -> 69.3 with 32-pixel tiles; from about 1500 tiles
     // on (the 56x56 C=64 and 1x1 C=1024 layers) the 256-pixel tile is ahead
-    // again (69.8 vs 63.9, 70.7 vs 67.5).  Two-way splits, a 3-slot ring and
-    // the 256-pixel tile held to 2 workgroups per CU measured lower.
+    // again (69.8 vs 63.9, 70.7 vs 67.5).  Two-way splits, a 3-slot ring, the
+    // 256-pixel tile held to 2 workgroups per CU, and 128- or 64-pixel tiles
+    // of two or one waves (more, smaller workgroups: 68.1 vs 64.9 and 60.8
+    // on the 56x56 layer) measured lower.
     static const DVariant v[] = {
         d_variant<8, 8, 8, 1, 2, 16>("p8c8l8s2k16"),
         d_variant<4, 16, 1, 4, 2, 16>("p4c16l1s2k16"),
@@ -447,7 +449,7 @@ hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const void *ws, const
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     void *args[] = {&a};
     dim3 grid((uint32_t)((sh.P + v.bm - 1) / v.bm), (uint32_t)((sh.Co + v.cw - 1) / v.cw));
-    return hipLaunchKernel(v.f, grid, dim3(256), args, 0, st);
+    return hipLaunchKernel(v.f, grid, dim3(v.nt), args, 0, st);
 }
 
 }  // namespace im2win
