@@ -62,6 +62,10 @@ def _load():
         lib.oracle_im2win.argtypes = [_i64] * 7 + [_vp, _vp]
         lib.oracle_windowed_conv_f64.restype = ctypes.c_int
         lib.oracle_windowed_conv_f64.argtypes = [_i64] * 8 + [_dp, _dp, _dp]
+        lib.oracle_conv_pad_f64.restype = ctypes.c_int
+        lib.oracle_conv_pad_f64.argtypes = [_i64] * 10 + [_dp, _dp, _dp, _dp]
+        lib.oracle_im2win_pad.restype = ctypes.c_int
+        lib.oracle_im2win_pad.argtypes = [_i64] * 9 + [_vp, _vp]
         _lib = lib
     return _lib
 
@@ -166,3 +170,42 @@ def window_elems(N: int, Ci: int, Hi: int, Wi: int, Kh: int, stride: int) -> int
 
 def im2col_elems(N: int, Ci: int, Hi: int, Wi: int, Kh: int, Kw: int, stride: int) -> int:
     return int(_load().oracle_im2col_elems(N, Ci, Hi, Wi, Kh, Kw, stride))
+
+
+def conv_pad(x, w, stride: int, pad_h: int, pad_w: int, with_abs: bool = False):
+    """Eq. (1) on the input zero-padded by ``pad_h`` rows above and below and
+    ``pad_w`` columns left and right (an extension: the paper's layers have no
+    padding).  Returns O (and A = sum |x||w|, if ``with_abs``)."""
+    x = _f64(x)
+    w = _f64(w)
+    N, Hi, Wi, Ci = x.shape
+    Kh, Kw, Ci2, Co = w.shape
+    if Ci2 != Ci:
+        raise ValueError("channel mismatch")
+    Ho, Wo = out_extent(Hi + 2 * pad_h, Kh, stride), out_extent(Wi + 2 * pad_w, Kw, stride)
+    if Ho < 0 or Wo < 0 or pad_h < 0 or pad_w < 0:
+        raise ValueError("filter does not fit")
+    out = np.empty((N, Ho, Wo, Co), np.float64)
+    ab = np.empty_like(out) if with_abs else None
+    rc = _load().oracle_conv_pad_f64(N, Ci, Hi, Wi, Co, Kh, Kw, stride, pad_h, pad_w, _ptr(x), _ptr(w),
+                                     _ptr(out), _ptr(ab) if with_abs else None)
+    if rc != 0:
+        raise ValueError("oracle_conv_pad_f64 rejected its arguments")
+    return (out, ab) if with_abs else out
+
+
+def im2win_pad(x, k_h: int, stride: int, pad_h: int, pad_w: int) -> np.ndarray:
+    """Eq. (2) on the zero-padded input: [N][H_o][(W_i+2 pad_w)*K_h][C_i],
+    bit-exact, zero bytes at padded positions."""
+    x = np.ascontiguousarray(x)
+    N, Hi, Wi, Ci = x.shape
+    Ho = out_extent(Hi + 2 * pad_h, k_h, stride)
+    if Ho < 0 or pad_h < 0 or pad_w < 0:
+        raise ValueError("filter does not fit")
+    Wp = Wi + 2 * pad_w
+    out = np.empty((N, Ho, Wp * k_h, Ci), x.dtype)
+    rc = _load().oracle_im2win_pad(N, Ci, Hi, Wi, k_h, stride, pad_h, pad_w, x.dtype.itemsize,
+                                   x.ctypes.data_as(_vp), out.ctypes.data_as(_vp))
+    if rc != 0:
+        raise ValueError("oracle_im2win_pad rejected its arguments")
+    return out

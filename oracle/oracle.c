@@ -10,8 +10,9 @@
  *   - tensors are NHWC: input I[N][H_i][W_i][C_i], output O[N][H_o][W_o][C_o];
  *   - the filter is stored F[K_h][K_w][C_i][C_o] (height, width, input
  *     channel, output channel);
- *   - indices are 0-based, one stride s for both spatial axes, no padding,
- *     no dilation, no groups, no bias, no filter flip (cross-correlation);
+ *   - indices are 0-based, one stride s for both spatial axes, no padding
+ *     (except in the two *_pad functions), no dilation, no groups, no bias,
+ *     no filter flip (cross-correlation);
  *   - H_o = floor((H_i - K_h) / s) + 1 and W_o likewise (Table I sizes).
  *
  * Every function follows one passage of the paper:
@@ -23,6 +24,10 @@
  *   oracle_window_elems /      element counts of the window tensor (Eq. 2
  *   oracle_im2col_elems        index ranges) and of the im2col matrix
  *                              (Sec. III-B, Fig. 1 right)
+ *   oracle_conv_pad_f64 /      Eq. (1) and Eq. (2) on a zero-padded input
+ *   oracle_im2win_pad          (an extension: the paper's layers have no
+ *                              padding), read through an index rule, never
+ *                              built
  */
 #include <stdint.h>
 #include <string.h>
@@ -227,6 +232,109 @@ int oracle_windowed_conv_f64(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int6
                         }
                     }
                     out[((i * Ho + m) * Wo + n) * Co + j] = acc;
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+/*
+ * Zero padding (not in the paper's layers: its Table I convolutions have
+ * none).  The padded input is the input surrounded by ph zero rows above and
+ * below and pw zero columns left and right:
+ *   Ip[i][h][w][r] = I[i][h - ph][w - pw][r]  when 0 <= h - ph < H_i and
+ *                                               0 <= w - pw < W_i,
+ *                  = 0                          otherwise,
+ * of extent (H_i + 2 ph) x (W_i + 2 pw).  Both functions below read Ip
+ * through that rule; neither builds it.
+ */
+static int oracle_pad_tap(int64_t h, int64_t w, int64_t Hi, int64_t Wi)
+{
+    return h >= 0 && h < Hi && w >= 0 && w < Wi;
+}
+
+/*
+ * Eq. (1) on the padded input: the sum over (u, v, r) of
+ * Ip[i][m*s+u][n*s+v][r] * F[u][v][r][j], with H_o = floor((H_i + 2 ph -
+ * K_h) / s) + 1 and W_o likewise; `absout` (may be NULL) gets the |x||w| sum.
+ * Seven nested loops, fixed order (i, m, n, j, u, v, r), fp64.
+ */
+int oracle_conv_pad_f64(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co,
+                        int64_t Kh, int64_t Kw, int64_t s, int64_t ph, int64_t pw,
+                        const double *in, const double *filt,
+                        double *out, double *absout)
+{
+    if (ph < 0 || pw < 0 || Hi <= 0 || Wi <= 0)
+        return -1;
+    int64_t Ho = oracle_out_extent(Hi + 2 * ph, Kh, s);
+    int64_t Wo = oracle_out_extent(Wi + 2 * pw, Kw, s);
+    if (N <= 0 || Ci <= 0 || Co <= 0 || Ho < 0 || Wo < 0)
+        return -1;
+
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t i = 0; i < N; ++i) {
+        for (int64_t m = 0; m < Ho; ++m) {
+            for (int64_t n = 0; n < Wo; ++n) {
+                for (int64_t j = 0; j < Co; ++j) {
+                    double acc = 0.0, aacc = 0.0;
+                    for (int64_t u = 0; u < Kh; ++u) {
+                        for (int64_t v = 0; v < Kw; ++v) {
+                            int64_t h = m * s + u - ph, w = n * s + v - pw;
+                            if (!oracle_pad_tap(h, w, Hi, Wi))
+                                continue;  /* a zero of the padding adds 0 */
+                            for (int64_t r = 0; r < Ci; ++r) {
+                                double x = in[((i * Hi + h) * Wi + w) * Ci + r];
+                                double f = filt[((u * Kw + v) * Ci + r) * Co + j];
+                                acc += x * f;
+                                aacc += fabs(x) * fabs(f);
+                            }
+                        }
+                    }
+                    int64_t o = ((i * Ho + m) * Wo + n) * Co + j;
+                    out[o] = acc;
+                    if (absout)
+                        absout[o] = aacc;
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+/*
+ * Eq. (2) on the padded input:
+ *   W[i][m][k*K_h + u][r] = Ip[i][m*s + u][k][r]
+ * for i<N, m<H_o, k<W_i+2pw, u<K_h, r<C_i; padded positions are all-zero
+ * bytes (the zero of every element type used here).  Raw `elt`-byte copies.
+ */
+int oracle_im2win_pad(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi,
+                      int64_t Kh, int64_t s, int64_t ph, int64_t pw, int64_t elt,
+                      const void *in, void *out)
+{
+    if (ph < 0 || pw < 0 || Hi <= 0 || Wi <= 0)
+        return -1;
+    int64_t Hp = Hi + 2 * ph, Wp = Wi + 2 * pw;
+    int64_t Ho = oracle_out_extent(Hp, Kh, s);
+    if (N <= 0 || Ci <= 0 || Ho < 0 || elt <= 0)
+        return -1;
+    const unsigned char *src = (const unsigned char *)in;
+    unsigned char *dst = (unsigned char *)out;
+
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t i = 0; i < N; ++i) {
+        for (int64_t m = 0; m < Ho; ++m) {
+            for (int64_t k = 0; k < Wp; ++k) {
+                for (int64_t u = 0; u < Kh; ++u) {
+                    int64_t h = m * s + u - ph, w = k - pw;
+                    for (int64_t r = 0; r < Ci; ++r) {
+                        int64_t d = ((i * Ho + m) * (Wp * Kh) + (k * Kh + u)) * Ci + r;
+                        if (oracle_pad_tap(h, w, Hi, Wi))
+                            memcpy(dst + d * elt, src + (((i * Hi + h) * Wi + w) * Ci + r) * elt,
+                                   (size_t)elt);
+                        else
+                            memset(dst + d * elt, 0, (size_t)elt);
+                    }
                 }
             }
         }

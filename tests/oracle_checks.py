@@ -264,10 +264,90 @@ def check_sizes_match_materialised(orc):
         assert orc.im2win(x, Kh, s).size == orc.window_elems(N, Ci, H, W, Kh, s)
 
 
+# Zero padding (an extension; the paper's layers have none), pinned against
+# torch's padded conv2d, against the unpadded oracle on an explicitly padded
+# input, and against closed forms.
+PAD_CASES = [
+    # N, Ci, H, W, Co, Kh, Kw, s, pad_h, pad_w
+    (2, 3, 5, 6, 4, 3, 3, 1, 1, 1),     # "same" 3x3
+    (1, 2, 7, 5, 3, 3, 2, 2, 2, 1),     # K_h != K_w, stride 2, pad_h != pad_w
+    (2, 4, 4, 4, 2, 2, 3, 3, 0, 2),     # padding on one axis only
+    (1, 1, 3, 2, 2, 2, 2, 1, 3, 3),     # pad larger than the filter: all-zero rims
+    (3, 5, 6, 7, 6, 5, 5, 1, 2, 2),     # "same" 5x5
+]
+
+
+def _torch_conv_pad(x, w, s, ph, pw):
+    xt = torch.from_numpy(np.ascontiguousarray(x, np.float64)).permute(0, 3, 1, 2)
+    wt = torch.from_numpy(np.ascontiguousarray(w, np.float64)).permute(3, 2, 0, 1)
+    y = torch.nn.functional.conv2d(xt, wt.contiguous(), stride=s, padding=(ph, pw))
+    return y.permute(0, 2, 3, 1).contiguous().numpy()
+
+
+def _zero_pad(x, ph, pw):
+    return np.pad(x, ((0, 0), (ph, ph), (pw, pw), (0, 0)))
+
+
+def check_pad_vs_torch_conv2d(orc):
+    for t, (N, Ci, H, W, Co, Kh, Kw, s, ph, pw) in enumerate(PAD_CASES):
+        r = _rng(60 + t)
+        x = r.uniform(-1, 1, (N, H, W, Ci))
+        w = r.uniform(-1, 1, (Kh, Kw, Ci, Co))
+        y = orc.conv_pad(x, w, s, ph, pw)
+        ref = _torch_conv_pad(x, w, s, ph, pw)
+        assert y.shape == ref.shape, (y.shape, ref.shape)
+        np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12)
+
+
+def check_pad_vs_explicit_zeros(orc):
+    # integer inputs: the padded sum equals the unpadded sum over the padded
+    # array exactly, and so does the |x||w| sum
+    for t, (N, Ci, H, W, Co, Kh, Kw, s, ph, pw) in enumerate(PAD_CASES):
+        r = _rng(70 + t)
+        x = r.integers(-2, 3, (N, H, W, Ci)).astype(np.float64)
+        w = r.integers(-2, 3, (Kh, Kw, Ci, Co)).astype(np.float64)
+        y, a = orc.conv_pad(x, w, s, ph, pw, with_abs=True)
+        ref = _slice_conv(_zero_pad(x, ph, pw), w, s)
+        aref = _slice_conv(np.abs(_zero_pad(x, ph, pw)), np.abs(w), s)
+        assert np.array_equal(y, ref) and np.array_equal(a, aref)
+
+
+def check_pad_same_delta(orc):
+    # centred delta filter with pad (K-1)/2 and stride 1: output = input
+    for (K, Ci) in [(3, 2), (5, 3)]:
+        x = _rng(80 + K).uniform(-1, 1, (2, 6, 5, Ci))
+        w = np.zeros((K, K, Ci, Ci))
+        for c in range(Ci):
+            w[K // 2, K // 2, c, c] = 1.0
+        y = orc.conv_pad(x, w, 1, K // 2, K // 2)
+        assert np.array_equal(y, x)
+
+
+def check_pad_zero_is_unpadded(orc):
+    for t, (N, Ci, H, W, Co, Kh, Kw, s) in enumerate(TINY):
+        r = _rng(90 + t)
+        x = r.uniform(-1, 1, (N, H, W, Ci))
+        w = r.uniform(-1, 1, (Kh, Kw, Ci, Co))
+        assert np.array_equal(orc.conv_pad(x, w, s, 0, 0), orc.conv(x, w, s))
+        x16 = x.astype(np.float16)
+        assert orc.im2win_pad(x16, Kh, s, 0, 0).tobytes() == orc.im2win(x16, Kh, s).tobytes()
+
+
+def check_im2win_pad_layout(orc):
+    for t, (N, Ci, H, W, Co, Kh, Kw, s, ph, pw) in enumerate(PAD_CASES):
+        r = _rng(100 + t)
+        for dt in (np.float32, np.float16):
+            x = r.uniform(-1, 1, (N, H, W, Ci)).astype(dt)
+            win = orc.im2win_pad(x, Kh, s, ph, pw)
+            assert win.dtype == dt
+            assert win.tobytes() == _numpy_im2win(_zero_pad(x, ph, pw), Kh, s).tobytes()
+
+
 ALL_CHECKS = [
     check_table1_extents, check_fig1_shapes, check_vs_torch_conv2d, check_vs_strided_slices,
     check_1x1_is_matmul, check_delta_filter, check_full_filter_is_dot, check_linearity,
     check_abs_sum, check_points, check_im2win_layout, check_im2win_identity,
     check_windows_contiguous, check_windowed_equals_direct, check_sizes,
-    check_sizes_match_materialised,
+    check_sizes_match_materialised, check_pad_vs_torch_conv2d, check_pad_vs_explicit_zeros,
+    check_pad_same_delta, check_pad_zero_is_unpadded, check_im2win_pad_layout,
 ]

@@ -39,6 +39,17 @@ MUTANTS = [
      "double x = w[((n * s + v) * Kw + u) * Ci + r];", 0),
     ("window_elems_no_Kh", "return N * Ho * Wi * Kh * Ci;", "return N * Ho * Wi * Ci;", 0),
     ("im2col_elems_Kh_twice", "return N * Ho * Wo * Kh * Kw * Ci;", "return N * Ho * Wo * Kh * Kh * Ci;", 0),
+    ("pad_shift_sign", "int64_t h = m * s + u - ph, w = n * s + v - pw;",
+     "int64_t h = m * s + u + ph, w = n * s + v - pw;", 0),
+    ("pad_swapped_axes", "int64_t h = m * s + u - ph, w = n * s + v - pw;",
+     "int64_t h = m * s + u - pw, w = n * s + v - ph;", 0),
+    ("pad_bound_off_by_one", "return h >= 0 && h < Hi && w >= 0 && w < Wi;",
+     "return h >= 0 && h < Hi && w >= 0 && w + 1 < Wi;", 0),
+    ("pad_extent_one_side", "int64_t Ho = oracle_out_extent(Hi + 2 * ph, Kh, s);",
+     "int64_t Ho = oracle_out_extent(Hi + ph, Kh, s);", 0),
+    ("im2win_pad_no_shift", "int64_t h = m * s + u - ph, w = k - pw;", "int64_t h = m * s + u, w = k;", 0),
+    ("im2win_pad_strip_width", "int64_t d = ((i * Ho + m) * (Wp * Kh) + (k * Kh + u)) * Ci + r;",
+     "int64_t d = ((i * Ho + m) * (Wi * Kh) + (k * Kh + u)) * Ci + r;", 0),
 ]
 
 
