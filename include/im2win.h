@@ -123,6 +123,28 @@ int conv_im2win_transform(const void *in_nhwc, void *ws, int64_t ws_bytes,
                           void *hip_stream);
 
 /*
+ * The im2win transform of a zero-padded input (Eq. 2 applied to the input
+ * surrounded by pad_h zero rows above and below and pad_w zero columns left
+ * and right; the paper's layers have no padding, real CNN layers do).  The
+ * padded input is never built: window-tensor positions outside the stored
+ * input are written as zeros.
+ *   in_nhwc  device, the stored input I [N][H_i][W_i][C_i], read only
+ *   ws       device, workspace of ws_bytes >= conv_workspace_bytes(N, C_i,
+ *            H_i + 2*pad_h, W_i + 2*pad_w, ..., dt); layout as above for the
+ *            padded extents
+ *   pad_h, pad_w  >= 0; pad 0 gives exactly conv_im2win_transform's result
+ * The convolution of the padded layer is then conv_im2win_fp32/fp16 called
+ * with H_i + 2*pad_h and W_i + 2*pad_w as the input extents (their output is
+ * H_o = floor((H_i + 2*pad_h - K_h)/s) + 1 by W_o likewise).  Errors as for
+ * conv_im2win_transform, with the padded extents checked as the layer
+ * (IM2WIN_EINVAL for a negative pad, IM2WIN_ERANGE for pads above 2^29).
+ */
+int conv_im2win_transform_padded(const void *in_nhwc, void *ws, int64_t ws_bytes, int64_t N,
+                                 int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h,
+                                 int64_t K_w, int64_t stride, int64_t pad_h, int64_t pad_w,
+                                 im2win_dtype_t dt, void *hip_stream);
+
+/*
  * fp32 windowed convolution on the vector ALUs (Sec. III-C, Eq. 3; the
  * paper's CUDA-core variant, Sec. IV-A).
  *   ws              device, workspace holding the fp32 window tensor written
@@ -154,7 +176,6 @@ int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
                      uint16_t *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream);
 
-/* A static, human-readable name for a status code. */
 /*
  * Mini-batch im2win: bytes of workspace conv_im2win_chunked needs for chunks
  * of n_chunk images (n_chunk is clamped to N), with one window-tensor slot, or
@@ -199,6 +220,7 @@ int conv_im2win_chunked(const void *in_nhwc, const void *filt_khkwcico, void *ou
                         int64_t K_h, int64_t K_w, int64_t stride, int64_t n_chunk, im2win_dtype_t dt,
                         void *hip_stream, void *hip_stream_aux);
 
+/* A static, human-readable name for a status code. */
 const char *conv_im2win_strerror(int status);
 
 #ifdef __cplusplus

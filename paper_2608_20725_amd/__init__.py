@@ -8,6 +8,7 @@ kernels; there is no fallback, and a missing library raises.
     H_o, W_o = conv_output_dims(H_i, W_i, K_h, K_w, stride)
     nbytes   = conv_workspace_bytes(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dtype)
     conv_im2win_transform(x, ws, C_o, K_h, K_w, stride)        # Sec. III-B, Eq. 2
+    conv_im2win_transform_padded(x, ws, C_o, K_h, K_w, stride, pad_h, pad_w)
     conv_im2win_fp32(ws, w, out, N, C_i, H_i, W_i, stride)     # Sec. III-C, Eq. 3
     conv_im2win_fp16(ws, w, out, N, C_i, H_i, W_i, stride)     # Sec. III-D, Alg. 1
 
@@ -22,7 +23,7 @@ import os
 __all__ = [
     "Im2winError", "load_library", "library_path", "F32", "F16",
     "conv_output_dims", "conv_workspace_bytes", "conv_im2col_bytes",
-    "conv_im2win_transform", "conv_im2win_fp32", "conv_im2win_fp16",
+    "conv_im2win_transform", "conv_im2win_transform_padded", "conv_im2win_fp32", "conv_im2win_fp16",
     "conv_im2win_strerror", "im2win_conv2d",
 ]
 
@@ -64,6 +65,8 @@ def load_library():
     lib.conv_im2col_bytes.argtypes = [_i64] * 7 + [ctypes.c_int]
     lib.conv_im2win_transform.restype = ctypes.c_int
     lib.conv_im2win_transform.argtypes = [_vp, _vp, _i64] + [_i64] * 8 + [ctypes.c_int, _vp]
+    lib.conv_im2win_transform_padded.restype = ctypes.c_int
+    lib.conv_im2win_transform_padded.argtypes = [_vp, _vp, _i64] + [_i64] * 10 + [ctypes.c_int, _vp]
     lib.conv_im2win_fp32.restype = ctypes.c_int
     lib.conv_im2win_fp32.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
     lib.conv_im2win_fp16.restype = ctypes.c_int
@@ -144,6 +147,20 @@ def conv_im2win_transform(x, ws, C_o: int, K_h: int, K_w: int, stride: int, stre
         _ptr(x), _ptr(ws), _nbytes(ws), N, C_i, H_i, W_i, C_o, K_h, K_w, stride,
         _dtype_code(x.dtype), _stream(stream))
     _check(rc, "conv_im2win_transform")
+
+
+def conv_im2win_transform_padded(x, ws, C_o: int, K_h: int, K_w: int, stride: int, pad_h: int,
+                                 pad_w: int, stream=None):
+    """Writes the window tensor of ``x`` zero-padded by ``pad_h`` rows and
+    ``pad_w`` columns on each side into ``ws`` (sized for the padded extents);
+    the convolutions then take ``H_i + 2*pad_h`` and ``W_i + 2*pad_w``."""
+    if x.dim() != 4 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous NHWC tensor")
+    N, H_i, W_i, C_i = x.shape
+    rc = load_library().conv_im2win_transform_padded(
+        _ptr(x), _ptr(ws), _nbytes(ws), N, C_i, H_i, W_i, C_o, K_h, K_w, stride, pad_h, pad_w,
+        _dtype_code(x.dtype), _stream(stream))
+    _check(rc, "conv_im2win_transform_padded")
 
 
 def _conv(fn, what, ws, w, out, N, C_i, H_i, W_i, stride, stream):

@@ -43,6 +43,8 @@ int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_
         return IM2WIN_EINVAL;
     if (Kh > Hi || Kw > Wi)
         return IM2WIN_EINVAL;
+    if (Hi > INT32_MAX || Wi > INT32_MAX)  // row and column indices are 32-bit in the kernels
+        return IM2WIN_ERANGE;
     Shape r;
     memset(&r, 0, sizeof r);
     r.N = N; r.Ci = Ci; r.Hi = Hi; r.Wi = Wi; r.Co = Co; r.Kh = Kh; r.Kw = Kw; r.s = s;
@@ -208,6 +210,45 @@ int conv_im2win_transform(const void *in_nhwc, void *ws, int64_t ws_bytes, int64
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
     return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream));
+}
+
+int conv_im2win_transform_padded(const void *in_nhwc, void *ws, int64_t ws_bytes, int64_t N,
+                                 int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h,
+                                 int64_t K_w, int64_t stride, int64_t pad_h, int64_t pad_w,
+                                 im2win_dtype_t dt, void *hip_stream)
+{
+    if (!in_nhwc || !ws)
+        return IM2WIN_EINVAL;
+    if (pad_h < 0 || pad_w < 0 || H_i <= 0 || W_i <= 0)
+        return IM2WIN_EINVAL;
+    if (pad_h > INT32_MAX / 4 || pad_w > INT32_MAX / 4 || H_i > INT32_MAX || W_i > INT32_MAX)
+        return IM2WIN_ERANGE;
+    Shape sh;  // the padded layer
+    int rc = make_shape(N, C_i, H_i + 2 * pad_h, W_i + 2 * pad_w, C_o, K_h, K_w, stride, (int)dt, &sh);
+    if (rc != IM2WIN_OK)
+        return rc;
+    if (!transform_range_ok(sh))
+        return IM2WIN_ERANGE;
+    if (!aligned16(in_nhwc) || !aligned16(ws))
+        return IM2WIN_EALIGN;
+    int64_t in_bytes;  // the stored input, without the padding
+    if (!mul_ok(N * H_i, W_i * C_i, kMaxBytes / 4, &in_bytes))
+        return IM2WIN_ERANGE;
+    in_bytes *= sh.elt;
+    if (ws_bytes < 0)
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_extent(in_nhwc, in_bytes)) != IM2WIN_OK)
+        return rc;
+    if ((rc = check_extent(ws, ws_bytes)) != IM2WIN_OK)
+        return rc;
+    if (overlaps(in_nhwc, in_bytes, ws, ws_bytes))
+        return IM2WIN_EOVERLAP;
+    if (ws_bytes < workspace_bytes(sh, (int)dt))
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_device()) != IM2WIN_OK)
+        return rc;
+    const Pad pad{H_i, W_i, pad_h, pad_w};
+    return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream, &pad));
 }
 
 int conv_im2win_fp32(void *ws, int64_t ws_bytes, const float *filt_khkwcico,

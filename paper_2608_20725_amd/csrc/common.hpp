@@ -112,7 +112,14 @@ int launch_status(hipError_t e);
 namespace im2win {
 // The gather form of the transform indexes elements with 32 bits.
 bool transform_range_ok(const Shape &sh);
-hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st);
+// Zero padding folded into the transform: the Shape describes the padded
+// layer; Hi x Wi is the input actually stored, ph/pw the zero rows above and
+// below / columns left and right.
+struct Pad {
+    int64_t Hi, Wi, ph, pw;
+};
+hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st,
+                            const Pad *pad = nullptr);
 hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hipStream_t st);
 hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed, float *out,
                             hipStream_t st);

@@ -13,6 +13,11 @@
 //             assembles one 16-byte granule of the flat window tensor element
 //             by element; granules may straddle strips.
 // Both zero the pad bytes that follow the window tensor.
+//
+// Zero padding of the input (not in the paper's layers) is folded in: the
+// window tensor is that of the input surrounded by ph zero rows and pw zero
+// columns on each side, and positions outside the stored input are written
+// as zeros; the padded input itself is never built.
 #include "common.hpp"
 
 namespace im2win {
@@ -24,7 +29,8 @@ constexpr int kGranPerThread = 4;
 struct TArgs {
     const char *in;
     char *ws;
-    uint32_t Ci, Hi, Wi, Kh, s, Ho;
+    uint32_t Ci, Hi, Wi, Kh, s, Ho;  // Hi x Wi: the stored (unpadded) input
+    uint32_t Wp, ph, pw;             // strip columns Wi + 2*pw; zero rows / columns per side
     uint32_t L;              // strip length (elements)
     uint32_t strips;
     uint32_t gran_per_strip; // vec: 16-byte granules per strip
@@ -75,8 +81,14 @@ __global__ __launch_bounds__(kThreads) void transform_vec(TArgs a)
             const uint32_t r = pos - seg * a.Ci;
             const uint32_t k = fdiv(seg, a.div_Kh);
             const uint32_t u = seg - k * a.Kh;
-            const uint64_t src = (((uint64_t)i * a.Hi + m * a.s + u) * a.Wi + k) * a.Ci + r;
-            const uint4 v = *reinterpret_cast<const uint4 *>(a.in + src * ELT);
+            // a granule lies inside one (column, row) piece of C_i elements:
+            // all of it is padding or none
+            const int32_t h = (int32_t)(m * a.s + u) - (int32_t)a.ph, w = (int32_t)k - (int32_t)a.pw;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (h >= 0 && h < (int32_t)a.Hi && w >= 0 && w < (int32_t)a.Wi) {
+                const uint64_t src = (((uint64_t)i * a.Hi + (uint32_t)h) * a.Wi + (uint32_t)w) * a.Ci + r;
+                v = *reinterpret_cast<const uint4 *>(a.in + src * ELT);
+            }
             *reinterpret_cast<uint4 *>(a.ws + (uint64_t)g * 16) = v;
         }
     }
@@ -116,19 +128,22 @@ __global__ __launch_bounds__(kThreads) void transform_gather(TArgs a)
 #pragma unroll
     for (uint32_t t = 0; t < V; ++t) {
         if ((uint64_t)e + t < a.win_elems) {
-            const uint64_t src = (((uint64_t)i * a.Hi + m * a.s + u) * a.Wi + k) * a.Ci + r;
-            uint32_t bits;
-            if (ELT == 4)
-                bits = reinterpret_cast<const uint32_t *>(a.in)[src];
-            else
-                bits = reinterpret_cast<const uint16_t *>(a.in)[src];
+            const int32_t hh = (int32_t)(m * a.s + u) - (int32_t)a.ph, ww = (int32_t)k - (int32_t)a.pw;
+            uint32_t bits = 0;
+            if (hh >= 0 && hh < (int32_t)a.Hi && ww >= 0 && ww < (int32_t)a.Wi) {
+                const uint64_t src = (((uint64_t)i * a.Hi + (uint32_t)hh) * a.Wi + (uint32_t)ww) * a.Ci + r;
+                if (ELT == 4)
+                    bits = reinterpret_cast<const uint32_t *>(a.in)[src];
+                else
+                    bits = reinterpret_cast<const uint16_t *>(a.in)[src];
+            }
             store_elem<ELT>(w, (int)t, bits);
             // advance (r, u, k, m, i) to the next window-tensor element
             if (++r == a.Ci) {
                 r = 0;
                 if (++u == a.Kh) {
                     u = 0;
-                    if (++k == a.Wi) {
+                    if (++k == a.Wp) {
                         k = 0;
                         if (++m == a.Ho) {
                             m = 0;
@@ -152,12 +167,20 @@ bool transform_range_ok(const Shape &sh)
     return (uint64_t)sh.win_elems + 16 < (1ull << 32);
 }
 
-hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st)
+hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st, const Pad *pad)
 {
     TArgs a;
     a.in = static_cast<const char *>(in);
     a.ws = static_cast<char *>(ws);
-    a.Ci = (uint32_t)sh.Ci; a.Hi = (uint32_t)sh.Hi; a.Wi = (uint32_t)sh.Wi;
+    a.Ci = (uint32_t)sh.Ci;
+    a.Wp = (uint32_t)sh.Wi;
+    if (pad) {
+        a.Hi = (uint32_t)pad->Hi; a.Wi = (uint32_t)pad->Wi;
+        a.ph = (uint32_t)pad->ph; a.pw = (uint32_t)pad->pw;
+    } else {
+        a.Hi = (uint32_t)sh.Hi; a.Wi = (uint32_t)sh.Wi;
+        a.ph = 0; a.pw = 0;
+    }
     a.Kh = (uint32_t)sh.Kh; a.s = (uint32_t)sh.s; a.Ho = (uint32_t)sh.Ho;
     a.L = (uint32_t)sh.L;
     a.strips = (uint32_t)sh.strips;

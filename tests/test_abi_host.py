@@ -197,3 +197,18 @@ def test_chunked_rejects(lib):
     # null pointers first
     assert lib.conv_im2win_chunked(None, v(256), v(512), v(1024), 1 << 20, 4, 8, 10, 10, 16, 3, 3, 1, 2,
                                    pkg.F32, None, None) == EINVAL
+
+
+def test_padded_transform_checks(lib):
+    v = ctypes.c_void_p
+    f = lib.conv_im2win_transform_padded
+    # null pointers first, then dims: negative pads, a filter larger than the
+    # padded input, pads past the range
+    assert f(None, v(0x100000), 1 << 20, 1, 3, 8, 8, 4, 3, 3, 1, 1, 1, pkg.F32, None) == EINVAL
+    assert f(v(0x1000), v(0x100000), 1 << 20, 1, 3, 8, 8, 4, 3, 3, 1, -1, 0, pkg.F32, None) == EINVAL
+    assert f(v(0x1000), v(0x100000), 1 << 20, 1, 3, 8, 8, 4, 3, 3, 1, 0, -2, pkg.F32, None) == EINVAL
+    assert f(v(0x1000), v(0x100000), 1 << 20, 1, 3, 2, 2, 4, 5, 5, 1, 1, 1, pkg.F32, None) == EINVAL
+    assert f(v(0x1000), v(0x100000), 1 << 20, 1, 3, 8, 8, 4, 3, 3, 1, 1 << 40, 0, pkg.F32, None) == ERANGE
+    # a filter that fits only thanks to the padding passes the dims: the
+    # misaligned input is what is rejected
+    assert f(v(0x1008), v(0x100000), 1 << 20, 1, 3, 2, 2, 4, 3, 3, 1, 1, 1, pkg.F32, None) == EALIGN
