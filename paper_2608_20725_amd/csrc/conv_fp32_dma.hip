@@ -79,9 +79,14 @@ struct DCfg {
     static constexpr int IF = (FBYTES / 1024 + NW - 1) / NW;
     static constexpr int IB = IW + IF;
     static constexpr int STAGE_ALLOC = WBYTES + NW * IF * 1024;
-    // every wave's sums, for the final add of the tap slices
-    static constexpr int PART_BYTES = KS > 1 ? NW * TM * TN * 64 * 4 : 0;
-    static constexpr int RING = NS * STAGE_ALLOC > PART_BYTES ? NS * STAGE_ALLOC : PART_BYTES;
+    // every wave's sums, for the final add of the tap slices: NW parts of
+    // WAVE_PART bytes laid over the ring slots, none straddling two slots
+    static constexpr int WAVE_PART = KS > 1 ? TM * TN * 64 * 4 : 1024;
+    static constexpr int PART_BYTES = KS > 1 ? NW * WAVE_PART : 0;
+    static constexpr int SLOT_MIN = (STAGE_ALLOC + WAVE_PART - 1) / WAVE_PART * WAVE_PART;
+    static constexpr int SLOT_PART = ((PART_BYTES + NS - 1) / NS + WAVE_PART - 1) / WAVE_PART * WAVE_PART;
+    // bytes of one ring slot (each slot is an LDS array of its own)
+    static constexpr int SLOT = SLOT_MIN > SLOT_PART ? SLOT_MIN : SLOT_PART;
     static_assert(WBYTES % (64 * GR * NW) == 0, "even split over waves");
     static_assert(GR == 16 || GR == 4, "window load granule");
     static_assert(KC == 8 || KC == 16, "stage depth");
@@ -144,6 +149,16 @@ struct DTile {
     __device__ inline uint32_t wpx() const { return (wave / C::WCH) % C::WPX; }
     __device__ inline uint32_t wch() const { return wave % C::WCH; }
 
+    // Accumulator slot c of a lane holds channel c ^ 1 of its channel group,
+    // and the filter values are unpacked to match.  The FMA acc[t][c] +=
+    // x * f[c] then finds its accumulator and its filter value in different
+    // VGPR banks (the compiler gives both arrays the same bank alignment).
+    // On gfx950 two waves of a SIMD issue fp32 FMAs together at full rate
+    // unless the accumulator and the second source share a bank while the
+    // first source stays in one bank from one FMA to the next (measured:
+    // ~94 vs ~128 TFLOP/s at four waves per SIMD); the loop below repeats its
+    // pixel operand over eight FMAs, so the pairing decides.  Sums and their
+    // order are unchanged; the stores undo the permutation.
     __device__ inline void compute(const char *slot)
     {
         // this lane's channels of the slice's first tap, and its first pixel
@@ -160,10 +175,12 @@ struct DTile {
                 for (int c = 0; c < C::TN; c += 4) {
                     const float4 v =
                         *reinterpret_cast<const float4 *>(fs + (4 * q + e) * C::CW * 4 + 4 * c);
-                    f[e][c] = v.x;
-                    f[e][c + 1] = v.y;
-                    f[e][c + 2] = v.z;
-                    f[e][c + 3] = v.w;
+                    // accumulator slot c holds channel c ^ 1 (see the
+                    // note above compute)
+                    f[e][c] = v.y;
+                    f[e][c + 1] = v.x;
+                    f[e][c + 2] = v.w;
+                    f[e][c + 3] = v.z;
                 }
 #pragma unroll
             for (int t = 0; t < C::TM; ++t) {
@@ -182,7 +199,12 @@ struct DTile {
         }
     }
 
-    __device__ inline void step(uint32_t st, char *cur, char *next)
+    // The slots are passed as the LDS arrays themselves: once inlined, every
+    // access names its array, so the compiler can tell that reading the
+    // current slot does not depend on the loads just issued into the next
+    // one and does not wait for them.
+    template <int N>
+    __device__ inline void step(uint32_t st, char (&cur)[N], char (&next)[N])
     {
         wait_vmcnt<(C::NS - 2) * C::IB>();
         ring_barrier();
@@ -195,8 +217,11 @@ struct DTile {
 template <class C>
 __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
 {
-    __shared__ __attribute__((aligned(1024))) char ring[C::RING];
-    char *const r0 = ring, *const r1 = ring + C::STAGE_ALLOC, *const r2 = ring + 2 * C::STAGE_ALLOC;
+    // ring slots: separate arrays (see DTile::step)
+    constexpr int S2 = C::NS > 2 ? C::SLOT : 1024;
+    __shared__ __attribute__((aligned(1024))) char r0[C::SLOT];
+    __shared__ __attribute__((aligned(1024))) char r1[C::SLOT];
+    __shared__ __attribute__((aligned(1024))) char r2[S2];
 
     DTile<C> w;
     const uint32_t tid = threadIdx.x;
@@ -281,10 +306,15 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
         // pixels and channels each finish TM/KS of the lane's pixel rows,
         // adding the tap slices' sums in slice order (a fixed order: the
         // result does not depend on timing).
-        constexpr int WAVE_PART = C::TM * C::TN * 64 * 4;
+        constexpr int PPS = C::SLOT / C::WAVE_PART;  // parts per slot
+        static_assert(C::NS * PPS >= C::NW, "the parts fit in the ring");
         const uint32_t ks = w.wks(), grp = w.wpx() * C::WCH + w.wch();
         auto part = [&](uint32_t k) {
-            return reinterpret_cast<float4 *>(ring + (k * (C::NW / C::KS) + grp) * WAVE_PART);
+            const uint32_t idx = k * (C::NW / C::KS) + grp;
+            char *slot = idx < (uint32_t)PPS ? r0 : r1;
+            if constexpr (C::NS > 2)
+                slot = idx < 2u * PPS ? slot : r2;
+            return reinterpret_cast<float4 *>(slot + (idx % PPS) * C::WAVE_PART);
         };
         __syncthreads();  // every wave is done with the ring
         float4 *mine = part(ks);
@@ -319,16 +349,17 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
                 v[c + 2] = sum.z;
                 v[c + 3] = sum.w;
             }
+            // slot c holds channel c ^ 1
             float *o = a.out + (uint64_t)p * a.Co + jw;
             if (jw + C::TN <= a.Co && (a.Co & 3) == 0) {
 #pragma unroll
                 for (int c = 0; c < C::TN; c += 4)
-                    *reinterpret_cast<float4 *>(o + c) = make_float4(v[c], v[c + 1], v[c + 2], v[c + 3]);
+                    *reinterpret_cast<float4 *>(o + c) = make_float4(v[c + 1], v[c], v[c + 3], v[c + 2]);
             } else {
 #pragma unroll
                 for (int c = 0; c < C::TN; ++c)
                     if (jw + c < a.Co)
-                        o[c] = v[c];
+                        o[c] = v[c ^ 1];
             }
         }
         return;
@@ -341,17 +372,18 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
         const uint32_t p = p0 + pl0 + C::LP * t;
         if (p >= a.P)
             continue;
+        // slot c holds channel c ^ 1
         float *o = a.out + (uint64_t)p * a.Co + jw;
         if (jw + C::TN <= a.Co && (a.Co & 3) == 0) {
 #pragma unroll
             for (int c = 0; c < C::TN; c += 4)
                 *reinterpret_cast<float4 *>(o + c) =
-                    make_float4(w.acc[t][c], w.acc[t][c + 1], w.acc[t][c + 2], w.acc[t][c + 3]);
+                    make_float4(w.acc[t][c + 1], w.acc[t][c], w.acc[t][c + 3], w.acc[t][c + 2]);
         } else {
 #pragma unroll
             for (int c = 0; c < C::TN; ++c)
                 if (jw + c < a.Co)
-                    o[c] = w.acc[t][c];
+                    o[c] = w.acc[t][c ^ 1];
         }
     }
 }
