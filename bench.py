@@ -12,7 +12,9 @@ Per-kernel durations come from HIP events recorded on the stream the kernels
 are launched on, around every call in the timed region.
 
 Prints ONE JSON line.  `--layer NAME` picks another configured layer and
-`--sweep` prints one line per configured layer instead (for reports).
+`--sweep` prints one line per configured layer instead (for reports).  Each
+line also carries a `bf16` block: the same layer with bf16 operands on the
+same matrix-core kernels, timed outside the step (an extension of the path).
 """
 from __future__ import annotations
 
@@ -30,7 +32,7 @@ if ROOT not in sys.path:
 # MI355X published peaks
 PEAK_HBM_GBS = 8000.0
 PEAK_FP32_VECTOR_TF = 157.3     # 256 CU x 256 flop/clk x 2.4 GHz
-PEAK_FP16_MFMA_TF = 2516.6      # dense
+PEAK_FP16_MFMA_TF = 2516.6      # dense (bf16 the same)
 
 # HBM-side bytes per launch of the fp32 conv kernel, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE counters (FETCH_SIZE scaled by 2.0 and WRITE_SIZE by 1.0, the
@@ -98,7 +100,7 @@ class Path:
         need = pkg.conv_workspace_bytes(l.N, l.C_i, l.H, l.W, l.C_o, l.K_h, l.K_w, l.stride, dtype)
         self.ws = torch.empty(need, dtype=torch.uint8, device=dev)
         self.out = torch.empty((l.N, Ho, Wo, l.C_o), dtype=dtype, device=dev)
-        self.conv = pkg.conv_im2win_fp32 if dtype == torch.float32 else pkg.conv_im2win_fp16
+        self.conv = pkg.conv_for_dtype(dtype)
 
     def transform(self):
         l = self.l
@@ -132,6 +134,37 @@ def measure_minibatch(l, paths, pkg, torch, n_chunk=32, reps=10):
                      "full_batch_workspace_bytes": p.ws.numel()}
         del ws
     return res
+
+
+def measure_bf16(l, x, w, pkg, torch, reps=20):
+    """The bf16 operand path (an extension beside the fp16 one: same kernels,
+    bf16 MFMA) on the same layer, outside the timed step: median transform
+    and pack+conv times over `reps` runs, HIP events on the launch stream."""
+    p = Path(l, x, w, torch.bfloat16, pkg, torch)
+    for _ in range(3):
+        p.transform()
+        p.run_conv()
+    torch.cuda.synchronize()
+    tr, cv = [], []
+    for _ in range(reps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record()
+        p.transform()
+        e[1].record()
+        p.run_conv()
+        e[2].record()
+        torch.cuda.synchronize()
+        tr.append(e[0].elapsed_time(e[1]))
+        cv.append(e[1].elapsed_time(e[2]))
+    tr.sort()
+    cv.sort()
+    Ho, Wo = pkg.conv_output_dims(l.H, l.W, l.K_h, l.K_w, l.stride)
+    flops = 2.0 * l.N * Ho * Wo * l.C_o * l.K_h * l.K_w * l.C_i
+    ms_t, ms_c = tr[reps // 2], cv[reps // 2]
+    del p
+    return {"transform_ms": round(ms_t, 5), "pack_conv_ms": round(ms_c, 5),
+            "TFLOP/s": round(flops / (ms_c * 1e-3) / 1e12, 3),
+            "frac_bf16_mfma": round(flops / (ms_c * 1e-3) / 1e12 / PEAK_FP16_MFMA_TF, 4)}
 
 
 def cpu_baseline(l, x, w, budget_s=10.0):
@@ -301,6 +334,7 @@ def main():
                 "allocator_peak_bytes": peak_alloc,
             },
         }
+        rec["bf16"] = measure_bf16(l, x, w, pkg, torch)
         if not args.sweep:
             mb = measure_minibatch(l, paths, pkg, torch)
             for name in ("f32", "f16"):

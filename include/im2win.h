@@ -25,7 +25,7 @@
  *                     the buffer
  *     [pad_end, ...)  the filter repacked in window order (tap k = (v*K_h+u)*C_i+r)
  *                     and zero-padded, written by the conv call:
- *                       fp16: C_o_pad*K_w*T_pad fp16 values, C_o_pad = round_up(C_o, 256),
+ *                       fp16 / bf16: C_o_pad*K_w*T_pad 16-bit values, C_o_pad = round_up(C_o, 256),
  *                             T_pad = round_up(K_h*C_i, 64): tiles of TB taps, each
  *                             holding C_o_pad rows per slice, either one slice of
  *                             K_pad = round_up(K, 64) taps or one slice of T_pad taps
@@ -50,8 +50,8 @@
  * (each pointer must lie in one device allocation that holds the whole
  * buffer) -> overlap -> workspace size -> device -> launch.  The first failing
  * check's status is returned; nothing is printed and no exception leaves the
- * library.  Numerics: fp32 conv accumulates in fp32 (FMA); fp16 conv takes
- * fp16 operands, accumulates in fp32 and rounds to nearest-even on store.
+ * library.  Numerics: fp32 conv accumulates in fp32 (FMA); fp16 and bf16 conv
+ * take 16-bit operands, accumulate in fp32 and round to nearest-even on store.
  */
 #ifndef IM2WIN_H
 #define IM2WIN_H
@@ -62,7 +62,8 @@
 extern "C" {
 #endif
 
-typedef enum { IM2WIN_F32 = 0, IM2WIN_F16 = 1 } im2win_dtype_t;
+/* Element types: fp32, IEEE fp16, bf16 (bfloat16: fp32's 8-bit exponent, 8-bit significand). */
+typedef enum { IM2WIN_F32 = 0, IM2WIN_F16 = 1, IM2WIN_BF16 = 2 } im2win_dtype_t;
 
 enum {
     IM2WIN_OK = 0,
@@ -90,7 +91,7 @@ int conv_output_dims(int64_t H_i, int64_t W_i, int64_t K_h, int64_t K_w, int64_t
  *
  * Index ranges the kernels support (else IM2WIN_ERANGE): one strip
  * W_i*K_h*C_i < 2^20 elements, K = K_h*K_w*C_i < 2^24, C_o < 2^19,
- * N*H_o*W_o < 2^31 output pixels, N*H_o < 2^31 strips, for IM2WIN_F16 a packed
+ * N*H_o*W_o < 2^31 output pixels, N*H_o < 2^31 strips, for IM2WIN_F16/BF16 a packed
  * filter (above) below 2^31 bytes, and every byte count below 2^62.
  */
 int64_t conv_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
@@ -107,7 +108,7 @@ int64_t conv_im2col_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
 
 /*
  * The im2win transform (Sec. III-B, Eq. 2).
- *   in_nhwc  device, input I (fp32 or fp16 bits, per `dt`), read only
+ *   in_nhwc  device, input I (fp32, fp16 or bf16 bits, per `dt`), read only
  *   ws       device, workspace of ws_bytes >= conv_workspace_bytes(..., dt);
  *            the window tensor and the zero pad are written, the rest of the
  *            workspace is left alone
@@ -177,6 +178,26 @@ int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream);
 
 /*
+ * bf16 windowed convolution on the matrix cores: the same product as
+ * conv_im2win_fp16 (Sec. III-D, Alg. 1) with bf16 operands.  An extension:
+ * the paper's multi-precision support (Sec. III-F) has two variants, fp32 on
+ * the vector units and fp16 on the matrix units; bf16 is a third operand type
+ * for the same kernels, with fp32's exponent range.
+ *   ws              device, workspace holding the bf16 window tensor written
+ *                   by conv_im2win_transform(..., IM2WIN_BF16); the window
+ *                   tensor is read, the packed-filter region is overwritten
+ *   filt_khkwcico   device, bf16 bits of F [K_h][K_w][C_i][C_o]; read only
+ *   out_nhwc        device, bf16 bits of O [N][H_o][W_o][C_o]; every element
+ *                   is written exactly once
+ * Products of bf16 operands are accumulated in fp32; each output is rounded
+ * to bf16 (nearest-even) once.  Workspace, index ranges and errors as for
+ * conv_im2win_fp16 (the workspace of IM2WIN_BF16 equals that of IM2WIN_F16).
+ */
+int conv_im2win_bf16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
+                     uint16_t *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
+                     int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream);
+
+/*
  * Mini-batch im2win: bytes of workspace conv_im2win_chunked needs for chunks
  * of n_chunk images (n_chunk is clamped to N), with one window-tensor slot, or
  * two when two_streams is non-zero:
@@ -191,9 +212,9 @@ int64_t conv_chunked_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_
 /*
  * Transform + windowed convolution of the whole batch in chunks of n_chunk
  * images (the mini-batch strategy of Sec. IV-C, against the full-batch
- * conv_im2win_transform + conv_im2win_fp32/fp16 pair): the workspace holds the
+ * conv_im2win_transform + conv_im2win_fp32/fp16/bf16 pair): the workspace holds the
  * window tensor of one chunk, or of two when a second stream is given.
- *   in_nhwc         device, input I (fp32 or fp16 bits per `dt`), read only
+ *   in_nhwc         device, input I (fp32, fp16 or bf16 bits per `dt`), read only
  *   filt_khkwcico   device, filter F, read only
  *   out_nhwc        device, output O, written once per element
  *   ws              device, ws_bytes >= conv_chunked_workspace_bytes(...,
@@ -211,7 +232,7 @@ int64_t conv_chunked_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_
  *                   hip_stream.  The ordering uses two HIP events that the
  *                   library creates on first use per host thread and device
  *                   and keeps (no device memory is allocated).
- * The output is bit-identical to conv_im2win_fp32/fp16 on the full batch.
+ * The output is bit-identical to conv_im2win_fp32/fp16/bf16 on the full batch.
  * Errors as for the other calls; input, filter, output and workspace must not
  * overlap, and the two streams must differ.
  */

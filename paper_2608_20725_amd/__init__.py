@@ -11,6 +11,7 @@ kernels; there is no fallback, and a missing library raises.
     conv_im2win_transform_padded(x, ws, C_o, K_h, K_w, stride, pad_h, pad_w)
     conv_im2win_fp32(ws, w, out, N, C_i, H_i, W_i, stride)     # Sec. III-C, Eq. 3
     conv_im2win_fp16(ws, w, out, N, C_i, H_i, W_i, stride)     # Sec. III-D, Alg. 1
+    conv_im2win_bf16(ws, w, out, N, C_i, H_i, W_i, stride)     # same, bf16 operands
 
 Layouts: ``x`` NHWC, ``w`` [K_h][K_w][C_i][C_o], ``out`` NHWC; ``ws`` is a
 flat byte tensor on the same device.
@@ -21,14 +22,16 @@ import ctypes
 import os
 
 __all__ = [
-    "Im2winError", "load_library", "library_path", "F32", "F16",
+    "Im2winError", "load_library", "library_path", "F32", "F16", "BF16",
     "conv_output_dims", "conv_workspace_bytes", "conv_im2col_bytes",
     "conv_im2win_transform", "conv_im2win_transform_padded", "conv_im2win_fp32", "conv_im2win_fp16",
+    "conv_im2win_bf16",
     "conv_im2win_strerror", "im2win_conv2d",
 ]
 
 F32 = 0
 F16 = 1
+BF16 = 2
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libim2win.so")
@@ -71,6 +74,8 @@ def load_library():
     lib.conv_im2win_fp32.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
     lib.conv_im2win_fp16.restype = ctypes.c_int
     lib.conv_im2win_fp16.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
+    lib.conv_im2win_bf16.restype = ctypes.c_int
+    lib.conv_im2win_bf16.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
     lib.conv_chunked_workspace_bytes.restype = _i64
     lib.conv_chunked_workspace_bytes.argtypes = [_i64] * 9 + [ctypes.c_int, ctypes.c_int]
     lib.conv_im2win_chunked.restype = ctypes.c_int
@@ -91,7 +96,9 @@ def _dtype_code(dtype) -> int:
         return F32
     if dtype in (F16, "f16", "fp16", torch.float16):
         return F16
-    raise ValueError("dtype must be fp32 or fp16, got %r" % (dtype,))
+    if dtype in (BF16, "bf16", torch.bfloat16):
+        return BF16
+    raise ValueError("dtype must be fp32, fp16 or bf16, got %r" % (dtype,))
 
 
 def _stream(stream):
@@ -139,7 +146,7 @@ def conv_im2col_bytes(N, C_i, H_i, W_i, K_h, K_w, stride, dtype) -> int:
 
 
 def conv_im2win_transform(x, ws, C_o: int, K_h: int, K_w: int, stride: int, stream=None):
-    """Writes the window tensor of NHWC input ``x`` (fp32 or fp16) into ``ws``."""
+    """Writes the window tensor of NHWC input ``x`` (fp32, fp16 or bf16) into ``ws``."""
     if x.dim() != 4 or not x.is_contiguous():
         raise ValueError("x must be a contiguous NHWC tensor")
     N, H_i, W_i, C_i = x.shape
@@ -192,6 +199,20 @@ def conv_im2win_fp16(ws, w, out, N: int, C_i: int, H_i: int, W_i: int, stride: i
           stride, stream)
 
 
+def conv_im2win_bf16(ws, w, out, N: int, C_i: int, H_i: int, W_i: int, stride: int, stream=None):
+    """bf16 conv (fp32 accumulation) from the bf16 window tensor in ``ws``."""
+    import torch
+    if w.dtype != torch.bfloat16 or out.dtype != torch.bfloat16:
+        raise TypeError("conv_im2win_bf16 takes bf16 filter and output")
+    _conv(load_library().conv_im2win_bf16, "conv_im2win_bf16", ws, w, out, N, C_i, H_i, W_i,
+          stride, stream)
+
+
+def conv_for_dtype(dtype):
+    """The conv entry point for an element type (fp32, fp16 or bf16)."""
+    return (conv_im2win_fp32, conv_im2win_fp16, conv_im2win_bf16)[_dtype_code(dtype)]
+
+
 def im2win_conv2d(x, w, stride: int, ws=None, out=None, stream=None):
     """Transform + conv on the current stream; allocates what is not given.
 
@@ -206,10 +227,7 @@ def im2win_conv2d(x, w, stride: int, ws=None, out=None, stream=None):
     if out is None:
         out = torch.empty((N, H_o, W_o, C_o), dtype=x.dtype, device=x.device)
     conv_im2win_transform(x, ws, C_o, K_h, K_w, stride, stream)
-    if x.dtype == torch.float32:
-        conv_im2win_fp32(ws, w, out, N, C_i, H_i, W_i, stride, stream)
-    else:
-        conv_im2win_fp16(ws, w, out, N, C_i, H_i, W_i, stride, stream)
+    conv_for_dtype(x.dtype)(ws, w, out, N, C_i, H_i, W_i, stride, stream)
     return out, ws
 
 

@@ -37,7 +37,7 @@ namespace im2win {
 int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_t Kh,
                int64_t Kw, int64_t s, int dt, Shape *sh)
 {
-    if (dt != IM2WIN_F32 && dt != IM2WIN_F16)
+    if (dt != IM2WIN_F32 && dt != IM2WIN_F16 && dt != IM2WIN_BF16)
         return IM2WIN_EINVAL;
     if (N <= 0 || Ci <= 0 || Hi <= 0 || Wi <= 0 || Co <= 0 || Kh <= 0 || Kw <= 0 || s <= 0)
         return IM2WIN_EINVAL;
@@ -72,8 +72,8 @@ int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_
     r.K_pad32 = round_up(r.K, 16);
     r.Co_pad32 = round_up(Co, 32);
     r.Tp = round_up(Kh * Ci, 64);
-    // the fp16 kernels address the packed filter with 31-bit offsets
-    if (dt == IM2WIN_F16 && r.Co_pad * r.Kw * r.Tp * 2 >= (int64_t)kMaxRecords)
+    // the 16-bit kernels address the packed filter with 31-bit offsets
+    if (dt != IM2WIN_F32 && r.Co_pad * r.Kw * r.Tp * 2 >= (int64_t)kMaxRecords)
         return IM2WIN_ERANGE;
     *sh = r;
     return IM2WIN_OK;
@@ -81,8 +81,8 @@ int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_
 
 int64_t packed_filter_bytes(const Shape &sh, int dt)
 {
-    // fp16: room for every packed layout (C_o_pad*K_pad <= C_o_pad*K_w*Tp)
-    return dt == IM2WIN_F16 ? sh.Co_pad * sh.Kw * sh.Tp * 2 : sh.K_pad32 * sh.Co_pad32 * 4;
+    // fp16 / bf16: room for every packed layout (C_o_pad*K_pad <= C_o_pad*K_w*Tp)
+    return dt != IM2WIN_F32 ? sh.Co_pad * sh.Kw * sh.Tp * 2 : sh.K_pad32 * sh.Co_pad32 * 4;
 }
 
 int64_t workspace_bytes(const Shape &sh, int dt) { return sh.pad_end + packed_filter_bytes(sh, dt); }
@@ -283,14 +283,19 @@ int conv_im2win_fp32(void *ws, int64_t ws_bytes, const float *filt_khkwcico,
     return launch_status(launch_conv_fp32(sh, ws, packed, out_nhwc, (hipStream_t)hip_stream));
 }
 
-int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
-                     uint16_t *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
-                     int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream)
+}  // extern "C"
+
+namespace {
+
+// The 16-bit matrix-core convolution, fp16 or bf16 operands (`dt`, `op`).
+int conv16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico, uint16_t *out_nhwc, int64_t N,
+           int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride,
+           void *hip_stream, int dt, Op16 op)
 {
     if (!ws || !filt_khkwcico || !out_nhwc)
         return IM2WIN_EINVAL;
     Shape sh;
-    int rc = make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, IM2WIN_F16, &sh);
+    int rc = make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dt, &sh);
     if (rc != IM2WIN_OK)
         return rc;
     if (!aligned16(ws) || !aligned16(filt_khkwcico) || !aligned16(out_nhwc))
@@ -305,14 +310,34 @@ int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
     if (overlaps(ws, ws_bytes, out_nhwc, o_bytes) || overlaps(filt_khkwcico, f_bytes, out_nhwc, o_bytes) ||
         overlaps(ws, ws_bytes, filt_khkwcico, f_bytes))
         return IM2WIN_EOVERLAP;
-    if (ws_bytes < workspace_bytes(sh, IM2WIN_F16))
+    if (ws_bytes < workspace_bytes(sh, dt))
         return IM2WIN_EWORKSPACE;
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
     void *packed = (char *)ws + sh.pad_end;
     if ((rc = launch_status(launch_pack_fp16(sh, filt_khkwcico, packed, (hipStream_t)hip_stream))) != IM2WIN_OK)
         return rc;
-    return launch_status(launch_conv_fp16(sh, ws, packed, out_nhwc, (hipStream_t)hip_stream));
+    return launch_status(launch_conv_fp16(sh, ws, packed, out_nhwc, (hipStream_t)hip_stream, op));
+}
+
+}  // namespace
+
+extern "C" {
+
+int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
+                     uint16_t *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
+                     int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream)
+{
+    return conv16(ws, ws_bytes, filt_khkwcico, out_nhwc, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, hip_stream,
+                  IM2WIN_F16, Op16::F16);
+}
+
+int conv_im2win_bf16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
+                     uint16_t *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
+                     int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream)
+{
+    return conv16(ws, ws_bytes, filt_khkwcico, out_nhwc, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, hip_stream,
+                  IM2WIN_BF16, Op16::BF16);
 }
 
 const char *conv_im2win_strerror(int status)

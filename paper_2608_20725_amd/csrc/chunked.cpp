@@ -148,7 +148,8 @@ int run_chunked(const void *in, const void *filt, void *out, void *ws, int64_t w
         if (dt == IM2WIN_F32)
             rc = launch_status(launch_conv_fp32(sh, wsl, packed, reinterpret_cast<float *>(outc), cs));
         else
-            rc = launch_status(launch_conv_fp16(sh, wsl, packed, reinterpret_cast<uint16_t *>(outc), cs));
+            rc = launch_status(launch_conv_fp16(sh, wsl, packed, reinterpret_cast<uint16_t *>(outc), cs,
+                                                dt == IM2WIN_BF16 ? Op16::BF16 : Op16::F16));
         if (rc != IM2WIN_OK)
             return rc;
     }
@@ -170,7 +171,7 @@ int64_t conv_chunked_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_
                                      int64_t K_h, int64_t K_w, int64_t stride, int64_t n_chunk,
                                      int two_streams, im2win_dtype_t dt)
 {
-    if (dt != IM2WIN_F32 && dt != IM2WIN_F16)
+    if (dt != IM2WIN_F32 && dt != IM2WIN_F16 && dt != IM2WIN_BF16)
         return IM2WIN_EINVAL;
     Plan p;
     int rc = make_plan(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, n_chunk, two_streams, (int)dt, &p);
@@ -184,7 +185,7 @@ int conv_im2win_chunked(const void *in_nhwc, const void *filt_khkwcico, void *ou
                         int64_t K_h, int64_t K_w, int64_t stride, int64_t n_chunk, im2win_dtype_t dt,
                         void *hip_stream, void *hip_stream_aux)
 {
-    if (dt != IM2WIN_F32 && dt != IM2WIN_F16)
+    if (dt != IM2WIN_F32 && dt != IM2WIN_F16 && dt != IM2WIN_BF16)
         return IM2WIN_EINVAL;
     return run_chunked(in_nhwc, filt_khkwcico, out_nhwc, ws, ws_bytes, N, C_i, H_i, W_i, C_o, K_h, K_w, stride,
                        n_chunk, (int)dt, (hipStream_t)hip_stream, (hipStream_t)hip_stream_aux);

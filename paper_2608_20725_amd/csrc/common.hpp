@@ -128,9 +128,12 @@ hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed,
 int dma32_plan(const Shape &sh);
 hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const void *ws, const void *packed,
                                 float *out, hipStream_t st);
+// Operand type of the 16-bit matrix-core kernels (every one of them is
+// instantiated for both).
+enum class Op16 { F16, BF16 };
 hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed, hipStream_t st);
 hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed, uint16_t *out,
-                            hipStream_t st);
+                            hipStream_t st, Op16 op);
 // Column-staged fp16 kernel: the variant for this layer, or -1 when the
 // row-per-pixel kernels run instead.  The filter pack layout follows it.
 int col_plan(const Shape &sh);
@@ -139,7 +142,7 @@ int col_stage_taps(int plan);  // taps per stage of that variant (packed-filter 
 // variant for this layer, or -1 when the register-staged kernel runs.
 int seg_plan(const Shape &sh);
 hipError_t launch_conv_fp16_seg(const Shape &sh, int plan, const void *ws, const void *packed,
-                                uint16_t *out, hipStream_t st);
+                                uint16_t *out, hipStream_t st, Op16 op);
 hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const void *packed,
-                                uint16_t *out, hipStream_t st);
+                                uint16_t *out, hipStream_t st, Op16 op);
 } // namespace im2win

@@ -26,7 +26,6 @@
 namespace im2win {
 namespace {
 
-typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int BK = 64;       // taps per stage
@@ -40,7 +39,7 @@ constexpr int LDK = BK + 8;  // halves per LDS row: 144 bytes, offsets rows acro
 constexpr int kLoadUnaligned = 1, kLoadElems = 2;
 
 struct C16Args {
-    const uint16_t *ws;      // window tensor (fp16 bits)
+    const uint16_t *ws;      // window tensor (16-bit elements)
     const uint16_t *packed;  // F' [Co_pad][K_pad]
     uint16_t *out;
     uint64_t win_bytes;
@@ -113,7 +112,7 @@ __global__ __launch_bounds__(256) void pack_filter_fp16(PackArgs a)
 // pbase + 32*j + (lane & 31) and, for accumulator element e of block (i, j),
 // channel chbase + 32*i + 8*(e/4) + 4*(lane/32) + e%4.  Each sum is rounded to
 // fp16 once (nearest-even) and four consecutive channels go out as 8 bytes.
-template <int WM, int WN>
+template <class E, int WM, int WN>
 __device__ inline void store_tile(const floatx16 (&acc)[WM][WN], const C16Args &a, uint32_t pbase,
                                   uint32_t chbase, uint32_t lane)
 {
@@ -130,10 +129,8 @@ __device__ inline void store_tile(const floatx16 (&acc)[WM][WN], const C16Args &
                 const uint32_t c = chbase + 32 * i + 8 * g + 4 * (lane >> 5);
                 uint32_t h[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const _Float16 v = (_Float16)acc[i][j][4 * g + e];
-                    h[e] = __builtin_bit_cast(uint16_t, v);
-                }
+                for (int e = 0; e < 4; ++e)
+                    h[e] = E::bits(acc[i][j][4 * g + e]);
                 if (c + 3 < a.Co && (a.Co & 3) == 0) {
                     *reinterpret_cast<uint2 *>(o + c) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
                 } else {
@@ -212,7 +209,7 @@ struct Stage16 {
         }
     }
 
-    __device__ inline void store(_Float16 (*Fs)[LDK], _Float16 (*Ws)[LDK])
+    __device__ inline void store(uint16_t (*Fs)[LDK], uint16_t (*Ws)[LDK])
     {
         const uint32_t tid = threadIdx.x;
 #pragma unroll
@@ -228,12 +225,14 @@ struct Stage16 {
     }
 };
 
-template <int WM, int WN, int WGM, int WGN, int LM>
+template <class E, int WM, int WN, int WGM, int WGN, int LM>
 __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
 {
+    typedef typename E::v8 v8;
     using C = Cfg<WM, WN, WGM, WGN, LM>;
-    __shared__ __attribute__((aligned(16))) _Float16 Fs[2][C::BMc][LDK];
-    __shared__ __attribute__((aligned(16))) _Float16 Ws[2][C::BNp][LDK];
+    // raw 16-bit operand bits
+    __shared__ __attribute__((aligned(16))) uint16_t Fs[2][C::BMc][LDK];
+    __shared__ __attribute__((aligned(16))) uint16_t Ws[2][C::BNp][LDK];
     __shared__ uint32_t rowoff[C::BNp];
 
     const uint32_t tid = threadIdx.x;
@@ -285,18 +284,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
             stg.load(rs, wsb, rowoff, fb, p0, (st + 1) * BK, a);
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
-            half8 af[WM], bf[WN];
+            v8 af[WM], bf[WN];
 #pragma unroll
             for (int i = 0; i < WM; ++i)
-                af[i] = *reinterpret_cast<const half8 *>(&Fs[buf][arow + 32 * i][16 * ks + kl]);
+                af[i] = *reinterpret_cast<const v8 *>(&Fs[buf][arow + 32 * i][16 * ks + kl]);
 #pragma unroll
             for (int j = 0; j < WN; ++j)
-                bf[j] = *reinterpret_cast<const half8 *>(&Ws[buf][brow + 32 * j][16 * ks + kl]);
+                bf[j] = *reinterpret_cast<const v8 *>(&Ws[buf][brow + 32 * j][16 * ks + kl]);
 #pragma unroll
             for (int i = 0; i < WM; ++i)
 #pragma unroll
                 for (int j = 0; j < WN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = E::mfma(af[i], bf[j], acc[i][j]);
         }
         if (st + 1 < nst)
             stg.store(Fs[buf ^ 1], Ws[buf ^ 1]);
@@ -304,11 +303,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
     }
 
     if constexpr (epilogue16_bytes<C::BMc, C::BNp>() <= (int)sizeof(Ws)) {
-        store_tile_lds<WM, WN, WGM, WGN>(acc, reinterpret_cast<char *>(&Ws[0][0][0]), a.out, a.P, a.Co, p0, ch0,
+        store_tile_lds<E, WM, WN, WGM, WGN>(acc, reinterpret_cast<char *>(&Ws[0][0][0]), a.out, a.P, a.Co, p0, ch0,
                                          wm, wn, lane, tid);
         return;
     }
-    store_tile<WM, WN>(acc, a, p0 + wn * 32 * WN, ch0 + wm * 32 * WM, lane);
+    store_tile<E, WM, WN>(acc, a, p0 + wn * 32 * WN, ch0 + wm * 32 * WM, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -372,9 +371,10 @@ __device__ inline uint32_t rsw(uint32_t r) { return (r ^ (r >> 3)) & 7u; }
 // LDS arrays and every step of the main loop names its slot at compile time,
 // so the compiler can tell that reading one slot does not depend on the
 // loads still landing in the others (and inserts no wait for them).
-template <int WM, int WN, int WGM, int WGN, int NSTAGE>
+template <class E, int WM, int WN, int WGM, int WGN, int NSTAGE>
 struct Pipe {
     using C = PipeCfg<WM, WN, WGM, WGN, NSTAGE>;
+    typedef typename E::v8 v8;
     __amdgpu_buffer_rsrc_t rf, rw;
     uint32_t voff[C::I];    // byte offset of this lane's chunk at tap 0 (kOOB: no pixel)
     uint32_t vchunk[C::I];  // first tap of this lane's chunk within a stage
@@ -408,22 +408,22 @@ struct Pipe {
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
             const uint32_t ch = 2 * ks + (lane >> 5);
-            half8 af[WM], bf[WN];
+            v8 af[WM], bf[WN];
 #pragma unroll
             for (int i = 0; i < WM; ++i) {
                 const uint32_t r = arow + 32 * i;
-                af[i] = *reinterpret_cast<const half8 *>(stage + r * 128 + 16u * (ch ^ rsw(r)));
+                af[i] = *reinterpret_cast<const v8 *>(stage + r * 128 + 16u * (ch ^ rsw(r)));
             }
 #pragma unroll
             for (int j = 0; j < WN; ++j) {
                 const uint32_t r = brow + 32 * j;
-                bf[j] = *reinterpret_cast<const half8 *>(stage + r * 128 + 16u * (ch ^ rsw(r)));
+                bf[j] = *reinterpret_cast<const v8 *>(stage + r * 128 + 16u * (ch ^ rsw(r)));
             }
 #pragma unroll
             for (int i = 0; i < WM; ++i)
 #pragma unroll
                 for (int j = 0; j < WN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = E::mfma(af[i], bf[j], acc[i][j]);
         }
     }
 
@@ -444,7 +444,7 @@ struct Pipe {
     }
 };
 
-template <int WM, int WN, int WGM, int WGN, int NSTAGE>
+template <class E, int WM, int WN, int WGM, int WGN, int NSTAGE>
 __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
 {
     using C = PipeCfg<WM, WN, WGM, WGN, NSTAGE>;
@@ -456,7 +456,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
     __shared__ __attribute__((aligned(1024))) char r3[S3];
     __shared__ uint32_t rowoff[C::BNp];
 
-    Pipe<WM, WN, WGM, WGN, NSTAGE> w;
+    Pipe<E, WM, WN, WGM, WGN, NSTAGE> w;
     const uint32_t tid = threadIdx.x;
     w.lane = tid & 63;
     w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -542,32 +542,34 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
     wait_vmcnt<0>();
 
     if constexpr (epilogue16_bytes<C::BMc, C::BNp>() <= C::STAGE) {
-        store_tile_lds<WM, WN, WGM, WGN>(w.acc, r0, a.out, a.P, a.Co, p0, ch0, wm, wn, w.lane, tid);
+        store_tile_lds<E, WM, WN, WGM, WGN>(w.acc, r0, a.out, a.P, a.Co, p0, ch0, wm, wn, w.lane, tid);
         return;
     }
-    store_tile<WM, WN>(w.acc, a, p0 + wn * 32 * WN, ch0 + wm * 32 * WM, w.lane);
+    store_tile<E, WM, WN>(w.acc, a, p0 + wn * 32 * WN, ch0 + wm * 32 * WM, w.lane);
 }
 
-template <int WM, int WN, int WGM, int WGN>
+template <class E, int WM, int WN, int WGM, int WGN>
 void pick_regs(bool unaligned_loads, const void **f, int *bm, int *bn)
 {
-    *f = unaligned_loads ? (const void *)&conv_fp16_kernel<WM, WN, WGM, WGN, kLoadUnaligned>
-                         : (const void *)&conv_fp16_kernel<WM, WN, WGM, WGN, kLoadElems>;
+    *f = unaligned_loads ? (const void *)&conv_fp16_kernel<E, WM, WN, WGM, WGN, kLoadUnaligned>
+                         : (const void *)&conv_fp16_kernel<E, WM, WN, WGM, WGN, kLoadElems>;
     *bm = 32 * WM * WGM;
     *bn = 32 * WN * WGN;
 }
 
 struct PipeVariant {
     const char *name;
-    const void *f;
+    const void *f[2];  // fp16 and bf16 operands
     int bm, bn, nt;
 };
 
 template <int WM, int WN, int WGM, int WGN, int NS>
 PipeVariant pipe_variant(const char *name)
 {
-    return PipeVariant{name, (const void *)&conv_fp16_pipe<WM, WN, WGM, WGN, NS>, 32 * WM * WGM,
-                       32 * WN * WGN, 64 * WGM * WGN};
+    return PipeVariant{name,
+                       {(const void *)&conv_fp16_pipe<F16Op, WM, WN, WGM, WGN, NS>,
+                        (const void *)&conv_fp16_pipe<BF16Op, WM, WN, WGM, WGN, NS>},
+                       32 * WM * WGM, 32 * WN * WGN, 64 * WGM * WGN};
 }
 
 // Tile shapes of the pipelined kernel: channels x pixels per workgroup,
@@ -615,11 +617,11 @@ hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed,
 }
 
 hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed, uint16_t *out,
-                            hipStream_t st)
+                            hipStream_t st, Op16 op)
 {
     const int plan = col_plan(sh);
     if (plan >= 0)
-        return launch_conv_fp16_col(sh, plan, ws, packed, out, st);
+        return launch_conv_fp16_col(sh, plan, ws, packed, out, st, op);
     C16Args a;
     a.ws = static_cast<const uint16_t *>(ws);
     a.packed = static_cast<const uint16_t *>(packed);
@@ -665,20 +667,29 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
         }
         const PipeVariant &p = v[pick];
         dim3 grid((uint32_t)((sh.P + p.bn - 1) / p.bn), (uint32_t)((sh.Co + p.bm - 1) / p.bm));
-        return hipLaunchKernel(p.f, grid, dim3(p.nt), args, 0, st);
+        return hipLaunchKernel(p.f[op == Op16::BF16], grid, dim3(p.nt), args, 0, st);
     }
     const int sp = seg_plan(sh);
     if (sp >= 0)
-        return launch_conv_fp16_seg(sh, sp, ws, packed, out, st);
+        return launch_conv_fp16_seg(sh, sp, ws, packed, out, st, op);
     const void *f;
     int bm, bn;
     const bool unal = sh.K >= 128;
-    if (sh.Co <= 32)
-        pick_regs<1, 2, 1, 4>(unal, &f, &bm, &bn);
-    else if (sh.Co <= 64)
-        pick_regs<2, 2, 1, 4>(unal, &f, &bm, &bn);
-    else
-        pick_regs<2, 2, 2, 2>(unal, &f, &bm, &bn);
+    if (op == Op16::BF16) {
+        if (sh.Co <= 32)
+            pick_regs<BF16Op, 1, 2, 1, 4>(unal, &f, &bm, &bn);
+        else if (sh.Co <= 64)
+            pick_regs<BF16Op, 2, 2, 1, 4>(unal, &f, &bm, &bn);
+        else
+            pick_regs<BF16Op, 2, 2, 2, 2>(unal, &f, &bm, &bn);
+    } else {
+        if (sh.Co <= 32)
+            pick_regs<F16Op, 1, 2, 1, 4>(unal, &f, &bm, &bn);
+        else if (sh.Co <= 64)
+            pick_regs<F16Op, 2, 2, 1, 4>(unal, &f, &bm, &bn);
+        else
+            pick_regs<F16Op, 2, 2, 2, 2>(unal, &f, &bm, &bn);
+    }
     dim3 grid((uint32_t)((sh.P + bn - 1) / bn), (uint32_t)((sh.Co + bm - 1) / bm));
     return hipLaunchKernel(f, grid, dim3(256), args, 0, st);
 }

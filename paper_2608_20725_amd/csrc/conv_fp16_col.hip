@@ -43,12 +43,11 @@
 namespace im2win {
 namespace {
 
-typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void *lds_ptr;
 
 struct ColArgs {
-    const uint16_t *ws;      // window tensor (fp16 bits)
+    const uint16_t *ws;      // window tensor (16-bit elements)
     const uint16_t *packed;  // G in BT-tap tiles: [Tp/BT][KW][Co_pad][BT]
     uint16_t *out;
     uint64_t win_bytes;
@@ -108,8 +107,10 @@ __device__ inline void ring_barrier()
     asm volatile("" ::: "memory");
 }
 
-template <class C>
+// E: the operand type (F16Op or BF16Op).
+template <class C, class E>
 struct ColTile {
+    typedef typename E::v8 v8;
     __amdgpu_buffer_rsrc_t rf, rw;
     uint32_t boff[C::IB];  // byte offset of this lane's chunk at t = 0 (kOOB: none)
     uint32_t bcm[C::IB];   // B rows: first t of the chunk (t-tail mask); A rows: 0
@@ -133,7 +134,7 @@ struct ColTile {
     }
 
     // Fragments of k-step ks (filter column v = ks / (BT/16)).
-    __device__ inline void frags(const char *slot, int ks, half8 (&af)[C::WM], half8 (&bf)[C::WN])
+    __device__ inline void frags(const char *slot, int ks, v8 (&af)[C::WM], v8 (&bf)[C::WN])
     {
         const int v = ks / (C::BT / 16), kk = ks % (C::BT / 16);
         const uint32_t chunk = 2 * kk + (lane >> 5);
@@ -141,12 +142,12 @@ struct ColTile {
 #pragma unroll
         for (int i = 0; i < C::WM; ++i) {
             const uint32_t row = v * C::BM + arow0 + 32 * i;
-            af[i] = *reinterpret_cast<const half8 *>(slot + row * C::RB + 16 * (chunk ^ sw<C>(row)));
+            af[i] = *reinterpret_cast<const v8 *>(slot + row * C::RB + 16 * (chunk ^ sw<C>(row)));
         }
 #pragma unroll
         for (int j = 0; j < C::WN; ++j) {
             const uint32_t row = C::AROWS + Rj[j] + v;
-            bf[j] = *reinterpret_cast<const half8 *>(slot + row * C::RB + 16 * (chunk ^ sw<C>(row)));
+            bf[j] = *reinterpret_cast<const v8 *>(slot + row * C::RB + 16 * (chunk ^ sw<C>(row)));
         }
     }
 
@@ -155,7 +156,7 @@ struct ColTile {
     __device__ inline void compute(const char *slot)
     {
         constexpr int KS = C::KW * C::BT / 16;
-        half8 af[2][C::WM], bf[2][C::WN];
+        v8 af[2][C::WM], bf[2][C::WN];
         frags(slot, 0, af[0], bf[0]);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
@@ -165,8 +166,7 @@ struct ColTile {
             for (int i = 0; i < C::WM; ++i)
 #pragma unroll
                 for (int j = 0; j < C::WN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[ks & 1][i], bf[ks & 1][j],
-                                                                       acc[i][j], 0, 0, 0);
+                    acc[i][j] = E::mfma(af[ks & 1][i], bf[ks & 1][j], acc[i][j]);
         }
     }
 
@@ -185,7 +185,7 @@ struct ColTile {
     }
 };
 
-template <class C>
+template <class C, class E>
 __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
 {
     constexpr int S2 = C::NS > 2 ? C::STAGE : 1024, S3 = C::NS > 3 ? C::STAGE : 1024;
@@ -195,7 +195,7 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
     __shared__ __attribute__((aligned(1024))) char r3[S3];
     __shared__ uint32_t tbl[C::NRMAX];
 
-    ColTile<C> w;
+    ColTile<C, E> w;
     const uint32_t tid = threadIdx.x;
     w.lane = tid & 63;
     w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -305,7 +305,7 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
     // Epilogue: through LDS (whole output lines per wave) when the tile fits
     // a ring slot, else directly from the accumulators.
     if constexpr (epilogue16_bytes<C::BM, C::BN>() <= C::STAGE) {
-        store_tile_lds<C::WM, C::WN, C::WGM, C::WGN>(w.acc, r0, a.out, a.P, a.Co, p0, ch0, w.wm, w.wn, w.lane,
+        store_tile_lds<E, C::WM, C::WN, C::WGM, C::WGN>(w.acc, r0, a.out, a.P, a.Co, p0, ch0, w.wm, w.wn, w.lane,
                                                      tid);
         return;
     }
@@ -325,10 +325,8 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
                 const uint32_t c = cb + 32 * i + 8 * g + 4 * (w.lane >> 5);
                 uint32_t h[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const _Float16 v = (_Float16)w.acc[i][j][4 * g + e];
-                    h[e] = __builtin_bit_cast(uint16_t, v);
-                }
+                for (int e = 0; e < 4; ++e)
+                    h[e] = E::bits(w.acc[i][j][4 * g + e]);
                 if (c + 3 < a.Co && (a.Co & 3) == 0) {
                     *reinterpret_cast<uint2 *>(o + c) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
                 } else {
@@ -344,7 +342,7 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
 
 struct ColVariant {
     const char *name;
-    const void *f;
+    const void *f[2];  // fp16 and bf16 operands
     int kw, bm, bn, nrmax, bt, nt;
 };
 
@@ -352,7 +350,8 @@ template <int KW, int BT, int WM, int WN, int WGM, int WGN, int NRMAX, int NS>
 ColVariant col_variant(const char *name)
 {
     using C = ColCfg<KW, BT, WM, WN, WGM, WGN, NRMAX, NS>;
-    return ColVariant{name, (const void *)&conv_fp16_col<C>, KW, C::BM, C::BN, NRMAX, BT, C::NT};
+    return ColVariant{name, {(const void *)&conv_fp16_col<C, F16Op>, (const void *)&conv_fp16_col<C, BF16Op>}, KW,
+                      C::BM, C::BN, NRMAX, BT, C::NT};
 }
 
 const ColVariant *col_variants(int *n)
@@ -448,7 +447,7 @@ int col_stage_taps(int plan)
 }
 
 hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const void *packed,
-                                uint16_t *out, hipStream_t st)
+                                uint16_t *out, hipStream_t st, Op16 op)
 {
     int n;
     const ColVariant &v = col_variants(&n)[plan];
@@ -466,7 +465,7 @@ hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     void *args[] = {&a};
     dim3 grid((uint32_t)((sh.P + v.bn - 1) / v.bn), (uint32_t)((sh.Co + v.bm - 1) / v.bm));
-    return hipLaunchKernel(v.f, grid, dim3(v.nt), args, 0, st);
+    return hipLaunchKernel(v.f[op == Op16::BF16], grid, dim3(v.nt), args, 0, st);
 }
 
 }  // namespace im2win

@@ -25,7 +25,6 @@
 namespace im2win {
 namespace {
 
-typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void *lds_ptr;
 
@@ -72,8 +71,10 @@ __device__ inline void ring_barrier()
     asm volatile("" ::: "memory");
 }
 
-template <class C>
+// E: the operand type (F16Op or BF16Op).
+template <class C, class E>
 struct SegTile {
+    typedef typename E::v8 v8;
     __amdgpu_buffer_rsrc_t rf;
     uint32_t aoff[C::IA];  // filter byte offset at stage 0
     uint32_t bb[C::WN];    // LDS byte offset of each of this lane's pixels' window
@@ -97,11 +98,11 @@ struct SegTile {
         for (int ks = 0; ks < BK / 16; ++ks) {
             const uint32_t ch = 2 * ks + (lane >> 5);
             const uint32_t k = st * BK + 8 * ch;  // first of this lane's 8 taps
-            half8 af[C::WM], bf[C::WN];
+            v8 af[C::WM], bf[C::WN];
 #pragma unroll
             for (int i = 0; i < C::WM; ++i) {
                 const uint32_t r = wm * 32 * C::WM + 32 * i + (lane & 31);
-                af[i] = *reinterpret_cast<const half8 *>(aslot + r * 128 + 16u * (ch ^ rsw(r)));
+                af[i] = *reinterpret_cast<const v8 *>(aslot + r * 128 + 16u * (ch ^ rsw(r)));
             }
 #pragma unroll
             for (int j = 0; j < C::WN; ++j) {
@@ -111,26 +112,26 @@ struct SegTile {
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
                         if (k + e >= K)
-                            bf[j][e] = (_Float16)0.f;
+                            bf[j][e] = (typename E::elem)0.f;
                 }
             }
 #pragma unroll
             for (int i = 0; i < C::WM; ++i)
 #pragma unroll
                 for (int j = 0; j < C::WN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = E::mfma(af[i], bf[j], acc[i][j]);
         }
     }
 };
 
-template <class C>
+template <class C, class E>
 __global__ __launch_bounds__(C::NT) void conv_fp16_seg(SegArgs a)
 {
     __shared__ __attribute__((aligned(1024))) char r0[C::ASTAGE];
     __shared__ __attribute__((aligned(1024))) char r1[C::ASTAGE];
     __shared__ __attribute__((aligned(1024))) char seg[C::GMAX * 16];
 
-    SegTile<C> w;
+    SegTile<C, E> w;
     const uint32_t tid = threadIdx.x;
     w.lane = tid & 63;
     w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -248,13 +249,13 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_seg(SegArgs a)
     }
     wait_vmcnt<0>();
 
-    store_tile_lds<C::WM, C::WN, C::WGM, C::WGN>(w.acc, seg, a.out, a.P, a.Co, p0, ch0, w.wm, w.wn, w.lane,
+    store_tile_lds<E, C::WM, C::WN, C::WGM, C::WGN>(w.acc, seg, a.out, a.P, a.Co, p0, ch0, w.wm, w.wn, w.lane,
                                                  tid);
 }
 
 struct SegVariant {
     const char *name;
-    const void *f;
+    const void *f[2];  // fp16 and bf16 operands
     int bm, bn, gmax, rmax, nt;
 };
 
@@ -262,7 +263,8 @@ template <int WM, int WN, int WGM, int WGN, int GMAX, int RMAX>
 SegVariant seg_variant(const char *name)
 {
     using C = SegCfg<WM, WN, WGM, WGN, GMAX, RMAX>;
-    return SegVariant{name, (const void *)&conv_fp16_seg<C>, C::BM, C::BN, GMAX, RMAX, C::NT};
+    return SegVariant{name, {(const void *)&conv_fp16_seg<C, F16Op>, (const void *)&conv_fp16_seg<C, BF16Op>}, C::BM,
+                      C::BN, GMAX, RMAX, C::NT};
 }
 
 const SegVariant *seg_variants(int *n)
@@ -324,7 +326,7 @@ int seg_plan(const Shape &sh)
 }
 
 hipError_t launch_conv_fp16_seg(const Shape &sh, int plan, const void *ws, const void *packed,
-                                uint16_t *out, hipStream_t st)
+                                uint16_t *out, hipStream_t st, Op16 op)
 {
     int n;
     const SegVariant &v = seg_variants(&n)[plan];
@@ -340,7 +342,7 @@ hipError_t launch_conv_fp16_seg(const Shape &sh, int plan, const void *ws, const
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     void *args[] = {&a};
     dim3 grid((uint32_t)((sh.P + v.bn - 1) / v.bn), (uint32_t)((sh.Co + v.bm - 1) / v.bm));
-    return hipLaunchKernel(v.f, grid, dim3(v.nt), args, 0, st);
+    return hipLaunchKernel(v.f[op == Op16::BF16], grid, dim3(v.nt), args, 0, st);
 }
 
 }  // namespace im2win

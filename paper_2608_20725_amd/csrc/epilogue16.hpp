@@ -1,10 +1,10 @@
-// Output epilogue of the fp16 matrix-core kernels.
+// Output epilogue of the 16-bit (fp16 / bf16) matrix-core kernels.
 //
 // A wave's v_mfma_f32_32x32x16_f16 sums are spread so that lane l holds pixel
 // (l & 31) and, for accumulator element e, channel 8*(e/4) + 4*(l/32) + e%4 of
 // each 32x32 block: stored directly, one wave instruction writes 8-byte pieces
 // of 32 different pixels' rows, and the memory pipeline pays per cache line
-// touched.  Here every sum is rounded to fp16 once (nearest-even), the
+// touched.  Here every sum is rounded to the output type once (nearest-even), the
 // workgroup's tile is assembled in LDS as [pixel][channel], and the tile is
 // then copied to the NHWC output in 16-byte pieces, a wave covering whole
 // consecutive pixel rows (whole 128-byte lines when the tile spans 64 or more
@@ -12,10 +12,9 @@
 #pragma once
 
 #include "common.hpp"
+#include "mfma16.hpp"
 
 namespace im2win {
-
-typedef float f32x16_acc __attribute__((ext_vector_type(16)));
 
 // Bytes of LDS the staged epilogue needs for a BM x BN tile.
 template <int BM, int BN>
@@ -28,7 +27,8 @@ constexpr int epilogue16_bytes()
 // wch = wm*32*WM and pixel wpx = wn*32*WN of the workgroup tile (p0, ch0).
 // `lds` must hold epilogue16_bytes<BM, BN>() bytes that no wave still reads or
 // loads into; the function synchronises the workgroup itself.
-template <int WM, int WN, int WGM, int WGN>
+// E (F16Op or BF16Op) rounds the sums to the output type.
+template <class E, int WM, int WN, int WGM, int WGN>
 __device__ inline void store_tile_lds(const f32x16_acc (&acc)[WM][WN], char *lds, uint16_t *out, uint32_t P,
                                       uint32_t Co, uint32_t p0, uint32_t ch0, uint32_t wm, uint32_t wn,
                                       uint32_t lane, uint32_t tid)
@@ -54,10 +54,8 @@ __device__ inline void store_tile_lds(const f32x16_acc (&acc)[WM][WN], char *lds
                 const uint32_t ch = wm * 32 * WM + 32 * i + 8 * g + 4 * (lane >> 5);
                 uint32_t h[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const _Float16 v = (_Float16)acc[i][j][4 * g + e];
-                    h[e] = __builtin_bit_cast(uint16_t, v);
-                }
+                for (int e = 0; e < 4; ++e)
+                    h[e] = E::bits(acc[i][j][4 * g + e]);
                 const uint32_t k = ch / 8;
                 *reinterpret_cast<uint2 *>(lds + px * RB + 16 * (k ^ sw(px)) + 2 * (ch % 8)) =
                     make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));

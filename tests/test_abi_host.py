@@ -68,8 +68,8 @@ def _closed_form(l, elt, fp16):
 
 @pytest.mark.parametrize("layer", workloads.ALL, ids=lambda l: l.name)
 def test_workspace_and_im2col_bytes(lib, layer, orc):
-    for dt, elt in ((pkg.F32, 4), (pkg.F16, 2)):
-        ws, im2col, win = _closed_form(layer, elt, dt == pkg.F16)
+    for dt, elt in ((pkg.F32, 4), (pkg.F16, 2), (pkg.BF16, 2)):
+        ws, im2col, win = _closed_form(layer, elt, dt != pkg.F32)
         args = (layer.N, layer.C_i, layer.H, layer.W, layer.C_o, layer.K_h, layer.K_w, layer.stride)
         assert pkg.conv_workspace_bytes(*args, dt) == ws
         assert pkg.conv_im2col_bytes(layer.N, layer.C_i, layer.H, layer.W, layer.K_h, layer.K_w,
@@ -104,6 +104,8 @@ def test_workspace_rejects_bad_dims(lib, args):
 
 def test_workspace_rejects_bad_dtype(lib):
     assert lib.conv_workspace_bytes(1, 3, 8, 8, 4, 3, 3, 1, 7) == EINVAL
+    assert lib.conv_workspace_bytes(1, 3, 8, 8, 4, 3, 3, 1, 3) == EINVAL
+    assert lib.conv_workspace_bytes(1, 3, 8, 8, 4, 3, 3, 1, -1) == EINVAL
 
 
 def test_ranges(lib):
@@ -117,6 +119,7 @@ def test_ranges(lib):
     assert lib.conv_workspace_bytes(1 << 20, 1, 64, 64, 1, 1, 1, 1, pkg.F32) == ERANGE
     # fp16 packed filter of 2^31 bytes or more (fp32 has no such limit)
     assert lib.conv_workspace_bytes(1, 1 << 12, 1, 64, 1 << 16, 1, 64, 1, pkg.F16) == ERANGE
+    assert lib.conv_workspace_bytes(1, 1 << 12, 1, 64, 1 << 16, 1, 64, 1, pkg.BF16) == ERANGE
     assert lib.conv_workspace_bytes(1, 1 << 12, 1, 64, 1 << 16, 1, 64, 1, pkg.F32) > 0
 
 
@@ -133,6 +136,8 @@ def test_null_pointers_rejected_first(lib):
     assert lib.conv_im2win_transform(None, v(256), 1 << 20, 0, 3, 8, 8, 4, 3, 3, 1, 0, None) == EINVAL
     assert lib.conv_im2win_fp32(v(256), 1 << 20, None, v(512), 1, 3, 8, 8, 4, 3, 3, 1, None) == EINVAL
     assert lib.conv_im2win_fp16(v(256), 1 << 20, v(512), None, 1, 3, 8, 8, 4, 3, 3, 1, None) == EINVAL
+    assert lib.conv_im2win_bf16(None, 1 << 20, v(512), v(768), 1, 3, 8, 8, 4, 3, 3, 1, None) == EINVAL
+    assert lib.conv_im2win_bf16(v(256), 1 << 20, v(512), v(768), 0, 3, 8, 8, 4, 3, 3, 1, None) == EINVAL
 
 
 def test_misaligned_pointers_rejected(lib):
@@ -142,6 +147,8 @@ def test_misaligned_pointers_rejected(lib):
     assert lib.conv_im2win_fp32(v(0x100000), 1 << 20, v(0x2004), v(0x3000), 1, 3, 8, 8, 4, 3, 3, 1,
                                 None) == EALIGN
     assert lib.conv_im2win_fp16(v(0x100000), 1 << 20, v(0x2000), v(0x3002), 1, 3, 8, 8, 4, 3, 3, 1,
+                                None) == EALIGN
+    assert lib.conv_im2win_bf16(v(0x100008), 1 << 20, v(0x2000), v(0x3000), 1, 3, 8, 8, 4, 3, 3, 1,
                                 None) == EALIGN
 
 

@@ -12,7 +12,7 @@ from paper_2608_20725_amd import workloads
 
 pytestmark = pytest.mark.gpu
 
-DTYPES = [torch.float32, torch.float16]
+DTYPES = [torch.float32, torch.float16, torch.bfloat16]
 SHAPES = [
     (5, 16, 12, 12, 24, 3, 3, 1),     # row-per-pixel fp16 kernel
     (4, 64, 24, 24, 64, 3, 3, 1),     # column-staged fp16 kernel
@@ -38,7 +38,7 @@ def _run_chunked(x, w, s, dtype, n_chunk, two, aux=None):
     return out
 
 
-@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "f16"])
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "f16", "bf16"])
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda t: "x".join(map(str, t)))
 def test_chunked_equals_full_batch(shape, dtype):
     N, Ci, H, W, Co, Kh, Kw, s = shape
@@ -51,8 +51,8 @@ def test_chunked_equals_full_batch(shape, dtype):
         say("chunked", shape, dtype, n_chunk, two)
         out = _run_chunked(x, w, s, dtype, n_chunk, two, aux if two else None)
         got = out.cpu()
-        assert torch.equal(got.view(torch.int16 if dtype == torch.float16 else torch.int32),
-                           ref.view(torch.int16 if dtype == torch.float16 else torch.int32)), (n_chunk, two)
+        bits = torch.int32 if dtype == torch.float32 else torch.int16
+        assert torch.equal(got.view(bits), ref.view(bits)), (n_chunk, two)
 
 
 def test_chunked_back_to_back_reuses_workspace():

@@ -11,7 +11,7 @@ from paper_2608_20725_amd import workloads
 
 pytestmark = pytest.mark.gpu
 
-DTYPES = [torch.float32, torch.float16]
+DTYPES = [torch.float32, torch.float16, torch.bfloat16]
 
 # (N, C_i, H, W, K_h, K_w, s): vector path (C_i*elt multiple of 16 bytes),
 # gather path (any other C_i), strips that are not a whole number of 16-byte
@@ -24,8 +24,14 @@ SHAPES += [
 ]
 
 
+def _bits(t):
+    """Host array of a tensor's element bits (numpy has no bfloat16; the
+    transform only moves bits)."""
+    return t.view(torch.int16).numpy() if t.dtype == torch.bfloat16 else t.numpy()
+
+
 def _compare(run, x):
-    xs = x.to(run.dtype).numpy()
+    xs = _bits(x.to(run.dtype))
     ref = oracle.im2win(xs, run.Kh, run.s)
     nb = run.window_bytes()
     got = run.ws[:nb].cpu().numpy()
@@ -37,7 +43,7 @@ def _compare(run, x):
     run.check_workspace_guard()
 
 
-@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "f16"])
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "f16", "bf16"])
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
 def test_transform_small(shape, dtype):
     N, Ci, H, W, Kh, Kw, s = shape
@@ -47,7 +53,7 @@ def test_transform_small(shape, dtype):
     _compare(run, x)
 
 
-@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "f16"])
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "f16", "bf16"])
 @pytest.mark.parametrize("layer", workloads.CONFIGS, ids=lambda l: l.name)
 def test_transform_configs_full(layer, dtype):
     """The four named configurations at full size, whole tensor compared."""
@@ -57,7 +63,7 @@ def test_transform_configs_full(layer, dtype):
     _compare(run, x)
 
 
-@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "f16"])
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "f16", "bf16"])
 @pytest.mark.parametrize("layer", workloads.SWEEP, ids=lambda l: l.name)
 def test_transform_sweep_sampled_strips(layer, dtype):
     """The sweep layers at full batch: the strips of images 0, N-1 and two
@@ -69,7 +75,7 @@ def test_transform_sweep_sampled_strips(layer, dtype):
     imgs = sorted({0, layer.N - 1, *rng.integers(1, layer.N - 1, 2).tolist()})
     per_img = run.Ho * run.W * run.Kh * run.Ci * run.xd.element_size()
     for i in imgs:
-        ref = oracle.im2win(x[i:i + 1].to(dtype).numpy(), run.Kh, run.s)
+        ref = oracle.im2win(_bits(x[i:i + 1].to(dtype)), run.Kh, run.s)
         got = run.ws[i * per_img:(i + 1) * per_img].cpu().numpy()
         assert got.tobytes() == ref.tobytes(), "image %d" % i
     nb = run.window_bytes()
