@@ -12,7 +12,9 @@ Per-kernel durations come from HIP events recorded on the stream the kernels
 are launched on, around every call in the timed region.
 
 Prints ONE JSON line.  `--layer NAME` picks another configured layer and
-`--sweep` prints one line per configured layer instead (for reports).  Each
+`--sweep` prints one line per configured layer instead (for reports);
+`--ablation LAYERS` times the path with each of the paper's techniques
+switched off (Sec. IV-D) on the named layers.  Each
 line also carries a `bf16` block: the same layer with bf16 operands on the
 same matrix-core kernels, timed outside the step (an extension of the path).
 """
@@ -167,6 +169,82 @@ def measure_bf16(l, x, w, pkg, torch, reps=20):
             "frac_bf16_mfma": round(flops / (ms_c * 1e-3) / 1e12 / PEAK_FP16_MFMA_TF, 4)}
 
 
+# The paper's ablation (Sec. IV-D, Table II) on its three tensor-core
+# techniques, mapped to their gfx950 counterparts; each entry switches one off
+# through the library's tuning variables (read at every launch).
+ABLATION = {
+    "f16": [
+        ("as built", {}),
+        ("no column reuse: row-per-pixel kernel", {"IM2WIN_FP16_KERNEL": "pipe"}),
+        ("row kernel 128x128, 2-slot ring", {"IM2WIN_FP16_KERNEL": "pipe", "IM2WIN_FP16_TILE": "c128p128s2"}),
+        ("row kernel 128x128, 1 slot (no double buffering)",
+         {"IM2WIN_FP16_KERNEL": "pipe", "IM2WIN_FP16_TILE": "c128p128s1"}),
+        ("register-staged loads (no direct-to-LDS copy)", {"IM2WIN_FP16_KERNEL": "regs"}),
+    ],
+    "f32": [
+        ("as built", {}),
+        ("register-staged loads (no direct-to-LDS copy)", {"IM2WIN_FP32_KERNEL": "regs"}),
+    ],
+    "transform": [
+        ("as built (XCD-aware block order)", {}),
+        ("linear block order", {"IM2WIN_TRANSFORM_ORDER": "linear"}),
+    ],
+}
+ABLATION_VARS = ("IM2WIN_FP16_KERNEL", "IM2WIN_FP16_TILE", "IM2WIN_FP32_KERNEL", "IM2WIN_TRANSFORM_ORDER")
+
+
+def run_ablation(l, pkg, torch, workloads, reps=15):
+    """Median time of each call of the path with one technique switched off,
+    on layer `l`; each call repeated back to back (warm caches)."""
+    x, w = workloads.draw_layer(l)
+    paths = {"f32": Path(l, x, w, torch.float32, pkg, torch),
+             "f16": Path(l, x, w, torch.float16, pkg, torch)}
+    nums = layer_numbers(l, pkg)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        ts.sort()
+        return ts[reps // 2]
+
+    res = {"layer": l.name, "f16": {}, "f32": {}, "transform": {}}
+    saved = {k: os.environ.get(k) for k in ABLATION_VARS}
+    try:
+        for part, rows in ABLATION.items():
+            for label, env in rows:
+                for k in ABLATION_VARS:
+                    os.environ.pop(k, None)
+                os.environ.update(env)
+                if part == "transform":
+                    for dt in ("f32", "f16"):
+                        ms = timed(paths[dt].transform)
+                        res[part]["%s %s" % (dt, label)] = {
+                            "ms": round(ms, 5), "GB/s": round(nums[dt]["transform_bytes"] / ms / 1e6, 1)}
+                else:
+                    p = paths[part]
+                    p.transform()
+                    ms = timed(p.run_conv)
+                    res[part][label] = {"ms": round(ms, 5),
+                                        "TFLOP/s": round(nums["flops"] / (ms * 1e-3) / 1e12, 2)}
+    finally:
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    del paths
+    return res
+
+
 def cpu_baseline(l, x, w, budget_s=10.0):
     """The fp64 oracle on the host cores over whole images of the same layer,
     a few images at a time, cycling through the batch until `budget_s` has
@@ -241,6 +319,9 @@ def main():
     ap.add_argument("--layer", default=None, help="configured layer name (default: cfg2)")
     ap.add_argument("--sweep", action="store_true", help="one line per configured layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ablation", default=None, metavar="LAYERS",
+                    help="comma-separated layer names: time the path with each of the paper's "
+                         "techniques switched off (one JSON line per layer) and exit")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes (HBM counter "
                          "calibration) and exit")
@@ -267,6 +348,12 @@ def main():
         from paper_2608_20725_amd import build
         build.build()
     pkg.load_library()
+
+    if args.ablation:
+        for name in args.ablation.split(","):
+            print(json.dumps(run_ablation(workloads.BY_NAME[name], pkg, torch, workloads)), flush=True)
+            torch.cuda.empty_cache()
+        return
 
     layers = list(workloads.ALL) if args.sweep else [
         workloads.BY_NAME[args.layer] if args.layer else workloads.CFG2]

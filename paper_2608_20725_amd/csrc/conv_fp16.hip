@@ -340,7 +340,7 @@ struct PipeCfg {
     static constexpr int BLOCKS = ROWS / 8;   // 8-row (1 KiB) blocks per stage
     static_assert(BLOCKS % NW == 0, "blocks split evenly over the waves");
     static constexpr int I = BLOCKS / NW;     // load instructions per wave per stage
-    static_assert((NSTAGE - 2) * I <= 63, "vmcnt range");
+    static_assert(NSTAGE == 1 || (NSTAGE - 2) * I <= 63, "vmcnt range");
     static constexpr int LDS = NSTAGE * STAGE;
 };
 
@@ -442,16 +442,30 @@ struct Pipe {
         if (st < nst)
             compute(cur);
     }
+
+    // One slot, no double buffering (the ablation of Alg. 1's double
+    // buffer): wait for stage st, multiply, and only when every wave is done
+    // reading load stage st+1 into the same slot.
+    template <int N>
+    __device__ inline void step_single(uint32_t st, char (&cur)[N])
+    {
+        wait_vmcnt<0>();
+        ring_barrier();
+        compute(cur);
+        ring_barrier();
+        issue(st + 1, cur);
+    }
 };
 
 template <class E, int WM, int WN, int WGM, int WGN, int NSTAGE>
 __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
 {
     using C = PipeCfg<WM, WN, WGM, WGN, NSTAGE>;
-    static_assert(NSTAGE >= 2 && NSTAGE <= 4, "ring depth");
+    static_assert(NSTAGE >= 1 && NSTAGE <= 4, "ring depth");
+    constexpr int S1 = NSTAGE > 1 ? C::STAGE : 1024;
     constexpr int S2 = NSTAGE > 2 ? C::STAGE : 1024, S3 = NSTAGE > 3 ? C::STAGE : 1024;
     __shared__ __attribute__((aligned(1024))) char r0[C::STAGE];
-    __shared__ __attribute__((aligned(1024))) char r1[C::STAGE];
+    __shared__ __attribute__((aligned(1024))) char r1[S1];
     __shared__ __attribute__((aligned(1024))) char r2[S2];
     __shared__ __attribute__((aligned(1024))) char r3[S3];
     __shared__ uint32_t rowoff[C::BNp];
@@ -516,7 +530,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
     // prologue: stages 0 .. NSTAGE-2 into slots 0 .. NSTAGE-2, then stage st
     // in slot st % NSTAGE
     w.issue(0, r0);
-    if constexpr (NSTAGE == 2) {
+    if constexpr (NSTAGE == 1) {
+        for (uint32_t st = 0; st < w.nst; ++st)
+            w.step_single(st, r0);
+    } else if constexpr (NSTAGE == 2) {
         for (uint32_t st = 0; st < w.nst; st += 2) {
             w.step(st, r0, r1);
             w.step(st + 1, r1, r0);
@@ -584,9 +601,19 @@ const PipeVariant *pipe_variants(int *n)
         // FLOP of the 128 x 128 tiles
         pipe_variant<4, 2, 2, 4, 2>("c256p256s2w8"),
         pipe_variant<2, 2, 2, 4, 2>("c128p256s2w8"),
+        // one ring slot: no double buffering (ablation)
+        pipe_variant<2, 2, 2, 2, 1>("c128p128s1"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
+}
+
+// IM2WIN_FP16_KERNEL=regs: the register-staged kernel on every layer (the
+// ablation of direct-to-LDS loads); the filter pack follows it.
+bool regs_forced()
+{
+    const char *e = getenv("IM2WIN_FP16_KERNEL");
+    return e && strcmp(e, "regs") == 0;
 }
 
 }  // namespace
@@ -604,7 +631,7 @@ hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed,
         a.nv = 1; a.tlen = (uint32_t)sh.K; a.tpad = (uint32_t)sh.K_pad;
         // pipelined and segment-staged kernels: 64-tap tiles; register-staged
         // kernel: one tile of K_pad taps
-        a.tb = ((sh.Ci % 8) == 0 || seg_plan(sh) >= 0) ? (uint32_t)BK : a.tpad;
+        a.tb = ((sh.Ci % 8 == 0 && !regs_forced()) || seg_plan(sh) >= 0) ? (uint32_t)BK : a.tpad;
     }
     a.grans = (uint64_t)sh.Co_pad * a.nv * a.tpad / 8;
     a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad;
@@ -633,7 +660,9 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
     a.Co = (uint32_t)sh.Co; a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.S = (uint32_t)sh.S;
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     void *args[] = {&a};
-    const bool aligned = (sh.Ci % 8) == 0;  // every window starts on a 16-byte boundary
+    // every window starts on a 16-byte boundary (unless the register-staged
+    // kernel is forced)
+    const bool aligned = (sh.Ci % 8) == 0 && !regs_forced();
     if (aligned) {
         int n;
         const PipeVariant *v = pipe_variants(&n);

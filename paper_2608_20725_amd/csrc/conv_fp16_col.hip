@@ -388,7 +388,7 @@ int col_plan(const Shape &sh)
     if (sh.Ci % 8 != 0)
         return -1;  // windows not 16-byte aligned
     if (const char *e = getenv("IM2WIN_FP16_KERNEL"))
-        if (strcmp(e, "pipe") == 0)
+        if (strcmp(e, "pipe") == 0 || strcmp(e, "regs") == 0)
             return -1;
     int n;
     const ColVariant *v = col_variants(&n);

@@ -20,6 +20,9 @@
 // as zeros; the padded input itself is never built.
 #include "common.hpp"
 
+#include <stdlib.h>
+#include <string.h>
+
 namespace im2win {
 namespace {
 
@@ -37,6 +40,7 @@ struct TArgs {
     uint64_t win_elems;
     uint64_t win_bytes, pad_end;
     uint64_t grans;          // gather: 16-byte granules of the window tensor
+    uint32_t xcd_order;      // vec: 1 = XCD-aware block order, 0 = linear (ablation)
     FastDiv div_Ci, div_Kh, div_Wi, div_Ho, div_L, div_gps;
 };
 
@@ -68,7 +72,8 @@ __global__ __launch_bounds__(kThreads) void transform_vec(TArgs a)
         zero_pad(a);
     // granules of the whole window tensor, numbered strip by strip
     // (granule counts fit 32 bits: transform_range_ok)
-    const uint32_t gb = xcd_block(blockIdx.x, gridDim.x) * (kThreads * kGranPerThread);
+    const uint32_t lb = a.xcd_order ? xcd_block(blockIdx.x, gridDim.x) : blockIdx.x;
+    const uint32_t gb = lb * (kThreads * kGranPerThread);
 #pragma unroll
     for (int t = 0; t < kGranPerThread; ++t) {
         const uint32_t g = gb + t * kThreads + threadIdx.x;
@@ -192,6 +197,10 @@ hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream
     a.div_Wi = make_fastdiv((uint32_t)sh.Wi);
     a.div_Ho = make_fastdiv((uint32_t)sh.Ho);
     a.div_L = make_fastdiv((uint32_t)sh.L);
+    // IM2WIN_TRANSFORM_ORDER=linear deals blocks in launch order (to measure
+    // what the XCD-aware order gains)
+    const char *order = getenv("IM2WIN_TRANSFORM_ORDER");
+    a.xcd_order = (order && strcmp(order, "linear") == 0) ? 0u : 1u;
     void *args[] = {&a};
     const bool vec = (sh.Ci * sh.elt) % 16 == 0;
     if (vec) {

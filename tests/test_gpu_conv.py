@@ -190,8 +190,12 @@ def test_fp16_register_kernel_on_segment_shapes(shape, monkeypatch):
 # variant tables in the C++ sources.
 VARIANT_CASES = [
     # (environment variable, names, shape, dtype, same summation order)
-    ("IM2WIN_FP16_TILE", ["c32p128s3", "c64p128s3", "c128p128s2", "c256p256s2w8", "c128p256s2w8"],
+    ("IM2WIN_FP16_TILE", ["c32p128s3", "c64p128s3", "c128p128s2", "c256p256s2w8", "c128p256s2w8", "c128p128s1"],
      (2, 16, 13, 13, 72, 5, 5, 1), torch.float16, True),
+    # the register-staged kernel forced on 16-byte-aligned windows (its filter
+    # pack follows): the same summation order as the row-per-pixel kernel
+    ("IM2WIN_FP16_KERNEL", ["pipe", "regs"], (2, 16, 13, 13, 72, 5, 5, 1), torch.float16, True),
+    ("IM2WIN_FP16_KERNEL", ["pipe", "regs"], (1, 64, 20, 20, 300, 3, 3, 1), torch.float16, True),
     ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c128p256t16s3", "k3c256p256t32s2w8", "k3c256p192t32s2w8"],
      (2, 64, 24, 24, 300, 3, 3, 1), torch.float16, False),
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16g4", "regs"],

@@ -82,3 +82,16 @@ def test_transform_sweep_sampled_strips(layer, dtype):
     pad_end = (nb + 255) // 256 * 256 + 256
     assert np.all(run.ws[nb:pad_end].cpu().numpy() == 0), "pad not zeroed"
     run.check_workspace_guard()
+
+
+@pytest.mark.parametrize("shape", [(4, 64, 30, 30, 3, 3, 1), (3, 8, 17, 19, 5, 3, 2)], ids=lambda s: "x".join(map(str, s)))
+def test_transform_linear_block_order_same_bytes(shape, monkeypatch):
+    """IM2WIN_TRANSFORM_ORDER=linear (the ablation of the XCD-aware block
+    order) changes only which block copies which granules: same bytes."""
+    N, Ci, H, W, Kh, Kw, s = shape
+    x, w = workloads.draw(N, Ci, H, W, 2, Kh, Kw, seed=3)
+    ref = Run(x, w, s, torch.float16, conv=False)
+    monkeypatch.setenv("IM2WIN_TRANSFORM_ORDER", "linear")
+    run = Run(x, w, s, torch.float16, conv=False)
+    _compare(run, x)
+    assert torch.equal(run.ws[:run.window_bytes()], ref.ws[:ref.window_bytes()])
