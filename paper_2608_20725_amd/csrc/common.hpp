@@ -137,6 +137,8 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
 // Column-staged fp16 kernel: the variant for this layer, or -1 when the
 // row-per-pixel kernels run instead.  The filter pack layout follows it.
 int col_plan(const Shape &sh);
+// The layer runs the one-slot row-per-pixel fp16 kernel (many tiles, C_o >= 128).
+bool fp16_single_slot_rows(const Shape &sh);
 int col_stage_taps(int plan);  // taps per stage of that variant (packed-filter tile)
 // Segment-staged fp16 kernel for windows that are not 16-byte aligned: the
 // variant for this layer, or -1 when the register-staged kernel runs.

@@ -608,6 +608,22 @@ const PipeVariant *pipe_variants(int *n)
     return v;
 }
 
+}  // namespace
+
+// Layers with C_o >= 128 and at least four 128 x 128 tiles per CU run the
+// row-per-pixel kernel with a one-slot ring: 32 KiB of LDS per workgroup lets
+// four workgroups share a CU, which keeps more stage bytes in flight per CU
+// than two double-buffered ones (measured, alternating runs: S7 639 vs 601
+// TFLOP/s with the column-staged kernel, S12 591 vs 547).  With fewer tiles the
+// workgroups' own double buffering wins (S5, S10).
+bool fp16_single_slot_rows(const Shape &sh)
+{
+    const int64_t tiles = ((sh.P + 127) / 128) * ((sh.Co + 127) / 128);
+    return sh.Ci % 8 == 0 && sh.Co >= 128 && tiles >= 1024;
+}
+
+namespace {
+
 // IM2WIN_FP16_KERNEL=regs: the register-staged kernel on every layer (the
 // ablation of direct-to-LDS loads); the filter pack follows it.
 bool regs_forced()
@@ -682,6 +698,8 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
         int pick;
         if (sh.Co <= 32)
             pick = find("c32p128s3");
+        else if (fp16_single_slot_rows(sh))
+            pick = find("c128p128s1");
         else if (sh.Co <= 64 || tiles(128, 128) < 256)
             pick = find("c64p128s3");
         else if (tiles(256, 256) >= 128 && tiles(256, 256) <= 256 && sh.Co >= 256)

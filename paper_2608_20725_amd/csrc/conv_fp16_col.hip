@@ -411,6 +411,8 @@ int col_plan(const Shape &sh)
         // lose (S5: 536 vs 636), so those layers keep the row kernel.
         auto tiles = [&](int64_t bn) { return ((sh.P + bn - 1) / bn) * ((sh.Co + 255) / 256); };
         const char *name = nullptr;
+        if (fp16_single_slot_rows(sh))
+            return -1;  // the one-slot row kernel is faster there
         if (sh.Kw == 3 && sh.Co <= 128)
             name = "k3c64p256t32s2";
         else if (sh.Kw == 7 && sh.Co <= 128)
