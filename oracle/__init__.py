@@ -7,7 +7,9 @@ definitions (Sec. III-A Eq. 1, Sec. III-B Eq. 2, Sec. III-C Eq. 3).  Only
 imports it.
 
 Layouts: input NHWC ``[N][H_i][W_i][C_i]``, filter ``[K_h][K_w][C_i][C_o]``,
-output NHWC ``[N][H_o][W_o][C_o]``, window tensor ``[N][H_o][W_i*K_h][C_i]``.
+output NHWC ``[N][H_o][W_o][C_o]``, window tensor ``[N][H_o][W_i*K_h][C_i]``
+(with filter dilation d: ``[N][H_o][d*ceil(W/d)*K_h][C_i]``, strip columns
+grouped by residue mod d; see ``oracle.c``).
 """
 from __future__ import annotations
 
@@ -66,6 +68,16 @@ def _load():
         lib.oracle_conv_pad_f64.argtypes = [_i64] * 10 + [_dp, _dp, _dp, _dp]
         lib.oracle_im2win_pad.restype = ctypes.c_int
         lib.oracle_im2win_pad.argtypes = [_i64] * 9 + [_vp, _vp]
+        lib.oracle_conv_dil_f64.restype = ctypes.c_int
+        lib.oracle_conv_dil_f64.argtypes = [_i64] * 11 + [_dp, _dp, _dp, _dp]
+        lib.oracle_dil_group_cols.restype = _i64
+        lib.oracle_dil_group_cols.argtypes = [_i64, _i64]
+        lib.oracle_dil_window_col.restype = _i64
+        lib.oracle_dil_window_col.argtypes = [_i64] * 4
+        lib.oracle_im2win_dil.restype = ctypes.c_int
+        lib.oracle_im2win_dil.argtypes = [_i64] * 10 + [_vp, _vp]
+        lib.oracle_windowed_conv_dil_f64.restype = ctypes.c_int
+        lib.oracle_windowed_conv_dil_f64.argtypes = [_i64] * 9 + [_dp, _dp, _dp]
         _lib = lib
     return _lib
 
@@ -208,4 +220,82 @@ def im2win_pad(x, k_h: int, stride: int, pad_h: int, pad_w: int) -> np.ndarray:
                                    x.ctypes.data_as(_vp), out.ctypes.data_as(_vp))
     if rc != 0:
         raise ValueError("oracle_im2win_pad rejected its arguments")
+    return out
+
+
+def dil_extent(n: int, k: int, stride: int, dilation: int) -> int:
+    """Output extent with filter dilation: floor((n - (k-1)*d - 1) / s) + 1,
+    or -1 when the dilated filter does not fit."""
+    if dilation <= 0 or k <= 0:
+        return -1
+    return out_extent(n, (k - 1) * dilation + 1, stride)
+
+
+def conv_dil(x, w, stride: int, pad_h: int, pad_w: int, dilation: int, with_abs: bool = False):
+    """Eq. (1) with filter dilation on the zero-padded input (an extension):
+    tap (u, v) reads padded row m*s + u*d and column n*s + v*d.  Returns O
+    (and A = sum |x||w|, if ``with_abs``)."""
+    x = _f64(x)
+    w = _f64(w)
+    N, Hi, Wi, Ci = x.shape
+    Kh, Kw, Ci2, Co = w.shape
+    if Ci2 != Ci:
+        raise ValueError("channel mismatch")
+    Ho = dil_extent(Hi + 2 * pad_h, Kh, stride, dilation)
+    Wo = dil_extent(Wi + 2 * pad_w, Kw, stride, dilation)
+    if Ho < 0 or Wo < 0 or pad_h < 0 or pad_w < 0:
+        raise ValueError("filter does not fit")
+    out = np.empty((N, Ho, Wo, Co), np.float64)
+    ab = np.empty_like(out) if with_abs else None
+    rc = _load().oracle_conv_dil_f64(N, Ci, Hi, Wi, Co, Kh, Kw, stride, pad_h, pad_w, dilation, _ptr(x),
+                                     _ptr(w), _ptr(out), _ptr(ab) if with_abs else None)
+    if rc != 0:
+        raise ValueError("oracle_conv_dil_f64 rejected its arguments")
+    return (out, ab) if with_abs else out
+
+
+def dil_group_cols(wp: int, dilation: int) -> int:
+    """Columns per residue group of a dilated strip, ceil(Wp / d)."""
+    return int(_load().oracle_dil_group_cols(wp, dilation))
+
+
+def dil_window_col(n: int, stride: int, dilation: int, wq: int) -> int:
+    """Strip position (in columns) where the window of output column n starts."""
+    return int(_load().oracle_dil_window_col(n, stride, dilation, wq))
+
+
+def im2win_dil(x, k_h: int, stride: int, pad_h: int, pad_w: int, dilation: int) -> np.ndarray:
+    """Eq. (2) with dilation on the zero-padded input: [N][H_o][d*Wq*K_h][C_i],
+    strip columns grouped by residue mod d, bit-exact, zero bytes at padded
+    and filler positions."""
+    x = np.ascontiguousarray(x)
+    N, Hi, Wi, Ci = x.shape
+    Ho = dil_extent(Hi + 2 * pad_h, k_h, stride, dilation)
+    if Ho < 0 or pad_h < 0 or pad_w < 0:
+        raise ValueError("filter does not fit")
+    Wq = dil_group_cols(Wi + 2 * pad_w, dilation)
+    out = np.empty((N, Ho, dilation * Wq * k_h, Ci), x.dtype)
+    rc = _load().oracle_im2win_dil(N, Ci, Hi, Wi, k_h, stride, pad_h, pad_w, dilation, x.dtype.itemsize,
+                                   x.ctypes.data_as(_vp), out.ctypes.data_as(_vp))
+    if rc != 0:
+        raise ValueError("oracle_im2win_dil rejected its arguments")
+    return out
+
+
+def windowed_conv_dil(win, w, hp: int, wp: int, stride: int, dilation: int) -> np.ndarray:
+    """Eq. (3) with dilation: the convolution read out of ``im2win_dil``'s
+    window tensor (padded extents ``hp`` x ``wp``)."""
+    win = _f64(win)
+    w = _f64(w)
+    N, Ho = win.shape[0], win.shape[1]
+    Ci = win.shape[3]
+    Kh, Kw, Ci2, Co = w.shape
+    Wo = dil_extent(wp, Kw, stride, dilation)
+    if Ci2 != Ci or Wo < 0:
+        raise ValueError("shape mismatch")
+    out = np.empty((N, Ho, Wo, Co), np.float64)
+    rc = _load().oracle_windowed_conv_dil_f64(N, Ci, hp, wp, Co, Kh, Kw, stride, dilation, _ptr(win), _ptr(w),
+                                              _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_windowed_conv_dil_f64 rejected its arguments")
     return out

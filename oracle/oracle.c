@@ -28,6 +28,11 @@
  *   oracle_im2win_pad          (an extension: the paper's layers have no
  *                              padding), read through an index rule, never
  *                              built
+ *   oracle_conv_dil_f64 /      Eq. (1), Eq. (2) and Eq. (3) with filter
+ *   oracle_im2win_dil /        dilation (an extension, with padding): taps
+ *   oracle_windowed_conv_dil_f64  d apart, and a window tensor whose strip
+ *                              columns are grouped by residue mod d so that
+ *                              every window stays one contiguous span
  */
 #include <stdint.h>
 #include <string.h>
@@ -335,6 +340,165 @@ int oracle_im2win_pad(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi,
                         else
                             memset(dst + d * elt, 0, (size_t)elt);
                     }
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+/*
+ * Filter dilation d >= 1 (an extension; the paper's layers have none): tap
+ * (u, v) of output (m, n) reads padded input row m*s + u*d and column
+ * n*s + v*d.  The dilated filter spans E_h = (K_h - 1)*d + 1 rows and E_w
+ * columns, so H_o = floor((H_i + 2 ph - E_h) / s) + 1 and W_o likewise.
+ * d = 1 is the padded convolution above.
+ */
+static int64_t oracle_dil_extent(int64_t in, int64_t k, int64_t s, int64_t d)
+{
+    if (d <= 0 || k <= 0)
+        return -1;
+    return oracle_out_extent(in, (k - 1) * d + 1, s);
+}
+
+/* Eq. (1) with dilation d on the padded input; `absout` (may be NULL) gets
+ * the |x||w| sum.  Loops (i, m, n, j, u, v, r), fp64. */
+int oracle_conv_dil_f64(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co,
+                        int64_t Kh, int64_t Kw, int64_t s, int64_t ph, int64_t pw, int64_t d,
+                        const double *in, const double *filt, double *out, double *absout)
+{
+    if (ph < 0 || pw < 0 || Hi <= 0 || Wi <= 0)
+        return -1;
+    int64_t Ho = oracle_dil_extent(Hi + 2 * ph, Kh, s, d);
+    int64_t Wo = oracle_dil_extent(Wi + 2 * pw, Kw, s, d);
+    if (N <= 0 || Ci <= 0 || Co <= 0 || Ho < 0 || Wo < 0)
+        return -1;
+
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t i = 0; i < N; ++i) {
+        for (int64_t m = 0; m < Ho; ++m) {
+            for (int64_t n = 0; n < Wo; ++n) {
+                for (int64_t j = 0; j < Co; ++j) {
+                    double acc = 0.0, aacc = 0.0;
+                    for (int64_t u = 0; u < Kh; ++u) {
+                        for (int64_t v = 0; v < Kw; ++v) {
+                            int64_t h = m * s + u * d - ph, w = n * s + v * d - pw;
+                            if (!oracle_pad_tap(h, w, Hi, Wi))
+                                continue;
+                            for (int64_t r = 0; r < Ci; ++r) {
+                                double x = in[((i * Hi + h) * Wi + w) * Ci + r];
+                                double f = filt[((u * Kw + v) * Ci + r) * Co + j];
+                                acc += x * f;
+                                aacc += fabs(x) * fabs(f);
+                            }
+                        }
+                    }
+                    int64_t o = ((i * Ho + m) * Wo + n) * Co + j;
+                    out[o] = acc;
+                    if (absout)
+                        absout[o] = aacc;
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+/*
+ * Columns per residue group of a strip: Wq = ceil(Wp / d) for the padded
+ * width Wp.  Strip position P (0 <= P < d*Wq) holds padded column
+ *   k = (P mod Wq) * d + floor(P / Wq)        (group floor(P / Wq)),
+ * or nothing (zero filler) when k >= Wp.  The window of output column n then
+ * starts at position ((n*s) mod d) * Wq + floor(n*s / d) and its K_w columns
+ * n*s + v*d are the K_w positions after it; d = 1 gives position n*s, Eq. 2's
+ * order.
+ */
+int64_t oracle_dil_group_cols(int64_t Wp, int64_t d)
+{
+    if (Wp <= 0 || d <= 0)
+        return -1;
+    return (Wp + d - 1) / d;
+}
+
+int64_t oracle_dil_window_col(int64_t n, int64_t s, int64_t d, int64_t Wq)
+{
+    int64_t c = n * s;
+    return (c % d) * Wq + c / d;
+}
+
+/*
+ * Eq. (2) with dilation on the padded input:
+ *   W[i][m][P*K_h + u][r] = Ip[i][m*s + u*d][k(P)][r]
+ * for P < d*Wq, u < K_h, r < C_i; filler positions and padded taps are zero
+ * bytes.  Raw `elt`-byte copies.
+ */
+int oracle_im2win_dil(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Kh, int64_t s,
+                      int64_t ph, int64_t pw, int64_t d, int64_t elt, const void *in, void *out)
+{
+    if (ph < 0 || pw < 0 || Hi <= 0 || Wi <= 0)
+        return -1;
+    int64_t Hp = Hi + 2 * ph, Wp = Wi + 2 * pw;
+    int64_t Ho = oracle_dil_extent(Hp, Kh, s, d);
+    int64_t Wq = oracle_dil_group_cols(Wp, d);
+    if (N <= 0 || Ci <= 0 || Ho < 0 || Wq < 0 || elt <= 0)
+        return -1;
+    int64_t cols = d * Wq;
+    const unsigned char *src = (const unsigned char *)in;
+    unsigned char *dst = (unsigned char *)out;
+
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t i = 0; i < N; ++i) {
+        for (int64_t m = 0; m < Ho; ++m) {
+            for (int64_t P = 0; P < cols; ++P) {
+                int64_t k = (P % Wq) * d + P / Wq;
+                for (int64_t u = 0; u < Kh; ++u) {
+                    int64_t h = m * s + u * d - ph, w = k - pw;
+                    for (int64_t r = 0; r < Ci; ++r) {
+                        int64_t o = ((i * Ho + m) * (cols * Kh) + (P * Kh + u)) * Ci + r;
+                        if (k < Wp && oracle_pad_tap(h, w, Hi, Wi))
+                            memcpy(dst + o * elt, src + (((i * Hi + h) * Wi + w) * Ci + r) * elt,
+                                   (size_t)elt);
+                        else
+                            memset(dst + o * elt, 0, (size_t)elt);
+                    }
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+/*
+ * Eq. (3) with dilation: the sums of oracle_conv_dil_f64 read out of the
+ * dilated window tensor `win` (as oracle_im2win_dil lays it out): the window
+ * of (i, m, n) is the K = K_w*K_h*C_i elements of strip (i, m) from position
+ * oracle_dil_window_col(n) on, in (v, u, r) order.  H_i, W_i are the padded
+ * extents.
+ */
+int oracle_windowed_conv_dil_f64(int64_t N, int64_t Ci, int64_t Hp, int64_t Wp, int64_t Co,
+                                 int64_t Kh, int64_t Kw, int64_t s, int64_t d,
+                                 const double *win, const double *filt, double *out)
+{
+    int64_t Ho = oracle_dil_extent(Hp, Kh, s, d);
+    int64_t Wo = oracle_dil_extent(Wp, Kw, s, d);
+    int64_t Wq = oracle_dil_group_cols(Wp, d);
+    if (N <= 0 || Ci <= 0 || Co <= 0 || Ho < 0 || Wo < 0 || Wq < 0)
+        return -1;
+    int64_t L = d * Wq * Kh * Ci;
+
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t i = 0; i < N; ++i) {
+        for (int64_t m = 0; m < Ho; ++m) {
+            const double *strip = win + (i * Ho + m) * L;
+            for (int64_t n = 0; n < Wo; ++n) {
+                const double *span = strip + oracle_dil_window_col(n, s, d, Wq) * Kh * Ci;
+                for (int64_t j = 0; j < Co; ++j) {
+                    double acc = 0.0;
+                    for (int64_t v = 0; v < Kw; ++v)
+                        for (int64_t u = 0; u < Kh; ++u)
+                            for (int64_t r = 0; r < Ci; ++r)
+                                acc += span[(v * Kh + u) * Ci + r] * filt[((u * Kw + v) * Ci + r) * Co + j];
+                    out[((i * Ho + m) * Wo + n) * Co + j] = acc;
                 }
             }
         }

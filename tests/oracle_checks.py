@@ -343,6 +343,116 @@ def check_im2win_pad_layout(orc):
             assert win.tobytes() == _numpy_im2win(_zero_pad(x, ph, pw), Kh, s).tobytes()
 
 
+# Filter dilation (an extension, combined with padding), pinned against
+# torch's dilated conv2d, against the padded oracle with a zero-inserted filter
+# (exact on integers), against d = 1 and 1x1 reductions, and a slicing-built
+# window layout.
+DIL_CASES = [
+    # N, Ci, H, W, Co, Kh, Kw, s, pad_h, pad_w, d
+    (2, 3, 9, 10, 4, 3, 3, 1, 2, 2, 2),     # "same" 3x3, d = 2
+    (1, 2, 11, 9, 3, 3, 2, 2, 1, 3, 3),     # K_h != K_w, stride 2, d = 3, pad_h != pad_w
+    (2, 4, 8, 8, 2, 2, 2, 1, 0, 0, 4),      # no padding, d = 4
+    (1, 1, 7, 13, 2, 3, 3, 3, 0, 1, 2),     # stride 3 > d, padded width not a multiple of d
+    (1, 3, 6, 6, 2, 1, 1, 1, 0, 0, 3),      # 1x1: dilation changes nothing
+]
+
+
+def _torch_conv_dil(x, w, s, ph, pw, d):
+    xt = torch.from_numpy(np.ascontiguousarray(x, np.float64)).permute(0, 3, 1, 2)
+    wt = torch.from_numpy(np.ascontiguousarray(w, np.float64)).permute(3, 2, 0, 1)
+    y = torch.nn.functional.conv2d(xt, wt.contiguous(), stride=s, padding=(ph, pw), dilation=d)
+    return y.permute(0, 2, 3, 1).contiguous().numpy()
+
+
+def _insert_zeros(w, d):
+    Kh, Kw, Ci, Co = w.shape
+    big = np.zeros(((Kh - 1) * d + 1, (Kw - 1) * d + 1, Ci, Co), w.dtype)
+    big[::d, ::d] = w
+    return big
+
+
+def check_dil_vs_torch_conv2d(orc):
+    for t, (N, Ci, H, W, Co, Kh, Kw, s, ph, pw, d) in enumerate(DIL_CASES):
+        r = _rng(110 + t)
+        x = r.uniform(-1, 1, (N, H, W, Ci))
+        w = r.uniform(-1, 1, (Kh, Kw, Ci, Co))
+        y = orc.conv_dil(x, w, s, ph, pw, d)
+        ref = _torch_conv_dil(x, w, s, ph, pw, d)
+        assert y.shape == ref.shape, (y.shape, ref.shape)
+        np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12)
+
+
+def check_dil_vs_inserted_zeros(orc):
+    # integer inputs: the dilated filter is the filter with d-1 zero rows and
+    # columns between taps; the padded oracle on it gives the same sums exactly
+    for t, (N, Ci, H, W, Co, Kh, Kw, s, ph, pw, d) in enumerate(DIL_CASES):
+        r = _rng(120 + t)
+        x = r.integers(-2, 3, (N, H, W, Ci)).astype(np.float64)
+        w = r.integers(-2, 3, (Kh, Kw, Ci, Co)).astype(np.float64)
+        y, a = orc.conv_dil(x, w, s, ph, pw, d, with_abs=True)
+        ref, aref = orc.conv_pad(x, _insert_zeros(w, d), s, ph, pw, with_abs=True)
+        assert np.array_equal(y, ref) and np.array_equal(a, aref)
+
+
+def check_dil_reductions(orc):
+    # d = 1 is the padded convolution and window tensor; a 1x1 filter ignores d
+    for t, (N, Ci, H, W, Co, Kh, Kw, s, ph, pw, d) in enumerate(DIL_CASES + [c[:10] + (1,) for c in DIL_CASES]):
+        r = _rng(130 + t)
+        x = r.uniform(-1, 1, (N, H, W, Ci))
+        w = r.uniform(-1, 1, (Kh, Kw, Ci, Co))
+        if d == 1:
+            assert np.array_equal(orc.conv_dil(x, w, s, ph, pw, 1), orc.conv_pad(x, w, s, ph, pw))
+            x16 = x.astype(np.float16)
+            assert orc.im2win_dil(x16, Kh, s, ph, pw, 1).tobytes() == orc.im2win_pad(x16, Kh, s, ph, pw).tobytes()
+        if Kh == 1 and Kw == 1:
+            assert np.array_equal(orc.conv_dil(x, w, s, ph, pw, d), orc.conv_pad(x, w, s, ph, pw))
+
+
+def check_im2win_dil_layout(orc):
+    # every window is one contiguous span of its strip, holding the dilated
+    # patch in (v, u, r) order; every padded column sits in exactly one strip
+    # position of its residue group, the rest of the strip is zero
+    for t, (N, Ci, H, W, Co, Kh, Kw, s, ph, pw, d) in enumerate(DIL_CASES):
+        x = _rng(140 + t).uniform(-1, 1, (N, H, W, Ci)).astype(np.float32)
+        xp = _zero_pad(x, ph, pw)
+        Hp, Wp = xp.shape[1], xp.shape[2]
+        win = orc.im2win_dil(x, Kh, s, ph, pw, d)
+        Ho = orc.dil_extent(Hp, Kh, s, d)
+        Wo = orc.dil_extent(Wp, Kw, s, d)
+        Wq = -(-Wp // d)
+        assert win.shape == (N, Ho, d * Wq * Kh, Ci)
+        strips = win.reshape(N, Ho, d * Wq, Kh, Ci)
+        seen = []
+        for P in range(d * Wq):
+            k = (P % Wq) * d + P // Wq
+            if k < Wp:
+                seen.append(k)
+                for m in range(Ho):
+                    rows = xp[:, m * s + np.arange(Kh) * d, k, :]
+                    assert np.array_equal(strips[:, m, P], rows)
+            else:
+                assert not strips[:, :, P].any()
+        assert sorted(seen) == list(range(Wp))
+        flat = win.reshape(N, Ho, -1)
+        T = Kh * Ci
+        for m in range(Ho):
+            for n in range(Wo):
+                c0 = orc.dil_window_col(n, s, d, Wq)
+                span = flat[:, m, c0 * T:(c0 + Kw) * T]
+                patch = xp[:, m * s + np.arange(Kh)[None, :] * d, n * s + np.arange(Kw)[:, None] * d, :]
+                assert np.array_equal(span, patch.reshape(N, -1)), (t, m, n)
+
+
+def check_windowed_dil_equals_direct(orc):
+    for t, (N, Ci, H, W, Co, Kh, Kw, s, ph, pw, d) in enumerate(DIL_CASES):
+        r = _rng(150 + t)
+        x = r.integers(-2, 3, (N, H, W, Ci)).astype(np.float64)
+        w = r.integers(-2, 3, (Kh, Kw, Ci, Co)).astype(np.float64)
+        win = orc.im2win_dil(x, Kh, s, ph, pw, d)
+        y = orc.windowed_conv_dil(win, w, H + 2 * ph, W + 2 * pw, s, d)
+        assert np.array_equal(y, orc.conv_dil(x, w, s, ph, pw, d))
+
+
 ALL_CHECKS = [
     check_table1_extents, check_fig1_shapes, check_vs_torch_conv2d, check_vs_strided_slices,
     check_1x1_is_matmul, check_delta_filter, check_full_filter_is_dot, check_linearity,
@@ -350,4 +460,6 @@ ALL_CHECKS = [
     check_windows_contiguous, check_windowed_equals_direct, check_sizes,
     check_sizes_match_materialised, check_pad_vs_torch_conv2d, check_pad_vs_explicit_zeros,
     check_pad_same_delta, check_pad_zero_is_unpadded, check_im2win_pad_layout,
+    check_dil_vs_torch_conv2d, check_dil_vs_inserted_zeros, check_dil_reductions, check_im2win_dil_layout,
+    check_windowed_dil_equals_direct,
 ]

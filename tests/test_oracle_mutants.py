@@ -50,6 +50,15 @@ MUTANTS = [
     ("im2win_pad_no_shift", "int64_t h = m * s + u - ph, w = k - pw;", "int64_t h = m * s + u, w = k;", 0),
     ("im2win_pad_strip_width", "int64_t d = ((i * Ho + m) * (Wp * Kh) + (k * Kh + u)) * Ci + r;",
      "int64_t d = ((i * Ho + m) * (Wi * Kh) + (k * Kh + u)) * Ci + r;", 0),
+    ("dil_row_undilated", "int64_t h = m * s + u * d - ph, w = n * s + v * d - pw;",
+     "int64_t h = m * s + u - ph, w = n * s + v * d - pw;", 0),
+    ("dil_extent_k_times_d", "return oracle_out_extent(in, (k - 1) * d + 1, s);",
+     "return oracle_out_extent(in, k * d, s);", 0),
+    ("dil_group_order_swapped", "int64_t k = (P % Wq) * d + P / Wq;", "int64_t k = (P / d) * d + P % d;", 0),
+    ("dil_window_col_swapped", "return (c % d) * Wq + c / d;", "return (c / d) * Wq + c % d;", 0),
+    ("im2win_dil_row_undilated", "int64_t h = m * s + u * d - ph, w = k - pw;",
+     "int64_t h = m * s + u - ph, w = k - pw;", 0),
+    ("windowed_dil_uses_Kw", "span[(v * Kh + u) * Ci + r]", "span[(v * Kw + u) * Ci + r]", 0),
 ]
 
 
