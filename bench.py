@@ -15,8 +15,10 @@ Prints ONE JSON line.  `--layer NAME` picks another configured layer and
 `--sweep` prints one line per configured layer instead (for reports);
 `--ablation LAYERS` times the path with each of the paper's techniques
 switched off (Sec. IV-D) on the named layers.  Each
-line also carries a `bf16` block: the same layer with bf16 operands on the
-same matrix-core kernels, timed outside the step (an extension of the path).
+line also carries a `bf16` block (the same layer with bf16 operands on the
+same matrix-core kernels) and a `dilated` block (the layer with filter
+dilation 2 and 'same' padding, fp32 and fp16), both timed outside the step
+(extensions of the path).
 """
 from __future__ import annotations
 
@@ -245,6 +247,56 @@ def run_ablation(l, pkg, torch, workloads, reps=15):
     return res
 
 
+def measure_dilated(l, x, w, pkg, torch, d=2, reps=20):
+    """The atrous version of the layer (filter dilation d, zero padding
+    d*(K-1)/2 so the output keeps the input extent when the stride is 1), in
+    fp32 and fp16, outside the timed step: median transform and pack+conv
+    times over `reps` runs, HIP events on the launch stream, and the window
+    tensor against an im2col matrix of the same layer."""
+    ph, pw = d * (l.K_h - 1) // 2, d * (l.K_w - 1) // 2
+    Hp, Wp = l.H + 2 * ph, l.W + 2 * pw
+    Ho, Wo = pkg.conv_output_dims_dilated(Hp, Wp, l.K_h, l.K_w, l.stride, d)
+    flops = 2.0 * l.N * Ho * Wo * l.C_o * l.K_h * l.K_w * l.C_i
+    res = {"dilation": d, "pad": [ph, pw], "output": [Ho, Wo]}
+    for name, dt in (("f32", torch.float32), ("f16", torch.float16)):
+        xd = x.to(dt).contiguous().cuda()
+        wd = w.to(dt).contiguous().cuda()
+        need = pkg.conv_workspace_bytes_dilated(l.N, l.C_i, Hp, Wp, l.C_o, l.K_h, l.K_w, l.stride, d, dt)
+        ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        out = torch.empty((l.N, Ho, Wo, l.C_o), dtype=dt, device="cuda")
+
+        def tr():
+            pkg.conv_im2win_transform_dilated(xd, ws, l.C_o, l.K_h, l.K_w, l.stride, ph, pw, d)
+
+        def cv():
+            pkg.conv_im2win_dilated(ws, wd, out, l.N, l.C_i, Hp, Wp, l.stride, d)
+        for _ in range(3):
+            tr()
+            cv()
+        torch.cuda.synchronize()
+        t_tr, t_cv = [], []
+        for _ in range(reps):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e[0].record()
+            tr()
+            e[1].record()
+            cv()
+            e[2].record()
+            torch.cuda.synchronize()
+            t_tr.append(e[0].elapsed_time(e[1]))
+            t_cv.append(e[1].elapsed_time(e[2]))
+        t_tr.sort()
+        t_cv.sort()
+        elt = 4 if dt == torch.float32 else 2
+        im2col = l.N * Ho * Wo * l.K_h * l.K_w * l.C_i * elt
+        win = l.N * Ho * d * ((Wp + d - 1) // d) * l.K_h * l.C_i * elt
+        res[name] = {"transform_ms": round(t_tr[reps // 2], 5), "pack_conv_ms": round(t_cv[reps // 2], 5),
+                     "TFLOP/s": round(flops / (t_cv[reps // 2] * 1e-3) / 1e12, 3),
+                     "window_bytes": win, "im2col_bytes": im2col, "window_over_im2col": round(win / im2col, 4)}
+        del xd, wd, ws, out
+    return res
+
+
 def cpu_baseline(l, x, w, budget_s=10.0):
     """The fp64 oracle on the host cores over whole images of the same layer,
     a few images at a time, cycling through the batch until `budget_s` has
@@ -422,6 +474,7 @@ def main():
             },
         }
         rec["bf16"] = measure_bf16(l, x, w, pkg, torch)
+        rec["dilated"] = measure_dilated(l, x, w, pkg, torch)
         if not args.sweep:
             mb = measure_minibatch(l, paths, pkg, torch)
             for name in ("f32", "f16"):

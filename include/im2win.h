@@ -34,7 +34,8 @@
  *                       fp32: [K_pad32][C_o_pad32] fp32, K_pad32 = round_up(K, 16),
  *                             C_o_pad32 = round_up(C_o, 32)
  *
- * Scope: one stride for both axes, no padding, dilation, groups or bias.
+ * Scope: one stride and one dilation for both axes; zero padding and dilation
+ * through the *_padded / *_dilated calls below; no groups or bias.
  *
  * Ownership and threading: the caller allocates and frees every buffer; the
  * library allocates nothing and keeps no state except a once-filled per-device
@@ -196,6 +197,63 @@ int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
 int conv_im2win_bf16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
                      uint16_t *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream);
+
+/*
+ * Filter dilation (an extension; the paper's layers have none): tap (u, v) of
+ * output (m, n) reads input row m*s + u*d and column n*s + v*d, so
+ *   O[i][m][n][j] = sum_u sum_v sum_r I[i][m*s+u*d][n*s+v*d][r] * F[u][v][r][j],
+ * the dilated filter spans E_h = (K_h-1)*d + 1 rows and E_w columns, and
+ * H_o = (H_i - E_h)/s + 1, W_o likewise.  d = 1 is the plain convolution.
+ *
+ * Window tensor with dilation: each strip (i, m) holds rows m*s + u*d of the
+ * input, and its columns are grouped by residue mod d: with Wq = ceil(W_i/d)
+ * columns per group, strip column P holds input column (P mod Wq)*d +
+ * floor(P/Wq) (zero filler where that is >= W_i), element (P*K_h + u)*C_i + r.
+ * The window of output column n is then one contiguous span of K elements
+ * starting at column ((n*s) mod d)*Wq + floor(n*s/d), in (filter column,
+ * filter row, channel) order as in Eq. 3.  Workspace layout as above with
+ * strips of d*Wq*K_h*C_i elements (at most (d-1)*K_h*C_i more than W_i*K_h*C_i).
+ */
+
+/* Output extent with dilation (no padding).  Host only.  IM2WIN_EINVAL when
+ * the dilated filter does not fit or an argument is out of range. */
+int conv_output_dims_dilated(int64_t H_i, int64_t W_i, int64_t K_h, int64_t K_w, int64_t stride,
+                             int64_t dilation, int64_t *H_o, int64_t *W_o);
+
+/* Workspace bytes of a dilated layer (H_i, W_i: the padded extents when the
+ * transform pads).  Index ranges as for conv_workspace_bytes, with the strip
+ * d*ceil(W_i/d)*K_h*C_i below 2^20 elements.  Host only. */
+int64_t conv_workspace_bytes_dilated(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
+                                     int64_t K_h, int64_t K_w, int64_t stride, int64_t dilation,
+                                     im2win_dtype_t dt);
+
+/*
+ * The dilated window tensor of the input zero-padded by pad_h rows and pad_w
+ * columns on each side (pads >= 0; dilation >= 1; dilation 1 is
+ * conv_im2win_transform_padded).
+ *   in_nhwc  device, the stored input [N][H_i][W_i][C_i], read only
+ *   ws       device, ws_bytes >= conv_workspace_bytes_dilated(N, C_i,
+ *            H_i + 2*pad_h, W_i + 2*pad_w, C_o, K_h, K_w, stride, dilation, dt)
+ * Errors as for conv_im2win_transform_padded.
+ */
+int conv_im2win_transform_dilated(const void *in_nhwc, void *ws, int64_t ws_bytes, int64_t N, int64_t C_i,
+                                  int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+                                  int64_t stride, int64_t pad_h, int64_t pad_w, int64_t dilation,
+                                  im2win_dtype_t dt, void *hip_stream);
+
+/*
+ * Dilated windowed convolution from the dilated window tensor in `ws`
+ * (written by conv_im2win_transform_dilated with the same dt and dilation),
+ * in the precision `dt` names: IM2WIN_F32 on the vector ALUs (filter and
+ * output fp32), IM2WIN_F16 / IM2WIN_BF16 on the matrix cores (16-bit filter
+ * and output bits, fp32 accumulation, one rounding on store).  H_i, W_i are
+ * the (padded) extents the window tensor was built for.  Numerics, buffer
+ * rules and errors as for conv_im2win_fp32/fp16/bf16; dilation 1 gives their
+ * results bit for bit.
+ */
+int conv_im2win_dilated(void *ws, int64_t ws_bytes, const void *filt_khkwcico, void *out_nhwc, int64_t N,
+                        int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+                        int64_t stride, int64_t dilation, im2win_dtype_t dt, void *hip_stream);
 
 /*
  * Mini-batch im2win: bytes of workspace conv_im2win_chunked needs for chunks

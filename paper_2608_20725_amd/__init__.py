@@ -12,6 +12,8 @@ kernels; there is no fallback, and a missing library raises.
     conv_im2win_fp32(ws, w, out, N, C_i, H_i, W_i, stride)     # Sec. III-C, Eq. 3
     conv_im2win_fp16(ws, w, out, N, C_i, H_i, W_i, stride)     # Sec. III-D, Alg. 1
     conv_im2win_bf16(ws, w, out, N, C_i, H_i, W_i, stride)     # same, bf16 operands
+    conv_im2win_transform_dilated(x, ws, C_o, K_h, K_w, stride, pad_h, pad_w, dilation)
+    conv_im2win_dilated(ws, w, out, N, C_i, H_p, W_p, stride, dilation)
 
 Layouts: ``x`` NHWC, ``w`` [K_h][K_w][C_i][C_o], ``out`` NHWC; ``ws`` is a
 flat byte tensor on the same device.
@@ -25,7 +27,8 @@ __all__ = [
     "Im2winError", "load_library", "library_path", "F32", "F16", "BF16",
     "conv_output_dims", "conv_workspace_bytes", "conv_im2col_bytes",
     "conv_im2win_transform", "conv_im2win_transform_padded", "conv_im2win_fp32", "conv_im2win_fp16",
-    "conv_im2win_bf16",
+    "conv_im2win_bf16", "conv_output_dims_dilated", "conv_workspace_bytes_dilated",
+    "conv_im2win_transform_dilated", "conv_im2win_dilated",
     "conv_im2win_strerror", "im2win_conv2d",
 ]
 
@@ -76,6 +79,14 @@ def load_library():
     lib.conv_im2win_fp16.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
     lib.conv_im2win_bf16.restype = ctypes.c_int
     lib.conv_im2win_bf16.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
+    lib.conv_output_dims_dilated.restype = ctypes.c_int
+    lib.conv_output_dims_dilated.argtypes = [_i64] * 6 + [ctypes.POINTER(_i64)] * 2
+    lib.conv_workspace_bytes_dilated.restype = _i64
+    lib.conv_workspace_bytes_dilated.argtypes = [_i64] * 9 + [ctypes.c_int]
+    lib.conv_im2win_transform_dilated.restype = ctypes.c_int
+    lib.conv_im2win_transform_dilated.argtypes = [_vp, _vp, _i64] + [_i64] * 11 + [ctypes.c_int, _vp]
+    lib.conv_im2win_dilated.restype = ctypes.c_int
+    lib.conv_im2win_dilated.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 9 + [ctypes.c_int, _vp]
     lib.conv_chunked_workspace_bytes.restype = _i64
     lib.conv_chunked_workspace_bytes.argtypes = [_i64] * 9 + [ctypes.c_int, ctypes.c_int]
     lib.conv_im2win_chunked.restype = ctypes.c_int
@@ -259,3 +270,48 @@ def conv_im2win_chunked(x, w, out, ws, stride: int, n_chunk: int, stream=None, a
         stride, n_chunk, _dtype_code(x.dtype), _stream(stream), aux)
     _check(rc, "conv_im2win_chunked")
 
+
+
+def conv_output_dims_dilated(H_i: int, W_i: int, K_h: int, K_w: int, stride: int, dilation: int):
+    ho, wo = _i64(), _i64()
+    _check(load_library().conv_output_dims_dilated(H_i, W_i, K_h, K_w, stride, dilation,
+                                                   ctypes.byref(ho), ctypes.byref(wo)),
+           "conv_output_dims_dilated")
+    return ho.value, wo.value
+
+
+def conv_workspace_bytes_dilated(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dilation, dtype) -> int:
+    n = load_library().conv_workspace_bytes_dilated(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dilation,
+                                                    _dtype_code(dtype))
+    if n < 0:
+        raise Im2winError(int(n), "conv_workspace_bytes_dilated")
+    return int(n)
+
+
+def conv_im2win_transform_dilated(x, ws, C_o: int, K_h: int, K_w: int, stride: int, pad_h: int, pad_w: int,
+                                  dilation: int, stream=None):
+    """Writes the dilated window tensor of ``x`` zero-padded by ``pad_h`` /
+    ``pad_w`` into ``ws`` (sized by conv_workspace_bytes_dilated for the
+    padded extents)."""
+    if x.dim() != 4 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous NHWC tensor")
+    N, H_i, W_i, C_i = x.shape
+    rc = load_library().conv_im2win_transform_dilated(
+        _ptr(x), _ptr(ws), _nbytes(ws), N, C_i, H_i, W_i, C_o, K_h, K_w, stride, pad_h, pad_w, dilation,
+        _dtype_code(x.dtype), _stream(stream))
+    _check(rc, "conv_im2win_transform_dilated")
+
+
+def conv_im2win_dilated(ws, w, out, N: int, C_i: int, H_i: int, W_i: int, stride: int, dilation: int,
+                        stream=None):
+    """Dilated conv from the dilated window tensor in ``ws``; the precision
+    follows ``w`` (fp32 on the vector ALUs, fp16 / bf16 on the matrix cores);
+    ``H_i``, ``W_i`` are the padded extents the window tensor was built for."""
+    if w.dim() != 4 or not w.is_contiguous() or not out.is_contiguous() or out.dtype != w.dtype:
+        raise ValueError("w must be a contiguous [K_h][K_w][C_i][C_o] tensor, out contiguous of w's dtype")
+    K_h, K_w, C_i2, C_o = w.shape
+    if C_i2 != C_i:
+        raise ValueError("filter has %d input channels, layer has %d" % (C_i2, C_i))
+    rc = load_library().conv_im2win_dilated(_ptr(ws), _nbytes(ws), _ptr(w), _ptr(out), N, C_i, H_i, W_i, C_o,
+                                            K_h, K_w, stride, dilation, _dtype_code(w.dtype), _stream(stream))
+    _check(rc, "conv_im2win_dilated")

@@ -33,26 +33,33 @@ bool mul_ok(int64_t a, int64_t b, int64_t lim, int64_t *out)
 // Shared with the chunked entry points (chunked.cpp).
 namespace im2win {
 
-// Fills `sh` from the user's arguments; returns a status.
-int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_t Kh,
-               int64_t Kw, int64_t s, int dt, Shape *sh)
+// Fills `sh` from the user's arguments (filter dilation d, 1 for none);
+// returns a status.
+int make_shape_dil(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_t Kh,
+                   int64_t Kw, int64_t s, int64_t d, int dt, Shape *sh)
 {
     if (dt != IM2WIN_F32 && dt != IM2WIN_F16 && dt != IM2WIN_BF16)
         return IM2WIN_EINVAL;
-    if (N <= 0 || Ci <= 0 || Hi <= 0 || Wi <= 0 || Co <= 0 || Kh <= 0 || Kw <= 0 || s <= 0)
+    if (N <= 0 || Ci <= 0 || Hi <= 0 || Wi <= 0 || Co <= 0 || Kh <= 0 || Kw <= 0 || s <= 0 || d <= 0)
         return IM2WIN_EINVAL;
-    if (Kh > Hi || Kw > Wi)
-        return IM2WIN_EINVAL;
-    if (Hi > INT32_MAX || Wi > INT32_MAX)  // row and column indices are 32-bit in the kernels
+    if (Hi > INT32_MAX || Wi > INT32_MAX || d > INT32_MAX)  // 32-bit row and column indices in the kernels
         return IM2WIN_ERANGE;
+    // the dilated filter spans (K-1)*d + 1 rows and columns
+    const int64_t Eh = (Kh - 1) * d + 1, Ew = (Kw - 1) * d + 1;
+    if (Kh > Hi || Kw > Wi || Eh > Hi || Ew > Wi)
+        return IM2WIN_EINVAL;
     Shape r;
     memset(&r, 0, sizeof r);
     r.N = N; r.Ci = Ci; r.Hi = Hi; r.Wi = Wi; r.Co = Co; r.Kh = Kh; r.Kw = Kw; r.s = s;
-    r.Ho = (Hi - Kh) / s + 1;
-    r.Wo = (Wi - Kw) / s + 1;
+    r.d = d;
+    r.Ho = (Hi - Eh) / s + 1;
+    r.Wo = (Wi - Ew) / s + 1;
+    // strip columns grouped by residue mod d, Wq per group
+    r.Wq = (Wi + d - 1) / d;
+    r.cols = d * r.Wq;  // < W_i + d <= 2^32
     r.elt = dt == IM2WIN_F32 ? 4 : 2;
     int64_t t;
-    if (!mul_ok(Wi, Kh, kMaxStrip, &t) || !mul_ok(t, Ci, kMaxStrip - 1, &r.L))
+    if (!mul_ok(r.cols, Kh, kMaxStrip, &t) || !mul_ok(t, Ci, kMaxStrip - 1, &r.L))
         return IM2WIN_ERANGE;
     if (!mul_ok(Kh, Kw, kMaxK, &t) || !mul_ok(t, Ci, kMaxK - 1, &r.K))
         return IM2WIN_ERANGE;
@@ -77,6 +84,12 @@ int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_
         return IM2WIN_ERANGE;
     *sh = r;
     return IM2WIN_OK;
+}
+
+int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_t Kh, int64_t Kw,
+               int64_t s, int dt, Shape *sh)
+{
+    return make_shape_dil(N, Ci, Hi, Wi, Co, Kh, Kw, s, 1, dt, sh);
 }
 
 int64_t packed_filter_bytes(const Shape &sh, int dt)
@@ -145,6 +158,83 @@ int launch_status(hipError_t e)
 
 }  // namespace im2win
 
+namespace {
+
+// The transform of the input zero-padded by pad_h / pad_w, for a filter
+// dilated by d (1: none).
+int transform_pad_dil(const void *in_nhwc, void *ws, int64_t ws_bytes, int64_t N, int64_t C_i, int64_t H_i,
+                      int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, int64_t pad_h,
+                      int64_t pad_w, int64_t d, int dt, void *hip_stream)
+{
+    if (!in_nhwc || !ws)
+        return IM2WIN_EINVAL;
+    if (pad_h < 0 || pad_w < 0 || H_i <= 0 || W_i <= 0)
+        return IM2WIN_EINVAL;
+    if (pad_h > INT32_MAX / 4 || pad_w > INT32_MAX / 4 || H_i > INT32_MAX || W_i > INT32_MAX)
+        return IM2WIN_ERANGE;
+    Shape sh;  // the padded layer
+    int rc = make_shape_dil(N, C_i, H_i + 2 * pad_h, W_i + 2 * pad_w, C_o, K_h, K_w, stride, d, dt, &sh);
+    if (rc != IM2WIN_OK)
+        return rc;
+    if (!transform_range_ok(sh))
+        return IM2WIN_ERANGE;
+    if (!aligned16(in_nhwc) || !aligned16(ws))
+        return IM2WIN_EALIGN;
+    int64_t in_bytes;  // the stored input, without the padding
+    if (!mul_ok(N * H_i, W_i * C_i, kMaxBytes / 4, &in_bytes))
+        return IM2WIN_ERANGE;
+    in_bytes *= sh.elt;
+    if (ws_bytes < 0)
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_extent(in_nhwc, in_bytes)) != IM2WIN_OK)
+        return rc;
+    if ((rc = check_extent(ws, ws_bytes)) != IM2WIN_OK)
+        return rc;
+    if (overlaps(in_nhwc, in_bytes, ws, ws_bytes))
+        return IM2WIN_EOVERLAP;
+    if (ws_bytes < workspace_bytes(sh, dt))
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_device()) != IM2WIN_OK)
+        return rc;
+    const Pad pad{H_i, W_i, pad_h, pad_w};
+    return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream, &pad));
+}
+
+// The fp32 convolution on the vector ALUs, filter dilated by d (1: none).
+int conv32(void *ws, int64_t ws_bytes, const float *filt_khkwcico, float *out_nhwc, int64_t N, int64_t C_i,
+           int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, int64_t d,
+           void *hip_stream)
+{
+    if (!ws || !filt_khkwcico || !out_nhwc)
+        return IM2WIN_EINVAL;
+    Shape sh;
+    int rc = make_shape_dil(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, d, IM2WIN_F32, &sh);
+    if (rc != IM2WIN_OK)
+        return rc;
+    if (!aligned16(ws) || !aligned16(filt_khkwcico) || !aligned16(out_nhwc))
+        return IM2WIN_EALIGN;
+    const int64_t f_bytes = sh.K * C_o * 4, o_bytes = sh.P * C_o * 4;
+    if (ws_bytes < 0)
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_extent(ws, ws_bytes)) != IM2WIN_OK ||
+        (rc = check_extent(filt_khkwcico, f_bytes)) != IM2WIN_OK ||
+        (rc = check_extent(out_nhwc, o_bytes)) != IM2WIN_OK)
+        return rc;
+    if (overlaps(ws, ws_bytes, out_nhwc, o_bytes) || overlaps(filt_khkwcico, f_bytes, out_nhwc, o_bytes) ||
+        overlaps(ws, ws_bytes, filt_khkwcico, f_bytes))
+        return IM2WIN_EOVERLAP;
+    if (ws_bytes < workspace_bytes(sh, IM2WIN_F32))
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_device()) != IM2WIN_OK)
+        return rc;
+    void *packed = (char *)ws + sh.pad_end;
+    if ((rc = launch_status(launch_pack_fp32(sh, filt_khkwcico, packed, (hipStream_t)hip_stream))) != IM2WIN_OK)
+        return rc;
+    return launch_status(launch_conv_fp32(sh, ws, packed, out_nhwc, (hipStream_t)hip_stream));
+}
+
+}  // namespace
+
 extern "C" {
 
 int conv_output_dims(int64_t H_i, int64_t W_i, int64_t K_h, int64_t K_w, int64_t stride,
@@ -157,6 +247,33 @@ int conv_output_dims(int64_t H_i, int64_t W_i, int64_t K_h, int64_t K_w, int64_t
     *H_o = (H_i - K_h) / stride + 1;
     *W_o = (W_i - K_w) / stride + 1;
     return IM2WIN_OK;
+}
+
+int conv_output_dims_dilated(int64_t H_i, int64_t W_i, int64_t K_h, int64_t K_w, int64_t stride,
+                             int64_t dilation, int64_t *H_o, int64_t *W_o)
+{
+    if (!H_o || !W_o)
+        return IM2WIN_EINVAL;
+    if (H_i <= 0 || W_i <= 0 || K_h <= 0 || K_w <= 0 || stride <= 0 || dilation <= 0 ||
+        dilation > INT32_MAX || K_h > H_i || K_w > W_i)
+        return IM2WIN_EINVAL;
+    const int64_t Eh = (K_h - 1) * dilation + 1, Ew = (K_w - 1) * dilation + 1;
+    if (Eh > H_i || Ew > W_i)
+        return IM2WIN_EINVAL;
+    *H_o = (H_i - Eh) / stride + 1;
+    *W_o = (W_i - Ew) / stride + 1;
+    return IM2WIN_OK;
+}
+
+int64_t conv_workspace_bytes_dilated(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
+                                     int64_t K_h, int64_t K_w, int64_t stride, int64_t dilation,
+                                     im2win_dtype_t dt)
+{
+    Shape sh;
+    int rc = make_shape_dil(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dilation, (int)dt, &sh);
+    if (rc != IM2WIN_OK)
+        return rc;
+    return workspace_bytes(sh, (int)dt);
 }
 
 int64_t conv_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
@@ -217,70 +334,24 @@ int conv_im2win_transform_padded(const void *in_nhwc, void *ws, int64_t ws_bytes
                                  int64_t K_w, int64_t stride, int64_t pad_h, int64_t pad_w,
                                  im2win_dtype_t dt, void *hip_stream)
 {
-    if (!in_nhwc || !ws)
-        return IM2WIN_EINVAL;
-    if (pad_h < 0 || pad_w < 0 || H_i <= 0 || W_i <= 0)
-        return IM2WIN_EINVAL;
-    if (pad_h > INT32_MAX / 4 || pad_w > INT32_MAX / 4 || H_i > INT32_MAX || W_i > INT32_MAX)
-        return IM2WIN_ERANGE;
-    Shape sh;  // the padded layer
-    int rc = make_shape(N, C_i, H_i + 2 * pad_h, W_i + 2 * pad_w, C_o, K_h, K_w, stride, (int)dt, &sh);
-    if (rc != IM2WIN_OK)
-        return rc;
-    if (!transform_range_ok(sh))
-        return IM2WIN_ERANGE;
-    if (!aligned16(in_nhwc) || !aligned16(ws))
-        return IM2WIN_EALIGN;
-    int64_t in_bytes;  // the stored input, without the padding
-    if (!mul_ok(N * H_i, W_i * C_i, kMaxBytes / 4, &in_bytes))
-        return IM2WIN_ERANGE;
-    in_bytes *= sh.elt;
-    if (ws_bytes < 0)
-        return IM2WIN_EWORKSPACE;
-    if ((rc = check_extent(in_nhwc, in_bytes)) != IM2WIN_OK)
-        return rc;
-    if ((rc = check_extent(ws, ws_bytes)) != IM2WIN_OK)
-        return rc;
-    if (overlaps(in_nhwc, in_bytes, ws, ws_bytes))
-        return IM2WIN_EOVERLAP;
-    if (ws_bytes < workspace_bytes(sh, (int)dt))
-        return IM2WIN_EWORKSPACE;
-    if ((rc = check_device()) != IM2WIN_OK)
-        return rc;
-    const Pad pad{H_i, W_i, pad_h, pad_w};
-    return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream, &pad));
+    return transform_pad_dil(in_nhwc, ws, ws_bytes, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, pad_h, pad_w, 1,
+                             (int)dt, hip_stream);
+}
+
+int conv_im2win_transform_dilated(const void *in_nhwc, void *ws, int64_t ws_bytes, int64_t N, int64_t C_i,
+                                  int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+                                  int64_t stride, int64_t pad_h, int64_t pad_w, int64_t dilation,
+                                  im2win_dtype_t dt, void *hip_stream)
+{
+    return transform_pad_dil(in_nhwc, ws, ws_bytes, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, pad_h, pad_w,
+                             dilation, (int)dt, hip_stream);
 }
 
 int conv_im2win_fp32(void *ws, int64_t ws_bytes, const float *filt_khkwcico,
                      float *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream)
 {
-    if (!ws || !filt_khkwcico || !out_nhwc)
-        return IM2WIN_EINVAL;
-    Shape sh;
-    int rc = make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, IM2WIN_F32, &sh);
-    if (rc != IM2WIN_OK)
-        return rc;
-    if (!aligned16(ws) || !aligned16(filt_khkwcico) || !aligned16(out_nhwc))
-        return IM2WIN_EALIGN;
-    const int64_t f_bytes = sh.K * C_o * 4, o_bytes = sh.P * C_o * 4;
-    if (ws_bytes < 0)
-        return IM2WIN_EWORKSPACE;
-    if ((rc = check_extent(ws, ws_bytes)) != IM2WIN_OK ||
-        (rc = check_extent(filt_khkwcico, f_bytes)) != IM2WIN_OK ||
-        (rc = check_extent(out_nhwc, o_bytes)) != IM2WIN_OK)
-        return rc;
-    if (overlaps(ws, ws_bytes, out_nhwc, o_bytes) || overlaps(filt_khkwcico, f_bytes, out_nhwc, o_bytes) ||
-        overlaps(ws, ws_bytes, filt_khkwcico, f_bytes))
-        return IM2WIN_EOVERLAP;
-    if (ws_bytes < workspace_bytes(sh, IM2WIN_F32))
-        return IM2WIN_EWORKSPACE;
-    if ((rc = check_device()) != IM2WIN_OK)
-        return rc;
-    void *packed = (char *)ws + sh.pad_end;
-    if ((rc = launch_status(launch_pack_fp32(sh, filt_khkwcico, packed, (hipStream_t)hip_stream))) != IM2WIN_OK)
-        return rc;
-    return launch_status(launch_conv_fp32(sh, ws, packed, out_nhwc, (hipStream_t)hip_stream));
+    return conv32(ws, ws_bytes, filt_khkwcico, out_nhwc, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, 1, hip_stream);
 }
 
 }  // extern "C"
@@ -290,12 +361,12 @@ namespace {
 // The 16-bit matrix-core convolution, fp16 or bf16 operands (`dt`, `op`).
 int conv16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico, uint16_t *out_nhwc, int64_t N,
            int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride,
-           void *hip_stream, int dt, Op16 op)
+           int64_t d, void *hip_stream, int dt, Op16 op)
 {
     if (!ws || !filt_khkwcico || !out_nhwc)
         return IM2WIN_EINVAL;
     Shape sh;
-    int rc = make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dt, &sh);
+    int rc = make_shape_dil(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, d, dt, &sh);
     if (rc != IM2WIN_OK)
         return rc;
     if (!aligned16(ws) || !aligned16(filt_khkwcico) || !aligned16(out_nhwc))
@@ -328,7 +399,7 @@ int conv_im2win_fp16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
                      uint16_t *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream)
 {
-    return conv16(ws, ws_bytes, filt_khkwcico, out_nhwc, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, hip_stream,
+    return conv16(ws, ws_bytes, filt_khkwcico, out_nhwc, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, 1, hip_stream,
                   IM2WIN_F16, Op16::F16);
 }
 
@@ -336,8 +407,26 @@ int conv_im2win_bf16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico,
                      uint16_t *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream)
 {
-    return conv16(ws, ws_bytes, filt_khkwcico, out_nhwc, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, hip_stream,
+    return conv16(ws, ws_bytes, filt_khkwcico, out_nhwc, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, 1, hip_stream,
                   IM2WIN_BF16, Op16::BF16);
+}
+
+int conv_im2win_dilated(void *ws, int64_t ws_bytes, const void *filt_khkwcico, void *out_nhwc, int64_t N,
+                        int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+                        int64_t stride, int64_t dilation, im2win_dtype_t dt, void *hip_stream)
+{
+    switch (dt) {
+    case IM2WIN_F32:
+        return conv32(ws, ws_bytes, static_cast<const float *>(filt_khkwcico), static_cast<float *>(out_nhwc), N,
+                      C_i, H_i, W_i, C_o, K_h, K_w, stride, dilation, hip_stream);
+    case IM2WIN_F16:
+    case IM2WIN_BF16:
+        return conv16(ws, ws_bytes, static_cast<const uint16_t *>(filt_khkwcico),
+                      static_cast<uint16_t *>(out_nhwc), N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dilation,
+                      hip_stream, (int)dt, dt == IM2WIN_BF16 ? Op16::BF16 : Op16::F16);
+    default:
+        return IM2WIN_EINVAL;
+    }
 }
 
 const char *conv_im2win_strerror(int status)

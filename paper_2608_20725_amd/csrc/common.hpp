@@ -55,9 +55,37 @@ struct Shape {
     int64_t K_pad32;    // packed fp32 filter rows (taps)
     int64_t Co_pad32;   // packed fp32 filter columns (channels)
     int64_t Tp;         // K_h*C_i rounded up to 64 (fp16 per-column filter slices)
+    int64_t d;          // filter dilation (1: none)
+    int64_t Wq;         // strip columns per residue group mod d (W_i when d = 1)
+    int64_t cols;       // strip columns d*Wq (>= W_i; the extra ones are zero filler)
 };
 
 inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+// Where the window of output column n starts inside its strip, in elements.
+// Undilated (Eq. 3): n*s columns of T = K_h*C_i elements.  With filter
+// dilation d the strip holds its columns grouped by residue mod d, Wq per
+// group, so the window's columns n*s + v*d are the K_w consecutive ones from
+// ((n*s) mod d)*Wq + floor(n*s/d) on.
+struct WinCols {
+    uint32_t s, d, Wq, T;
+    FastDiv div_d;
+
+    __host__ __device__ inline uint32_t start(uint32_t n) const
+    {
+        const uint32_t c = n * s;
+        if (d == 1)
+            return c * T;
+        const uint32_t g = fdiv(c, div_d);
+        return ((c - g * d) * Wq + g) * T;
+    }
+};
+
+inline WinCols make_wincols(const Shape &sh)
+{
+    return WinCols{(uint32_t)sh.s, (uint32_t)sh.d, (uint32_t)sh.Wq, (uint32_t)(sh.Kh * sh.Ci),
+                   make_fastdiv((uint32_t)sh.d)};
+}
 
 // Raw buffer resource (gfx9 family): base, no swizzle, num_records bytes.
 // Loads whose byte offset falls outside [0, num_records) return zero and
@@ -99,6 +127,9 @@ __device__ inline uint32_t ld_b16(__amdgpu_buffer_rsrc_t r, uint32_t off)
 namespace im2win {
 int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_t Kh, int64_t Kw,
                int64_t s, int dt, Shape *sh);
+// The same with filter dilation d >= 1.
+int make_shape_dil(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_t Kh, int64_t Kw,
+                   int64_t s, int64_t d, int dt, Shape *sh);
 int64_t packed_filter_bytes(const Shape &sh, int dt);
 bool aligned16(const void *p);
 bool overlaps(const void *a, int64_t na, const void *b, int64_t nb);

@@ -43,7 +43,8 @@ struct C16Args {
     const uint16_t *packed;  // F' [Co_pad][K_pad]
     uint16_t *out;
     uint64_t win_bytes;
-    uint32_t P, K, K_pad, Co, Co_pad, Wo, L, S;
+    uint32_t P, K, K_pad, Co, Co_pad, Wo, L;
+    WinCols wc;              // window start of an output column in its strip
     uint32_t pk_bytes;       // bytes of the packed filter
     FastDiv div_Wo;
 };
@@ -252,7 +253,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
         uint32_t off = 0;
         if (p < a.P) {
             const uint32_t q = fdiv(p, a.div_Wo);
-            off = (q - q0) * a.L + (p - q * a.Wo) * a.S;
+            off = (q - q0) * a.L + a.wc.start(p - q * a.Wo);
         }
         rowoff[t] = off;
     }
@@ -492,7 +493,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
         uint32_t off = 0;
         if (p < a.P) {
             const uint32_t q = fdiv(p, a.div_Wo);
-            off = (q - q0) * a.L + (p - q * a.Wo) * a.S;
+            off = (q - q0) * a.L + a.wc.start(p - q * a.Wo);
         }
         rowoff[t] = off;
     }
@@ -673,7 +674,7 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
     a.P = (uint32_t)sh.P; a.K = (uint32_t)sh.K; a.K_pad = (uint32_t)sh.K_pad;
     a.Co_pad = (uint32_t)sh.Co_pad;
     a.pk_bytes = (uint32_t)(sh.Co_pad * sh.K_pad * 2);  // < 2^31 (checked with the shape)
-    a.Co = (uint32_t)sh.Co; a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.S = (uint32_t)sh.S;
+    a.Co = (uint32_t)sh.Co; a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.wc = make_wincols(sh);
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     void *args[] = {&a};
     // every window starts on a 16-byte boundary (unless the register-staged

@@ -387,6 +387,8 @@ int col_plan(const Shape &sh)
 {
     if (sh.Ci % 8 != 0)
         return -1;  // windows not 16-byte aligned
+    if (sh.d != 1)
+        return -1;  // the column table assumes consecutive strip columns
     if (const char *e = getenv("IM2WIN_FP16_KERNEL"))
         if (strcmp(e, "pipe") == 0 || strcmp(e, "regs") == 0)
             return -1;

@@ -301,6 +301,8 @@ int seg_plan(const Shape &sh)
 {
     if (sh.Ci % 8 == 0)
         return -1;  // 16-byte-aligned windows have their own kernels
+    if (sh.d != 1)
+        return -1;  // strip segments assume windows s*K_h*C_i apart
     if (const char *e = getenv("IM2WIN_FP16_KERNEL"))
         if (strcmp(e, "regs") == 0)
             return -1;

@@ -41,7 +41,8 @@ struct C32Args {
     const float *packed;  // F' [K_pad32][Co_pad32]
     float *out;
     uint64_t win_bytes;
-    uint32_t P, K, K_pad, Co, Co_pad, Wo, L, S;
+    uint32_t P, K, K_pad, Co, Co_pad, Wo, L;
+    WinCols wc;              // window start of an output column in its strip
     FastDiv div_Wo;
 };
 
@@ -355,7 +356,7 @@ __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
         uint32_t off = 0;
         if (p < a.P) {
             const uint32_t q = fdiv(p, a.div_Wo);
-            off = (q - q0) * a.L + (p - q * a.Wo) * a.S;
+            off = (q - q0) * a.L + a.wc.start(p - q * a.Wo);
         }
         rowoff[t] = off;
     }
@@ -505,7 +506,7 @@ hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed,
     a.win_bytes = (uint64_t)sh.win_bytes;
     a.P = (uint32_t)sh.P; a.K = (uint32_t)sh.K; a.K_pad = (uint32_t)sh.K_pad32;
     a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
-    a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.S = (uint32_t)sh.S;
+    a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.wc = make_wincols(sh);
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
 
     const int ntiles = (int)(sizeof kTiles / sizeof kTiles[0]);

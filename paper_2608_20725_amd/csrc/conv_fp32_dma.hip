@@ -42,7 +42,8 @@ struct D32Args {
     const float *packed;  // F' [K_pad32][Co_pad32]
     float *out;
     uint64_t win_bytes;
-    uint32_t P, K, K_pad, Co, Co_pad, Wo, L, S;
+    uint32_t P, K, K_pad, Co, Co_pad, Wo, L;
+    WinCols wc;              // window start of an output column in its strip
     FastDiv div_Wo;
 };
 
@@ -264,7 +265,7 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
         w.woff[i] = kOOB;
         if (p < a.P) {
             const uint32_t q = fdiv(p, a.div_Wo);
-            w.woff[i] = ((q - q0) * a.L + (p - q * a.Wo) * a.S + w.wk) * 4u;
+            w.woff[i] = ((q - q0) * a.L + a.wc.start(p - q * a.Wo) + w.wk) * 4u;
         }
     }
     // Filter load i fills taps 4*b .. 4*b+3 of the slab (b = wave + 4i): lane
@@ -477,7 +478,7 @@ hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const void *ws, const
     a.win_bytes = (uint64_t)sh.win_bytes;
     a.P = (uint32_t)sh.P; a.K = (uint32_t)sh.K; a.K_pad = (uint32_t)sh.K_pad32;
     a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
-    a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.S = (uint32_t)sh.S;
+    a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.wc = make_wincols(sh);
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     void *args[] = {&a};
     dim3 grid((uint32_t)((sh.P + v.bm - 1) / v.bm), (uint32_t)((sh.Co + v.cw - 1) / v.cw));

@@ -33,7 +33,8 @@ struct TArgs {
     const char *in;
     char *ws;
     uint32_t Ci, Hi, Wi, Kh, s, Ho;  // Hi x Wi: the stored (unpadded) input
-    uint32_t Wp, ph, pw;             // strip columns Wi + 2*pw; zero rows / columns per side
+    uint32_t Wp, ph, pw;             // padded width Wi + 2*pw; zero rows / columns per side
+    uint32_t d, Wq, cols;            // dilation; strip columns per residue group; d*Wq columns
     uint32_t L;              // strip length (elements)
     uint32_t strips;
     uint32_t gran_per_strip; // vec: 16-byte granules per strip
@@ -41,8 +42,20 @@ struct TArgs {
     uint64_t win_bytes, pad_end;
     uint64_t grans;          // gather: 16-byte granules of the window tensor
     uint32_t xcd_order;      // vec: 1 = XCD-aware block order, 0 = linear (ablation)
-    FastDiv div_Ci, div_Kh, div_Wi, div_Ho, div_L, div_gps;
+    FastDiv div_Ci, div_Kh, div_Wi, div_Ho, div_L, div_gps, div_Wq;
 };
+
+// Padded-input column held by strip column position k: k itself, or with
+// dilation d (columns grouped by residue mod d, Wq per group) column
+// (k mod Wq)*d + floor(k/Wq); positions past the padded width are filler and
+// map to columns >= Wp, outside the stored input like the right-hand padding.
+__device__ inline uint32_t strip_col(uint32_t k, const TArgs &a)
+{
+    if (a.d == 1)
+        return k;
+    const uint32_t g = fdiv(k, a.div_Wq);
+    return (k - g * a.Wq) * a.d + g;
+}
 
 __device__ inline void zero_pad(const TArgs &a)
 {
@@ -88,7 +101,8 @@ __global__ __launch_bounds__(kThreads) void transform_vec(TArgs a)
             const uint32_t u = seg - k * a.Kh;
             // a granule lies inside one (column, row) piece of C_i elements:
             // all of it is padding or none
-            const int32_t h = (int32_t)(m * a.s + u) - (int32_t)a.ph, w = (int32_t)k - (int32_t)a.pw;
+            const int32_t h = (int32_t)(m * a.s + u * a.d) - (int32_t)a.ph;
+            const int32_t w = (int32_t)strip_col(k, a) - (int32_t)a.pw;
             uint4 v = make_uint4(0u, 0u, 0u, 0u);
             if (h >= 0 && h < (int32_t)a.Hi && w >= 0 && w < (int32_t)a.Wi) {
                 const uint64_t src = (((uint64_t)i * a.Hi + (uint32_t)h) * a.Wi + (uint32_t)w) * a.Ci + r;
@@ -133,7 +147,8 @@ __global__ __launch_bounds__(kThreads) void transform_gather(TArgs a)
 #pragma unroll
     for (uint32_t t = 0; t < V; ++t) {
         if ((uint64_t)e + t < a.win_elems) {
-            const int32_t hh = (int32_t)(m * a.s + u) - (int32_t)a.ph, ww = (int32_t)k - (int32_t)a.pw;
+            const int32_t hh = (int32_t)(m * a.s + u * a.d) - (int32_t)a.ph;
+            const int32_t ww = (int32_t)strip_col(k, a) - (int32_t)a.pw;
             uint32_t bits = 0;
             if (hh >= 0 && hh < (int32_t)a.Hi && ww >= 0 && ww < (int32_t)a.Wi) {
                 const uint64_t src = (((uint64_t)i * a.Hi + (uint32_t)hh) * a.Wi + (uint32_t)ww) * a.Ci + r;
@@ -148,7 +163,7 @@ __global__ __launch_bounds__(kThreads) void transform_gather(TArgs a)
                 r = 0;
                 if (++u == a.Kh) {
                     u = 0;
-                    if (++k == a.Wp) {
+                    if (++k == a.cols) {
                         k = 0;
                         if (++m == a.Ho) {
                             m = 0;
@@ -197,6 +212,10 @@ hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream
     a.div_Wi = make_fastdiv((uint32_t)sh.Wi);
     a.div_Ho = make_fastdiv((uint32_t)sh.Ho);
     a.div_L = make_fastdiv((uint32_t)sh.L);
+    a.d = (uint32_t)sh.d;
+    a.Wq = (uint32_t)sh.Wq;
+    a.cols = (uint32_t)sh.cols;
+    a.div_Wq = make_fastdiv((uint32_t)sh.Wq);
     // IM2WIN_TRANSFORM_ORDER=linear deals blocks in launch order (to measure
     // what the XCD-aware order gains)
     const char *order = getenv("IM2WIN_TRANSFORM_ORDER");

@@ -219,3 +219,56 @@ def test_padded_transform_checks(lib):
     # a filter that fits only thanks to the padding passes the dims: the
     # misaligned input is what is rejected
     assert f(v(0x1008), v(0x100000), 1 << 20, 1, 3, 2, 2, 4, 3, 3, 1, 1, 1, pkg.F32, None) == EALIGN
+
+
+@pytest.mark.parametrize("args", [
+    # N, C_i, H, W, C_o, K_h, K_w, s, d
+    (2, 3, 9, 10, 4, 3, 3, 1, 2), (1, 2, 11, 9, 3, 3, 2, 2, 3), (2, 4, 8, 8, 2, 2, 2, 1, 4),
+    (1, 1, 7, 13, 2, 3, 3, 3, 2), (1, 64, 60, 60, 64, 3, 3, 1, 2), (3, 5, 13, 13, 8, 2, 2, 1, 12),
+])
+def test_dilated_workspace_and_dims(lib, orc, args):
+    """The dilated window tensor is the oracle's (residue-grouped strips of
+    d*ceil(W/d) columns); workspace = its bytes, the zero pad and the packed
+    filter; output extents (H - (K-1)d - 1)/s + 1."""
+    import numpy as np
+    N, Ci, H, W, Co, Kh, Kw, s, d = args
+    for dt, elt in ((pkg.F32, 4), (pkg.F16, 2), (pkg.BF16, 2)):
+        win = orc.im2win_dil(np.zeros((N, H, W, Ci), np.float32 if elt == 4 else np.float16), Kh, s, 0, 0, d)
+        Ho, Wo = pkg.conv_output_dims_dilated(H, W, Kh, Kw, s, d)
+        assert (Ho, Wo) == (orc.dil_extent(H, Kh, s, d), orc.dil_extent(W, Kw, s, d))
+        assert win.shape[1] == Ho
+        pad_end = (win.nbytes + 255) // 256 * 256 + 256
+        K = Kh * Kw * Ci
+        if dt == pkg.F32:
+            packed = ((K + 15) // 16 * 16) * ((Co + 31) // 32 * 32) * 4
+        else:
+            packed = ((Co + 255) // 256 * 256) * Kw * ((Kh * Ci + 63) // 64 * 64) * 2
+        assert pkg.conv_workspace_bytes_dilated(N, Ci, H, W, Co, Kh, Kw, s, d, dt) == pad_end + packed
+        if d == 1:
+            assert pkg.conv_workspace_bytes_dilated(N, Ci, H, W, Co, Kh, Kw, s, 1, dt) == \
+                pkg.conv_workspace_bytes(N, Ci, H, W, Co, Kh, Kw, s, dt)
+
+
+def test_dilated_rejects(lib):
+    v = ctypes.c_void_p
+    ho, wo = ctypes.c_int64(), ctypes.c_int64()
+    # dilation < 1, dilated filter larger than the input
+    assert lib.conv_output_dims_dilated(8, 8, 3, 3, 1, 0, ctypes.byref(ho), ctypes.byref(wo)) == EINVAL
+    assert lib.conv_output_dims_dilated(8, 8, 3, 3, 1, 4, ctypes.byref(ho), ctypes.byref(wo)) == EINVAL
+    assert lib.conv_output_dims_dilated(9, 9, 3, 3, 1, 4, ctypes.byref(ho), ctypes.byref(wo)) == OK
+    assert (ho.value, wo.value) == (1, 1)
+    assert lib.conv_workspace_bytes_dilated(1, 3, 8, 8, 4, 3, 3, 1, 0, pkg.F32) == EINVAL
+    assert lib.conv_workspace_bytes_dilated(1, 3, 8, 8, 4, 3, 3, 1, 4, pkg.F32) == EINVAL
+    assert lib.conv_workspace_bytes_dilated(1, 3, 8, 8, 4, 3, 3, 1, 1 << 40, pkg.F32) == ERANGE
+    # null pointers first, bad dtype, bad dims before any pointer is resolved
+    assert lib.conv_im2win_dilated(None, 1 << 20, v(512), v(768), 1, 3, 8, 8, 4, 3, 3, 1, 2, pkg.F32,
+                                   None) == EINVAL
+    assert lib.conv_im2win_dilated(v(256), 1 << 20, v(512), v(768), 1, 3, 8, 8, 4, 3, 3, 1, 2, 7, None) == EINVAL
+    assert lib.conv_im2win_dilated(v(0x100000), 1 << 20, v(0x2000), v(0x3000), 1, 3, 8, 8, 4, 3, 3, 1, 4,
+                                   pkg.F16, None) == EINVAL
+    assert lib.conv_im2win_transform_dilated(None, v(256), 1 << 20, 1, 3, 8, 8, 4, 3, 3, 1, 0, 0, 2, 0,
+                                             None) == EINVAL
+    assert lib.conv_im2win_transform_dilated(v(0x1000), v(0x100000), 1 << 20, 1, 3, 8, 8, 4, 3, 3, 1, 0, 0, 0,
+                                             0, None) == EINVAL
+    assert lib.conv_im2win_transform_dilated(v(0x1008), v(0x100000), 1 << 20, 1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 2,
+                                             0, None) == EALIGN
