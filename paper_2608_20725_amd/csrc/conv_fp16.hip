@@ -404,27 +404,41 @@ struct Pipe {
         }
     }
 
+    // Fragments of k-step ks of the stage.
+    __device__ inline void frags(const char *stage, int ks, v8 (&af)[WM], v8 (&bf)[WN])
+    {
+        const uint32_t ch = 2 * ks + (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < WM; ++i) {
+            const uint32_t r = arow + 32 * i;
+            af[i] = *reinterpret_cast<const v8 *>(stage + r * 128 + 16u * (ch ^ rsw(r)));
+        }
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+            const uint32_t r = brow + 32 * j;
+            bf[j] = *reinterpret_cast<const v8 *>(stage + r * 128 + 16u * (ch ^ rsw(r)));
+        }
+    }
+
+    // All k-steps of one stage; the fragments of step ks+1 are read before
+    // the matrix operations of step ks, so their LDS latency runs under them
+    // (with about one wave per SIMD nothing else would hide it).
     __device__ inline void compute(const char *stage)
     {
+        v8 af[2][WM], bf[2][WN];
+        frags(stage, 0, af[0], bf[0]);
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
-            const uint32_t ch = 2 * ks + (lane >> 5);
-            v8 af[WM], bf[WN];
-#pragma unroll
-            for (int i = 0; i < WM; ++i) {
-                const uint32_t r = arow + 32 * i;
-                af[i] = *reinterpret_cast<const v8 *>(stage + r * 128 + 16u * (ch ^ rsw(r)));
-            }
-#pragma unroll
-            for (int j = 0; j < WN; ++j) {
-                const uint32_t r = brow + 32 * j;
-                bf[j] = *reinterpret_cast<const v8 *>(stage + r * 128 + 16u * (ch ^ rsw(r)));
-            }
+            if (ks + 1 < BK / 16)
+                frags(stage, ks + 1, af[(ks + 1) & 1], bf[(ks + 1) & 1]);
+            // keep the reads above the matrix operations (the scheduler would
+            // otherwise sink them below to reuse the same registers)
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int i = 0; i < WM; ++i)
 #pragma unroll
                 for (int j = 0; j < WN; ++j)
-                    acc[i][j] = E::mfma(af[i], bf[j], acc[i][j]);
+                    acc[i][j] = E::mfma(af[ks & 1][i], bf[ks & 1][j], acc[i][j]);
         }
     }
 
@@ -612,11 +626,12 @@ const PipeVariant *pipe_variants(int *n)
 }  // namespace
 
 // Layers with C_o >= 128 and at least four 128 x 128 tiles per CU run the
-// row-per-pixel kernel with a one-slot ring: 32 KiB of LDS per workgroup lets
-// four workgroups share a CU, which keeps more stage bytes in flight per CU
-// than two double-buffered ones (measured, alternating runs: S7 639 vs 601
-// TFLOP/s with the column-staged kernel, S12 591 vs 547).  With fewer tiles the
-// workgroups' own double buffering wins (S5, S10).
+// row-per-pixel kernel with a one-slot ring.  Registers (about 200 per wave)
+// hold both ring depths to two workgroups per CU; with one slot each
+// workgroup alternates whole stages of loading and multiplying, and the two
+// on a CU interleave.  Measured faster there (alternating runs: S7 639 vs
+// 601 TFLOP/s with the column-staged kernel, S12 591 vs 547); with fewer
+// tiles the two-slot ring wins (S5, S10).
 bool fp16_single_slot_rows(const Shape &sh)
 {
     const int64_t tiles = ((sh.P + 127) / 128) * ((sh.Co + 127) / 128);
