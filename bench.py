@@ -16,9 +16,10 @@ Prints ONE JSON line.  `--layer NAME` picks another configured layer and
 `--ablation LAYERS` times the path with each of the paper's techniques
 switched off (Sec. IV-D) on the named layers.  Each
 line also carries a `bf16` block (the same layer with bf16 operands on the
-same matrix-core kernels) and a `dilated` block (the layer with filter
-dilation 2 and 'same' padding, fp32 and fp16), both timed outside the step
-(extensions of the path).
+same matrix-core kernels), an `fp32_mfma` block (the alternate fp32 path on
+the matrix cores) and a `dilated` block (the layer with filter dilation 2 and
+'same' padding, fp32 and fp16), all timed outside the step (extensions of the
+path).
 """
 from __future__ import annotations
 
@@ -35,7 +36,7 @@ if ROOT not in sys.path:
 
 # MI355X published peaks
 PEAK_HBM_GBS = 8000.0
-PEAK_FP32_VECTOR_TF = 157.3     # 256 CU x 256 flop/clk x 2.4 GHz
+PEAK_FP32_VECTOR_TF = 157.3     # 256 CU x 256 flop/clk x 2.4 GHz (fp32 MFMA dense: the same)
 PEAK_FP16_MFMA_TF = 2516.6      # dense (bf16 the same)
 
 # HBM-side bytes per launch of the fp32 conv kernel, from rocprofv3 FETCH_SIZE and
@@ -138,6 +139,35 @@ def measure_minibatch(l, paths, pkg, torch, n_chunk=32, reps=10):
                      "full_batch_workspace_bytes": p.ws.numel()}
         del ws
     return res
+
+
+def measure_fp32_mfma(l, x, w, pkg, torch, reps=20):
+    """The alternate fp32 path on the matrix cores (v_mfma_f32_32x32x2_f32) on
+    the same layer, outside the timed step: median pack+conv time over `reps`
+    runs, HIP events on the launch stream (layers with C_i not a multiple of
+    4 run the vector-ALU kernel there)."""
+    p = Path(l, x, w, torch.float32, pkg, torch)
+    p.conv = pkg.conv_im2win_fp32_mfma
+    p.transform()
+    for _ in range(3):
+        p.run_conv()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        p.run_conv()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ts.sort()
+    Ho, Wo = pkg.conv_output_dims(l.H, l.W, l.K_h, l.K_w, l.stride)
+    flops = 2.0 * l.N * Ho * Wo * l.C_o * l.K_h * l.K_w * l.C_i
+    ms = ts[reps // 2]
+    del p
+    return {"pack_conv_ms": round(ms, 5), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 3),
+            "frac_fp32_mfma": round(flops / (ms * 1e-3) / 1e12 / PEAK_FP32_VECTOR_TF, 4),
+            "on_matrix_cores": l.C_i % 4 == 0}
 
 
 def measure_bf16(l, x, w, pkg, torch, reps=20):
@@ -474,6 +504,7 @@ def main():
             },
         }
         rec["bf16"] = measure_bf16(l, x, w, pkg, torch)
+        rec["fp32_mfma"] = measure_fp32_mfma(l, x, w, pkg, torch)
         rec["dilated"] = measure_dilated(l, x, w, pkg, torch)
         if not args.sweep:
             mb = measure_minibatch(l, paths, pkg, torch)

@@ -31,8 +31,10 @@
  *                             K_pad = round_up(K, 64) taps or one slice of T_pad taps
  *                             per filter column; TB depends on the kernel the layer
  *                             runs (an internal layout, rewritten by every conv call)
- *                       fp32: [K_pad32][C_o_pad32] fp32, K_pad32 = round_up(K, 16),
- *                             C_o_pad32 = round_up(C_o, 32)
+ *                       fp32: the larger of [K_pad32][C_o_pad32] fp32, K_pad32 =
+ *                             round_up(K, 16), C_o_pad32 = round_up(C_o, 32) (vector-ALU
+ *                             kernels) and round_up(C_o, 128)*round_up(K, 32) fp32
+ *                             (conv_im2win_fp32_mfma)
  *
  * Scope: one stride and one dilation for both axes; zero padding and dilation
  * through the *_padded / *_dilated calls below; no groups or bias.
@@ -161,6 +163,21 @@ int conv_im2win_transform_padded(const void *in_nhwc, void *ws, int64_t ws_bytes
 int conv_im2win_fp32(void *ws, int64_t ws_bytes, const float *filt_khkwcico,
                      float *out_nhwc, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream);
+
+/*
+ * fp32 windowed convolution on the matrix cores: the sums of
+ * conv_im2win_fp32 computed as the product of Alg. 1 (M = C_o by N =
+ * N*H_o*W_o over K = C_i*K_h*K_w) with v_mfma_f32_32x32x2_f32, fp32 operands
+ * and fp32 accumulation.  An alternate fp32 path (the paper's fp32 variant
+ * runs on the vector units, Sec. III-F).  Arguments, workspace, buffer rules
+ * and errors as for conv_im2win_fp32.  Results meet the same bound; the
+ * order of the fp32 additions differs from the vector-ALU kernel's, so the
+ * bits may differ.  Layers whose C_i is not a multiple of 4 (windows not made
+ * of whole 16-byte chunks) run the vector-ALU kernel instead.
+ */
+int conv_im2win_fp32_mfma(void *ws, int64_t ws_bytes, const float *filt_khkwcico, float *out_nhwc, int64_t N,
+                          int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+                          int64_t stride, void *hip_stream);
 
 /*
  * fp16 windowed convolution on the matrix cores (Sec. III-D, Alg. 1: the

@@ -12,6 +12,7 @@ kernels; there is no fallback, and a missing library raises.
     conv_im2win_fp32(ws, w, out, N, C_i, H_i, W_i, stride)     # Sec. III-C, Eq. 3
     conv_im2win_fp16(ws, w, out, N, C_i, H_i, W_i, stride)     # Sec. III-D, Alg. 1
     conv_im2win_bf16(ws, w, out, N, C_i, H_i, W_i, stride)     # same, bf16 operands
+    conv_im2win_fp32_mfma(ws, w, out, N, C_i, H_i, W_i, stride)  # fp32 on the matrix cores
     conv_im2win_transform_dilated(x, ws, C_o, K_h, K_w, stride, pad_h, pad_w, dilation)
     conv_im2win_dilated(ws, w, out, N, C_i, H_p, W_p, stride, dilation)
 
@@ -27,7 +28,7 @@ __all__ = [
     "Im2winError", "load_library", "library_path", "F32", "F16", "BF16",
     "conv_output_dims", "conv_workspace_bytes", "conv_im2col_bytes",
     "conv_im2win_transform", "conv_im2win_transform_padded", "conv_im2win_fp32", "conv_im2win_fp16",
-    "conv_im2win_bf16", "conv_output_dims_dilated", "conv_workspace_bytes_dilated",
+    "conv_im2win_bf16", "conv_im2win_fp32_mfma", "conv_output_dims_dilated", "conv_workspace_bytes_dilated",
     "conv_im2win_transform_dilated", "conv_im2win_dilated",
     "conv_im2win_strerror", "im2win_conv2d",
 ]
@@ -79,6 +80,8 @@ def load_library():
     lib.conv_im2win_fp16.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
     lib.conv_im2win_bf16.restype = ctypes.c_int
     lib.conv_im2win_bf16.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
+    lib.conv_im2win_fp32_mfma.restype = ctypes.c_int
+    lib.conv_im2win_fp32_mfma.argtypes = [_vp, _i64, _vp, _vp] + [_i64] * 8 + [_vp]
     lib.conv_output_dims_dilated.restype = ctypes.c_int
     lib.conv_output_dims_dilated.argtypes = [_i64] * 6 + [ctypes.POINTER(_i64)] * 2
     lib.conv_workspace_bytes_dilated.restype = _i64
@@ -216,6 +219,17 @@ def conv_im2win_bf16(ws, w, out, N: int, C_i: int, H_i: int, W_i: int, stride: i
     if w.dtype != torch.bfloat16 or out.dtype != torch.bfloat16:
         raise TypeError("conv_im2win_bf16 takes bf16 filter and output")
     _conv(load_library().conv_im2win_bf16, "conv_im2win_bf16", ws, w, out, N, C_i, H_i, W_i,
+          stride, stream)
+
+
+def conv_im2win_fp32_mfma(ws, w, out, N: int, C_i: int, H_i: int, W_i: int, stride: int, stream=None):
+    """fp32 conv on the matrix cores (an alternate fp32 path) from the fp32
+    window tensor in ``ws``; layers with C_i not a multiple of 4 run on the
+    vector ALUs."""
+    import torch
+    if w.dtype != torch.float32 or out.dtype != torch.float32:
+        raise TypeError("conv_im2win_fp32_mfma takes fp32 filter and output")
+    _conv(load_library().conv_im2win_fp32_mfma, "conv_im2win_fp32_mfma", ws, w, out, N, C_i, H_i, W_i,
           stride, stream)
 
 

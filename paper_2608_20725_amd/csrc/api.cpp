@@ -94,8 +94,13 @@ int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_
 
 int64_t packed_filter_bytes(const Shape &sh, int dt)
 {
-    // fp16 / bf16: room for every packed layout (C_o_pad*K_pad <= C_o_pad*K_w*Tp)
-    return dt != IM2WIN_F32 ? sh.Co_pad * sh.Kw * sh.Tp * 2 : sh.K_pad32 * sh.Co_pad32 * 4;
+    // fp16 / bf16: room for every packed layout (C_o_pad*K_pad <= C_o_pad*K_w*Tp);
+    // fp32: the vector-ALU layout [K_pad32][C_o_pad32] or the matrix-core one
+    // [K/32][C_o_pad][32], whichever is larger
+    if (dt != IM2WIN_F32)
+        return sh.Co_pad * sh.Kw * sh.Tp * 2;
+    const int64_t valu = sh.K_pad32 * sh.Co_pad32 * 4, mfma = fp32_mfma_packed_bytes(sh);
+    return valu > mfma ? valu : mfma;
 }
 
 int64_t workspace_bytes(const Shape &sh, int dt) { return sh.pad_end + packed_filter_bytes(sh, dt); }
@@ -200,10 +205,11 @@ int transform_pad_dil(const void *in_nhwc, void *ws, int64_t ws_bytes, int64_t N
     return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream, &pad));
 }
 
-// The fp32 convolution on the vector ALUs, filter dilated by d (1: none).
+// The fp32 convolution, filter dilated by d (1: none): on the vector ALUs,
+// or on the matrix cores when `mfma` is set and the layer allows it.
 int conv32(void *ws, int64_t ws_bytes, const float *filt_khkwcico, float *out_nhwc, int64_t N, int64_t C_i,
            int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, int64_t d,
-           void *hip_stream)
+           void *hip_stream, bool mfma = false)
 {
     if (!ws || !filt_khkwcico || !out_nhwc)
         return IM2WIN_EINVAL;
@@ -228,6 +234,8 @@ int conv32(void *ws, int64_t ws_bytes, const float *filt_khkwcico, float *out_nh
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
     void *packed = (char *)ws + sh.pad_end;
+    if (mfma && fp32_mfma_ok(sh))
+        return launch_status(launch_conv_fp32_mfma(sh, filt_khkwcico, packed, out_nhwc, ws, (hipStream_t)hip_stream));
     if ((rc = launch_status(launch_pack_fp32(sh, filt_khkwcico, packed, (hipStream_t)hip_stream))) != IM2WIN_OK)
         return rc;
     return launch_status(launch_conv_fp32(sh, ws, packed, out_nhwc, (hipStream_t)hip_stream));
@@ -352,6 +360,14 @@ int conv_im2win_fp32(void *ws, int64_t ws_bytes, const float *filt_khkwcico,
                      int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, void *hip_stream)
 {
     return conv32(ws, ws_bytes, filt_khkwcico, out_nhwc, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, 1, hip_stream);
+}
+
+int conv_im2win_fp32_mfma(void *ws, int64_t ws_bytes, const float *filt_khkwcico, float *out_nhwc, int64_t N,
+                          int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+                          int64_t stride, void *hip_stream)
+{
+    return conv32(ws, ws_bytes, filt_khkwcico, out_nhwc, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, 1, hip_stream,
+                  true);
 }
 
 }  // extern "C"

@@ -154,6 +154,13 @@ hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream
 hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hipStream_t st);
 hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed, float *out,
                             hipStream_t st);
+// fp32 on the matrix cores: whether the layer can run there (C_i a multiple
+// of 4, offsets in range), the bytes of its packed filter, and the launch
+// (filter pack, then conv).
+bool fp32_mfma_ok(const Shape &sh);
+int64_t fp32_mfma_packed_bytes(const Shape &sh);
+hipError_t launch_conv_fp32_mfma(const Shape &sh, const float *filt, void *packed, float *out, const void *ws,
+                                 hipStream_t st);
 // fp32 kernel with stages loaded straight into LDS: the variant for this
 // layer, or -1 when the register-staged kernel runs instead.
 int dma32_plan(const Shape &sh);

@@ -60,8 +60,10 @@ def _closed_form(l, elt, fp16):
     if fp16:   # packed filter round_up(C_o,256) x K_w x round_up(K_h*C_i,64) fp16
         packed = ((l.C_o + 255) // 256 * 256) * l.K_w * ((l.K_h * l.C_i + 63) // 64 * 64) * 2
         assert packed >= ((l.C_o + 255) // 256 * 256) * ((K + 63) // 64 * 64) * 2
-    else:      # packed filter [round_up(K,16)][round_up(C_o,32)] fp32
-        packed = ((K + 15) // 16 * 16) * ((l.C_o + 31) // 32 * 32) * 4
+    else:      # packed filter: the larger of [round_up(K,16)][round_up(C_o,32)] fp32 (vector-ALU
+               # kernels) and round_up(C_o,128) x round_up(K,32) fp32 (matrix-core kernel)
+        packed = max(((K + 15) // 16 * 16) * ((l.C_o + 31) // 32 * 32),
+                     ((l.C_o + 127) // 128 * 128) * ((K + 31) // 32 * 32)) * 4
     im2col = l.N * Ho * Wo * K * elt
     return pad_end + packed, im2col, win
 
@@ -150,6 +152,8 @@ def test_misaligned_pointers_rejected(lib):
                                 None) == EALIGN
     assert lib.conv_im2win_bf16(v(0x100008), 1 << 20, v(0x2000), v(0x3000), 1, 3, 8, 8, 4, 3, 3, 1,
                                 None) == EALIGN
+    assert lib.conv_im2win_fp32_mfma(v(0x100000), 1 << 20, v(0x2004), v(0x3000), 1, 3, 8, 8, 4, 3, 3, 1,
+                                     None) == EALIGN
 
 
 def test_dims_checked_before_pointers_resolve(lib):
@@ -240,7 +244,7 @@ def test_dilated_workspace_and_dims(lib, orc, args):
         pad_end = (win.nbytes + 255) // 256 * 256 + 256
         K = Kh * Kw * Ci
         if dt == pkg.F32:
-            packed = ((K + 15) // 16 * 16) * ((Co + 31) // 32 * 32) * 4
+            packed = max(((K + 15) // 16 * 16) * ((Co + 31) // 32 * 32), ((Co + 127) // 128 * 128) * ((K + 31) // 32 * 32)) * 4
         else:
             packed = ((Co + 255) // 256 * 256) * Kw * ((Kh * Ci + 63) // 64 * 64) * 2
         assert pkg.conv_workspace_bytes_dilated(N, Ci, H, W, Co, Kh, Kw, s, d, dt) == pad_end + packed
