@@ -27,6 +27,7 @@ import argparse
 import json
 import math
 import os
+import statistics
 import sys
 import time
 
@@ -47,8 +48,8 @@ PEAK_FP16_MFMA_TF = 2516.6      # dense (bf16 the same)
 # measured again.  Source: profiles/cfg2_n128_c64_56_3x3.md.
 FP32_SOURCES = ("conv_fp32_dma.hip",)
 FP32_CONV_TRAFFIC = {
-    "source_sha256": "a7724652b273d220b6d7bad46e5884f8b3bf14e68421ef67bb2ac30bcc44f923",
-    "bytes": {"cfg2_n128_c64_56_3x3": 1004.8e6 + 95.6e6},
+    "source_sha256": "78d76da377aa206509df9b005ba951bffdeec34fcb65e8d74b3ecffaf8ed2c7d",
+    "bytes": {"cfg2_n128_c64_56_3x3": 1004.4e6 + 95.6e6},
 }
 
 
@@ -212,67 +213,88 @@ ABLATION = {
         ("row kernel 128x128, 1 slot (no double buffering)",
          {"IM2WIN_FP16_KERNEL": "pipe", "IM2WIN_FP16_TILE": "c128p128s1"}),
         ("register-staged loads (no direct-to-LDS copy)", {"IM2WIN_FP16_KERNEL": "regs"}),
+        ("launch-order tiles (no XCD-aware tile order)", {"IM2WIN_TILE_ORDER": "linear"}),
     ],
     "f32": [
         ("as built", {}),
         ("register-staged loads (no direct-to-LDS copy)", {"IM2WIN_FP32_KERNEL": "regs"}),
+        ("launch-order tiles (no XCD-aware tile order)", {"IM2WIN_TILE_ORDER": "linear"}),
     ],
     "transform": [
         ("as built (XCD-aware block order)", {}),
         ("linear block order", {"IM2WIN_TRANSFORM_ORDER": "linear"}),
     ],
 }
-ABLATION_VARS = ("IM2WIN_FP16_KERNEL", "IM2WIN_FP16_TILE", "IM2WIN_FP32_KERNEL", "IM2WIN_TRANSFORM_ORDER")
+ABLATION_VARS = ("IM2WIN_FP16_KERNEL", "IM2WIN_FP16_TILE", "IM2WIN_FP32_KERNEL", "IM2WIN_TRANSFORM_ORDER",
+                 "IM2WIN_TILE_ORDER")
 
 
-def run_ablation(l, pkg, torch, workloads, reps=15):
-    """Median time of each call of the path with one technique switched off,
-    on layer `l`; each call repeated back to back (warm caches)."""
+def run_ablation(l, pkg, torch, workloads, reps=9, rounds=5):
+    """Time of each call of the path with one technique switched off, on
+    layer `l`.  The variants are interleaved so that clock ramps and drift
+    fall on all of them alike: after an untimed pass over every variant,
+    `rounds` passes each time `reps` back-to-back calls (warm caches) of
+    every variant, in reverse order on every other pass; the figure is the
+    median over the passes of each pass's median."""
     x, w = workloads.draw_layer(l)
     paths = {"f32": Path(l, x, w, torch.float32, pkg, torch),
              "f16": Path(l, x, w, torch.float16, pkg, torch)}
     nums = layer_numbers(l, pkg)
+    for p in paths.values():
+        p.transform()   # the window tensor the conv variants read
 
-    def timed(fn):
+    cases = []   # (part, label, environment, call, bytes moved or None)
+    for part, rows in ABLATION.items():
+        for label, env in rows:
+            if part == "transform":
+                for dt in ("f32", "f16"):
+                    cases.append((part, "%s %s" % (dt, label), env, paths[dt].transform,
+                                  nums[dt]["transform_bytes"]))
+            else:
+                cases.append((part, label, env, paths[part].run_conv, None))
+
+    def set_env(env):
+        for k in ABLATION_VARS:
+            os.environ.pop(k, None)
+        os.environ.update(env)
+
+    def timed(fn, n):
         for _ in range(3):
             fn()
         torch.cuda.synchronize()
         ts = []
-        for _ in range(reps):
+        for _ in range(n):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
             fn()
             e1.record()
             torch.cuda.synchronize()
             ts.append(e0.elapsed_time(e1))
-        ts.sort()
-        return ts[reps // 2]
+        return statistics.median(ts)
 
-    res = {"layer": l.name, "f16": {}, "f32": {}, "transform": {}}
+    times = {c[1] + "\0" + c[0]: [] for c in cases}
     saved = {k: os.environ.get(k) for k in ABLATION_VARS}
     try:
-        for part, rows in ABLATION.items():
-            for label, env in rows:
-                for k in ABLATION_VARS:
-                    os.environ.pop(k, None)
-                os.environ.update(env)
-                if part == "transform":
-                    for dt in ("f32", "f16"):
-                        ms = timed(paths[dt].transform)
-                        res[part]["%s %s" % (dt, label)] = {
-                            "ms": round(ms, 5), "GB/s": round(nums[dt]["transform_bytes"] / ms / 1e6, 1)}
-                else:
-                    p = paths[part]
-                    p.transform()
-                    ms = timed(p.run_conv)
-                    res[part][label] = {"ms": round(ms, 5),
-                                        "TFLOP/s": round(nums["flops"] / (ms * 1e-3) / 1e12, 2)}
+        for _, _, env, fn, _ in cases:
+            set_env(env)
+            timed(fn, reps)
+        for r in range(rounds):
+            for part, label, env, fn, _ in (cases if r % 2 == 0 else cases[::-1]):
+                set_env(env)
+                times[label + "\0" + part].append(timed(fn, reps))
     finally:
         for k, v in saved.items():
             if v is None:
                 os.environ.pop(k, None)
             else:
                 os.environ[k] = v
+    res = {"layer": l.name, "rounds": rounds, "reps": reps, "f16": {}, "f32": {}, "transform": {}}
+    for part, label, _, _, nbytes in cases:
+        ms = statistics.median(times[label + "\0" + part])
+        if nbytes is not None:
+            res[part][label] = {"ms": round(ms, 5), "GB/s": round(nbytes / ms / 1e6, 1)}
+        else:
+            res[part][label] = {"ms": round(ms, 5), "TFLOP/s": round(nums["flops"] / (ms * 1e-3) / 1e12, 2)}
     del paths
     return res
 

@@ -6,6 +6,7 @@
 #include "common.hpp"
 
 #include <atomic>
+#include <stdlib.h>
 #include <string.h>
 
 using namespace im2win;
@@ -90,6 +91,18 @@ int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_
                int64_t s, int dt, Shape *sh)
 {
     return make_shape_dil(N, Ci, Hi, Wi, Co, Kh, Kw, s, 1, dt, sh);
+}
+
+TileGrid make_tilegrid(int64_t gx, int64_t gy)
+{
+    // XCD order against launch order on MI355X (128 images): fp16 3x3 C=128
+    // at 28x28 487 -> 583 TFLOP/s, 3x3 C=512 at 7x7 276 -> 309, 1x1 C=1024
+    // at 14x14 632 -> 655; fp32 5x5 C_o=256 at 24x24 81.9 -> 86.5.  With one
+    // channel tile there is nothing to share and launch order measured
+    // slightly ahead (56x56 C=64: 457 vs 449 fp16, 78.5 vs 76.6 fp32).
+    const char *e = getenv("IM2WIN_TILE_ORDER");
+    const bool linear = gy <= 1 || (e && strcmp(e, "linear") == 0);
+    return TileGrid{(uint32_t)gx, (uint32_t)gy, linear ? 0u : 1u};
 }
 
 int64_t packed_filter_bytes(const Shape &sh, int dt)

@@ -81,6 +81,36 @@ struct WinCols {
     }
 };
 
+// Tile of a workgroup in a 1-D launch of gx * gy output tiles (gx along
+// pixels, gy along channels).  The hardware deals the workgroups of a launch
+// to the 8 XCDs round-robin (block b to XCD b % 8), each XCD with its own L2.
+// With `xcd` set, XCD k walks one contiguous run of tiles numbered
+// channel-fastest, so the gy channel tiles of a pixel tile, which read the
+// same windows, run on one XCD at about the same time and share those windows
+// through its L2; else tiles follow launch order pixel-fastest (the order of
+// a 2-D launch).
+struct TileGrid {
+    uint32_t gx, gy, xcd;
+
+    __device__ inline void tile(uint32_t &x, uint32_t &y) const
+    {
+        const uint32_t b = blockIdx.x;
+        if (!xcd) {
+            y = b / gx;
+            x = b - y * gx;
+            return;
+        }
+        const uint32_t nb = gx * gy, k = b % 8, j = b / 8, per = nb / 8, rem = nb % 8;
+        const uint32_t t = k * per + (k < rem ? k : rem) + j;
+        x = t / gy;
+        y = t - x * gy;
+    }
+};
+
+// gx * gy tiles (< 2^31, the caller's grid checks); IM2WIN_TILE_ORDER=linear
+// selects the launch order (to measure what the XCD-aware order gains).
+TileGrid make_tilegrid(int64_t gx, int64_t gy);
+
 inline WinCols make_wincols(const Shape &sh)
 {
     return WinCols{(uint32_t)sh.s, (uint32_t)sh.d, (uint32_t)sh.Wq, (uint32_t)(sh.Kh * sh.Ci),

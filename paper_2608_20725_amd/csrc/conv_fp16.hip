@@ -46,6 +46,7 @@ struct C16Args {
     uint32_t P, K, K_pad, Co, Co_pad, Wo, L;
     WinCols wc;              // window start of an output column in its strip
     uint32_t pk_bytes;       // bytes of the packed filter
+    TileGrid tg;             // pixel x channel tiles of the 1-D launch
     FastDiv div_Wo;
 };
 
@@ -240,8 +241,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_kernel(C16Args a)
     const uint32_t lane = tid & 63;
     const uint32_t wave = tid >> 6;
     const uint32_t wm = wave / WGN, wn = wave % WGN;
-    const uint32_t p0 = blockIdx.x * C::BNp;
-    const uint32_t ch0 = blockIdx.y * C::BMc;
+    uint32_t tx, ty;
+    a.tg.tile(tx, ty);
+    const uint32_t p0 = tx * C::BNp;
+    const uint32_t ch0 = ty * C::BMc;
 
     const uint32_t q0 = fdiv(p0, a.div_Wo);
     const uint64_t tb_elem = (uint64_t)q0 * a.L;
@@ -492,8 +495,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
     w.K = a.K;
     w.nst = a.K_pad / BK;
     const uint32_t wm = w.wave / WGN, wn = w.wave % WGN;
-    const uint32_t p0 = blockIdx.x * C::BNp;
-    const uint32_t ch0 = blockIdx.y * C::BMc;
+    uint32_t tx, ty;
+    a.tg.tile(tx, ty);
+    const uint32_t p0 = tx * C::BNp;
+    const uint32_t ch0 = ty * C::BMc;
 
     const uint32_t q0 = fdiv(p0, a.div_Wo);
     const uint64_t tb_elem = (uint64_t)q0 * a.L;
@@ -729,8 +734,11 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
                     pick = t;
         }
         const PipeVariant &p = v[pick];
-        dim3 grid((uint32_t)((sh.P + p.bn - 1) / p.bn), (uint32_t)((sh.Co + p.bm - 1) / p.bm));
-        return hipLaunchKernel(p.f[op == Op16::BF16], grid, dim3(p.nt), args, 0, st);
+        const int64_t gx = (sh.P + p.bn - 1) / p.bn, gy = (sh.Co + p.bm - 1) / p.bm;
+        if (gx * gy > 0x7fffffff)
+            return hipErrorInvalidValue;
+        a.tg = make_tilegrid(gx, gy);
+        return hipLaunchKernel(p.f[op == Op16::BF16], dim3((uint32_t)(gx * gy)), dim3(p.nt), args, 0, st);
     }
     const int sp = seg_plan(sh);
     if (sp >= 0)
@@ -753,8 +761,11 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
         else
             pick_regs<F16Op, 2, 2, 2, 2>(unal, &f, &bm, &bn);
     }
-    dim3 grid((uint32_t)((sh.P + bn - 1) / bn), (uint32_t)((sh.Co + bm - 1) / bm));
-    return hipLaunchKernel(f, grid, dim3(256), args, 0, st);
+    const int64_t gx = (sh.P + bn - 1) / bn, gy = (sh.Co + bm - 1) / bm;
+    if (gx * gy > 0x7fffffff)
+        return hipErrorInvalidValue;
+    a.tg = make_tilegrid(gx, gy);
+    return hipLaunchKernel(f, dim3((uint32_t)(gx * gy)), dim3(256), args, 0, st);
 }
 
 }  // namespace im2win

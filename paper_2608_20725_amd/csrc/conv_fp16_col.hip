@@ -53,6 +53,7 @@ struct ColArgs {
     uint64_t win_bytes;
     uint64_t pk_bytes;       // bytes of G
     uint32_t P, Co, Co_pad, Wo, L, T, Tp, s, ms, nst;
+    TileGrid tg;             // pixel x channel tiles of the 1-D launch
     FastDiv div_Wo;
 };
 
@@ -204,8 +205,10 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
     w.wn = w.wave % C::WGN;
     w.T = a.T;
     w.nst = a.Tp / C::BT;
-    const uint32_t p0 = blockIdx.x * C::BN;
-    const uint32_t ch0 = blockIdx.y * C::BM;
+    uint32_t tx, ty;
+    a.tg.tile(tx, ty);
+    const uint32_t p0 = tx * C::BN;
+    const uint32_t ch0 = ty * C::BM;
     const uint32_t q0 = fdiv(p0, a.div_Wo);
 
     // B rows address the window tensor from strip q0 on, A rows the filter
@@ -467,9 +470,12 @@ hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const
     a.ms = (uint32_t)(sh.s < sh.Kw ? sh.s : sh.Kw);
     a.nst = 0;
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
+    const int64_t gx = (sh.P + v.bn - 1) / v.bn, gy = (sh.Co + v.bm - 1) / v.bm;
+    if (gx * gy > 0x7fffffff)
+        return hipErrorInvalidValue;
+    a.tg = make_tilegrid(gx, gy);
     void *args[] = {&a};
-    dim3 grid((uint32_t)((sh.P + v.bn - 1) / v.bn), (uint32_t)((sh.Co + v.bm - 1) / v.bm));
-    return hipLaunchKernel(v.f[op == Op16::BF16], grid, dim3(v.nt), args, 0, st);
+    return hipLaunchKernel(v.f[op == Op16::BF16], dim3((uint32_t)(gx * gy)), dim3(v.nt), args, 0, st);
 }
 
 }  // namespace im2win

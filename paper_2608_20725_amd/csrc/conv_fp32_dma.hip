@@ -44,6 +44,7 @@ struct D32Args {
     uint64_t win_bytes;
     uint32_t P, K, K_pad, Co, Co_pad, Wo, L;
     WinCols wc;              // window start of an output column in its strip
+    TileGrid tg;             // pixel x channel tiles of the 1-D launch
     FastDiv div_Wo;
 };
 
@@ -232,8 +233,10 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
     w.K = a.K;
     w.Co_pad = a.Co_pad;
     w.nst = (a.K_pad + C::KT - 1) / C::KT;  // taps past K_pad read zero (masked, or past the filter)
-    const uint32_t p0 = blockIdx.x * C::BM;
-    const uint32_t jb = blockIdx.y * C::CW;  // first channel of the workgroup
+    uint32_t tx, ty;
+    a.tg.tile(tx, ty);
+    const uint32_t p0 = tx * C::BM;
+    const uint32_t jb = ty * C::CW;  // first channel of the workgroup
 
     // windows are addressed from the strip of p0 on
     const uint32_t q0 = fdiv(p0, a.div_Wo);
@@ -480,9 +483,12 @@ hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const void *ws, const
     a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
     a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.wc = make_wincols(sh);
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
+    const int64_t gx = (sh.P + v.bm - 1) / v.bm, gy = (sh.Co + v.cw - 1) / v.cw;
+    if (gx * gy > 0x7fffffff)
+        return hipErrorInvalidValue;
+    a.tg = make_tilegrid(gx, gy);
     void *args[] = {&a};
-    dim3 grid((uint32_t)((sh.P + v.bm - 1) / v.bm), (uint32_t)((sh.Co + v.cw - 1) / v.cw));
-    return hipLaunchKernel(v.f, grid, dim3(v.nt), args, 0, st);
+    return hipLaunchKernel(v.f, dim3((uint32_t)(gx * gy)), dim3(v.nt), args, 0, st);
 }
 
 }  // namespace im2win

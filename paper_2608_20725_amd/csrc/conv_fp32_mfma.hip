@@ -41,6 +41,7 @@ struct M32Args {
     uint32_t pk_bytes;
     uint32_t P, K, K_pad, Co, Co_pad, Wo, L;
     WinCols wc;
+    TileGrid tg;          // pixel x channel tiles of the 1-D launch
     FastDiv div_Wo;
 };
 
@@ -203,8 +204,10 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_mfma(M32Args a)
     w.K = a.K;
     w.nst = a.K_pad / BK;
     const uint32_t wm = w.wave / C::WGN, wn = w.wave % C::WGN;
-    const uint32_t p0 = blockIdx.x * C::BN;
-    const uint32_t ch0 = blockIdx.y * C::BM;
+    uint32_t tx, ty;
+    a.tg.tile(tx, ty);
+    const uint32_t p0 = tx * C::BN;
+    const uint32_t ch0 = ty * C::BM;
 
     // windows from the strip of p0 on; the packed filter from row ch0 of tile 0
     const uint32_t q0 = fdiv(p0, a.div_Wo);
@@ -392,9 +395,12 @@ hipError_t launch_conv_fp32_mfma(const Shape &sh, const float *filt, void *packe
     a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L;
     a.wc = make_wincols(sh);
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
+    const int64_t gx = (sh.P + v[pick].bn - 1) / v[pick].bn, gy = (sh.Co + v[pick].bm - 1) / v[pick].bm;
+    if (gx * gy > 0x7fffffff)
+        return hipErrorInvalidValue;
+    a.tg = make_tilegrid(gx, gy);
     void *args[] = {&a};
-    dim3 grid((uint32_t)((sh.P + v[pick].bn - 1) / v[pick].bn), (uint32_t)((sh.Co + v[pick].bm - 1) / v[pick].bm));
-    return hipLaunchKernel(v[pick].f, grid, dim3(v[pick].nt), args, 0, st);
+    return hipLaunchKernel(v[pick].f, dim3((uint32_t)(gx * gy)), dim3(v[pick].nt), args, 0, st);
 }
 
 }  // namespace im2win

@@ -11,6 +11,7 @@ import pytest
 import torch
 
 import oracle
+import paper_2608_20725_amd as pkg
 from gpu_util import Run, TOL, check_full, check_sampled, oracle_inputs, rel_err, say
 from oracle_checks import TINY
 from paper_2608_20725_amd import workloads
@@ -229,6 +230,48 @@ def test_kernel_variants_agree(case, monkeypatch):
         elif same_order:
             assert np.array_equal(out.view(np.uint8), first.view(np.uint8)), name
 
+
+
+# The XCD-aware tile order (several channel tiles) against launch order
+# (IM2WIN_TILE_ORDER=linear): each tile computes the same sums whichever
+# workgroup takes it, so the outputs agree bit for bit.  Grids with a ragged
+# share per XCD (tiles not a multiple of 8) and with fewer tiles than XCDs.
+ORDER_CASES = [
+    # (forced variables, shape, dtype, matrix-core fp32)
+    ({}, (2, 16, 17, 19, 300, 3, 3, 1), torch.float32, False),
+    ({"IM2WIN_FP32_KERNEL": "p4c8l8s2k16t4"}, (2, 16, 17, 19, 300, 3, 3, 1), torch.float32, False),
+    ({}, (1, 8, 6, 6, 200, 3, 3, 1), torch.float32, False),
+    ({}, (2, 64, 24, 24, 300, 3, 3, 1), torch.float32, True),
+    ({}, (1, 8, 6, 6, 200, 3, 3, 1), torch.float32, True),
+    ({}, (2, 64, 24, 24, 300, 3, 3, 1), torch.float16, False),
+    ({"IM2WIN_FP16_KERNEL": "pipe"}, (2, 16, 13, 13, 300, 5, 5, 1), torch.float16, False),
+    ({"IM2WIN_FP16_KERNEL": "regs"}, (2, 16, 13, 13, 300, 5, 5, 1), torch.bfloat16, False),
+    ({}, (1, 8, 6, 6, 200, 3, 3, 1), torch.float16, False),
+]
+
+
+@pytest.mark.parametrize("case", ORDER_CASES,
+                         ids=lambda c: "-".join(list(c[0].values()) + [_id(c[1]), str(c[2])[6:]] + (["mfma"] if c[3] else [])))
+def test_tile_order_same_bits(case, monkeypatch):
+    env, shape, dtype, mfma = case
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=19)
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    outs = []
+    for order in ("xcd", "linear"):
+        say("tile order", order, env, shape, dtype)
+        if order == "linear":
+            monkeypatch.setenv("IM2WIN_TILE_ORDER", "linear")
+        run = Run(x, w, s, dtype, conv=not mfma)
+        if mfma:
+            pkg.conv_im2win_fp32_mfma(run.ws, run.wd, run.out, run.N, run.Ci, run.H, run.W, s)
+            torch.cuda.synchronize()
+        check_full(run, x, w)
+        run.check_out_guards()
+        outs.append(run.out.clone())
+    bits = torch.int32 if dtype == torch.float32 else torch.int16
+    assert torch.equal(outs[0].view(bits), outs[1].view(bits))
 
 
 # Non-finite inputs stay inside the windows that hold them: an output is
