@@ -19,7 +19,9 @@ line also carries a `bf16` block (the same layer with bf16 operands on the
 same matrix-core kernels), an `fp32_mfma` block (the alternate fp32 path on
 the matrix cores) and a `dilated` block (the layer with filter dilation 2 and
 'same' padding, fp32 and fp16), all timed outside the step (extensions of the
-path).
+path), a `cold` block (pack+conv with L2 and Infinity Cache flushed before
+each call) and a `clock` block (the shader clock sampled while the step
+runs).
 """
 from __future__ import annotations
 
@@ -369,10 +371,47 @@ def cpu_baseline(l, x, w, budget_s=10.0):
         oracle.conv(xs[i0:i0 + n], wd, l.stride)
         done += n
     dt = time.perf_counter() - t0
-    return {"value": per_img * done / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.threads(),
+    cores = oracle.threads()
+    # one image on one thread
+    oracle.set_threads(1)
+    try:
+        t1 = time.perf_counter()
+        oracle.conv(xs[:1], wd, l.stride)
+        dt1 = time.perf_counter() - t1
+    finally:
+        oracle.set_threads(cores)
+    return {"value": per_img * done / dt / 1e12, "unit": "TFLOP/s", "cores": cores,
             "kind": "oracle",
             "sample": "%d images (%.1f passes over the batch of %d) of the same layer, fp64 direct "
-                      "convolution, %.1f s" % (done, done / l.N, l.N, dt)}
+                      "convolution, %.1f s" % (done, done / l.N, l.N, dt),
+            "single_thread": {"value": per_img / dt1 / 1e12, "unit": "TFLOP/s", "seconds": round(dt1, 3),
+                              "sample": "1 image of the same layer on 1 thread"}}
+
+
+def measure_cold(l, paths, nums, torch, reps=10):
+    """Pack+conv time with cold caches: before each timed call a 1 GiB
+    buffer is overwritten (untimed), which evicts the window tensor and the
+    filter from L2 and the 256 MB Infinity Cache; median of `reps` calls,
+    HIP events on the launch stream."""
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    res = {"flush_bytes": flush.numel() * 4, "reps": reps}
+    for name, p in paths.items():
+        p.transform()
+        ts = []
+        for r in range(reps):
+            flush.fill_(float(r))
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            p.run_conv()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        ms = statistics.median(ts)
+        res[name] = {"ms": round(ms, 5), "min_ms": round(min(ts), 5),
+                     "TFLOP/s": round(nums["flops"] / (ms * 1e-3) / 1e12, 3)}
+    del flush
+    return res
 
 
 def measure(l, steps, warmup, pkg, torch, workloads):
@@ -412,7 +451,62 @@ def measure(l, steps, warmup, pkg, torch, workloads):
     for j, name in enumerate(("f32", "f16")):
         k[name + "_transform_ms"] = avg(3 * j, 3 * j + 1)
         k[name + "_conv_ms"] = avg(3 * j + 1, 3 * j + 2)
+    k["clock"] = sample_clock(step, torch)
     return nums, k, elapsed, x, w, paths
+
+
+def sample_clock(step, torch, seconds=1.5, settle=0.5, period=0.01):
+    """Shader clock while the step runs: after the timed region, untimed
+    steps of the same workload for `seconds`, with a background thread
+    reading each XCD's current gfx clock (amdsmi GPU metrics, which the
+    driver refreshes every few tens of ms) every `period` seconds; samples
+    from the first `settle` seconds are dropped.  Returns an "error" entry
+    when amdsmi is unusable."""
+    import threading
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+    except Exception as e:   # no amdsmi on this host: report, do not fail
+        return {"error": "amdsmi unavailable: %s" % e}
+    samples = []
+    try:
+        handles = amdsmi.amdsmi_get_processor_handles()
+        h = handles[torch.cuda.current_device()] if len(handles) == torch.cuda.device_count() else handles[0]
+        stop = threading.Event()
+        t0 = time.perf_counter()
+
+        def run():
+            while not stop.is_set():
+                m = amdsmi.amdsmi_get_gpu_metrics_info(h)
+                c = [v for v in m.get("current_gfxclks", []) if isinstance(v, int) and v < 0xFFFF]
+                if c and time.perf_counter() - t0 >= settle:
+                    samples.append(c)
+                stop.wait(period)
+        th = threading.Thread(target=run, daemon=True)
+        th.start()
+        n = 0
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(20):
+                step()
+            n += 20
+            torch.cuda.synchronize()
+        stop.set()
+        th.join()
+    except Exception as e:
+        return {"error": "amdsmi: %s" % e}
+    finally:
+        try:
+            amdsmi.amdsmi_shut_down()
+        except Exception:
+            pass
+    if not samples:
+        return {"error": "no clock samples"}
+    mean = sorted(sum(c) / len(c) for c in samples)
+    per = [statistics.median(c[j] for c in samples) for j in range(min(len(c) for c in samples))]
+    return {"MHz_median": round(statistics.median(mean)), "MHz_min": round(mean[0]), "MHz_max": round(mean[-1]),
+            "per_xcd_median_MHz": [round(v) for v in per], "samples": len(samples),
+            "source": "amdsmi current_gfxclks (mean over XCDs) during %d untimed steps (%.1f s) after the "
+                      "timed region, first %.1f s dropped" % (n, seconds, settle)}
 
 
 def main():
@@ -511,8 +605,8 @@ def main():
                                   "frac_fp16_mfma": round(tf16 / PEAK_FP16_MFMA_TF, 4),
                                   "GB/s": round(f16["conv_bytes"] / c16 / 1e6, 1),
                                   "frac_hbm": round(f16["conv_bytes"] / c16 / 1e6 / PEAK_HBM_GBS, 4)},
-                "median_ms": {n: round(v[2], 5) for n, v in k.items()},
-                "min_ms": {n: round(v[1], 5) for n, v in k.items()},
+                "median_ms": {n: round(v[2], 5) for n, v in k.items() if n != "clock"},
+                "min_ms": {n: round(v[1], 5) for n, v in k.items() if n != "clock"},
             },
             "end_to_end_TFLOP/s": {"f32": round(flops / ((t32 + c32) * 1e-3) / 1e12, 3),
                                    "f16": round(flops / ((t16 + c16) * 1e-3) / 1e12, 3)},
@@ -525,9 +619,15 @@ def main():
                 "allocator_peak_bytes": peak_alloc,
             },
         }
+        rec["clock"] = k["clock"]
+        if "MHz_median" in rec["clock"]:
+            # the fp32 conv against the vector peak at the clock it ran at
+            rec["clock"]["f32_conv_frac_at_clock"] = round(
+                tf32 / (PEAK_FP32_VECTOR_TF * rec["clock"]["MHz_median"] / 2400.0), 4)
         rec["bf16"] = measure_bf16(l, x, w, pkg, torch)
         rec["fp32_mfma"] = measure_fp32_mfma(l, x, w, pkg, torch)
         rec["dilated"] = measure_dilated(l, x, w, pkg, torch)
+        rec["cold"] = measure_cold(l, paths, nums, torch)
         if not args.sweep:
             mb = measure_minibatch(l, paths, pkg, torch)
             for name in ("f32", "f16"):

@@ -51,6 +51,8 @@ def _load():
         lib.oracle_out_extent.restype = _i64
         lib.oracle_out_extent.argtypes = [_i64, _i64, _i64]
         lib.oracle_threads.restype = ctypes.c_int
+        lib.oracle_set_threads.restype = None
+        lib.oracle_set_threads.argtypes = [ctypes.c_int]
         lib.oracle_conv_f64.restype = ctypes.c_int
         lib.oracle_conv_f64.argtypes = [_i64] * 8 + [_dp, _dp, _dp, _dp]
         lib.oracle_conv_f64_points.restype = ctypes.c_int
@@ -99,6 +101,11 @@ def out_extent(n_in: int, k: int, s: int) -> int:
 def threads() -> int:
     """OpenMP threads the oracle runs with."""
     return int(_load().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Run the oracle's parallel loops on `n` threads (timing only)."""
+    _load().oracle_set_threads(int(n))
 
 
 def conv(x, w, stride: int, with_abs: bool = False):

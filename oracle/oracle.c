@@ -59,6 +59,18 @@ int oracle_threads(void)
 #endif
 }
 
+/* Threads the following parallel loops use (timing only; results do not
+ * depend on it: each output is summed by one thread in a fixed order). */
+void oracle_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /*
  * Eq. (1), written with the stride:
  *   O[i][m][n][j] = sum_u sum_v sum_r I[i][m*s+u][n*s+v][r] * F[u][v][r][j]
