@@ -33,8 +33,9 @@
  *                             runs (an internal layout, rewritten by every conv call)
  *                       fp32: the larger of [K_pad32][C_o_pad32] fp32, K_pad32 =
  *                             round_up(K, 16), C_o_pad32 = round_up(C_o, 32) (vector-ALU
- *                             kernels) and round_up(C_o, 128)*round_up(K, 32) fp32
- *                             (conv_im2win_fp32_mfma)
+ *                             kernels; channels 2i and 2i+1 swapped in each row for the
+ *                             LDS-staged kernel) and round_up(C_o, 128)*round_up(K, 32)
+ *                             fp32 (conv_im2win_fp32_mfma)
  *
  * Scope: one stride and one dilation for both axes; zero padding and dilation
  * through the *_padded / *_dilated calls below; no groups or bias.

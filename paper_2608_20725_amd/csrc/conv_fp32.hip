@@ -53,6 +53,7 @@ struct Pack32Args {
     float *packed;
     uint64_t quads;
     uint32_t K, Co, Co_pad, Ci, Kh, Kw;
+    uint32_t pair_swap;  // store channels 2i and 2i+1 swapped (the DMA-staged kernel's order)
 };
 
 __global__ __launch_bounds__(256) void pack_filter_fp32(Pack32Args a)
@@ -73,7 +74,8 @@ __global__ __launch_bounds__(256) void pack_filter_fp32(Pack32Args a)
                 if (j0 + e < a.Co)
                     v[e] = src[j0 + e];
         }
-        *reinterpret_cast<float4 *>(a.packed + g * 4) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4 *>(a.packed + g * 4) =
+            a.pair_swap ? make_float4(v[1], v[0], v[3], v[2]) : make_float4(v[0], v[1], v[2], v[3]);
     }
 }
 
@@ -486,6 +488,7 @@ hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hi
     a.quads = (uint64_t)sh.K_pad32 * sh.Co_pad32 / 4;
     a.K = (uint32_t)sh.K; a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
     a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
+    a.pair_swap = dma32_plan(sh) >= 0;  // the conv call picks its kernel by the same rule
     uint64_t blocks = (a.quads + 255) / 256;
     if (blocks > 65536)
         blocks = 65536;

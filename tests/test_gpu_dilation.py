@@ -148,7 +148,8 @@ def test_dilation_one_is_the_undilated_path(shape, dtype):
 # dilated layers; the register-staged ones and every row-per-pixel tile and
 # fp32 variant compute window starts through the dilated rule).
 VARIANTS = [
-    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16t4", "p4c8l8s2k16t4", "regs"],
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p6c8l8s2k16", "p4c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16t4",
+                            "p4c8l8s2k16t4", "regs"],
      (2, 16, 14, 17, 72, 3, 3, 1, 2, 2, 2), torch.float32),
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16g4", "regs"], (2, 3, 20, 20, 16, 3, 3, 1, 0, 0, 4), torch.float32),
     ("IM2WIN_FP16_TILE", ["c32p128s3", "c64p128s3", "c128p128s2", "c256p256s2w8", "c128p256s2w8", "c128p128s1"],
