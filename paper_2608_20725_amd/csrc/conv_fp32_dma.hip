@@ -71,7 +71,7 @@ struct DCfg {
     static constexpr int BM = WPX * WBM;          // pixels per workgroup
     static constexpr int CW = WCH * LC * TN;      // channels per workgroup
     static_assert(TN % 4 == 0 && NW % (WCH * KS) == 0, "tile");
-    static_assert(CW == 64, "the filter slab loads cover 64 channels");
+    static_assert(CW % 16 == 0, "whole 1 KiB filter loads per stage");
     static_assert(KS == 1 || (KC == 16 && GR == 16), "tap split: 16-tap quads groups, 16-byte loads");
     static constexpr int WBYTES = BM * KT * 4;    // window part of a stage
     static constexpr int FBYTES = KT * CW * 4;    // filter part of a stage
@@ -272,12 +272,14 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
             w.woff[i] = ((q - q0) * a.L + a.wc.start(p - q * a.Wo) + w.wk) * 4u;
         }
     }
-    // Filter load i fills taps 4*b .. 4*b+3 of the slab (b = wave + 4i): lane
-    // -> tap 4*b + lane/16, channels jb + 4*(lane%16) .. +3.
+    // Filter load i fills bytes 1024*b .. 1024*b+1023 of the stage's [KT][CW]
+    // slab (b = wave + NW*i): lane -> element e = 256*b + 4*lane, tap e / CW,
+    // channels jb + e % CW .. +3.
 #pragma unroll
     for (int i = 0; i < C::IF; ++i) {
         const uint32_t b = w.wave + C::NW * i;
-        const uint32_t row = 4 * b + w.lane / 16, col = jb + 4 * (w.lane % 16);
+        const uint32_t e = 256 * b + 4 * w.lane;
+        const uint32_t row = e / C::CW, col = jb + e % C::CW;
         w.foff[i] = (row < (uint32_t)C::KT && col < a.Co_pad) ? (row * a.Co_pad + col) * 4u : kOOB;
     }
 #pragma unroll
@@ -433,6 +435,11 @@ const DVariant *d_variants(int *n)
         d_variant<6, 8, 8, 1, 2, 16>("p6c8l8s2k16"),
         d_variant<4, 8, 8, 1, 2, 16>("p4c8l8s2k16"),
         d_variant<4, 16, 1, 4, 2, 16>("p4c16l1s2k16"),
+        // 96-channel tiles (12 channels per lane) for C_o = 96, 288, ...
+        d_variant<8, 12, 8, 1, 2, 16>("p8c12l8s2k16"),
+        d_variant<4, 12, 8, 1, 2, 16>("p4c12l8s2k16"),
+        d_variant<8, 12, 8, 1, 2, 16, 4>("p8c12l8s2k16g4"),
+        d_variant<4, 12, 8, 1, 2, 16, 4>("p4c12l8s2k16g4"),
         // 4-byte window loads: windows that start anywhere (C_i % 4 != 0)
         d_variant<8, 8, 8, 1, 2, 16, 4>("p8c8l8s2k16g4"),
         d_variant<8, 8, 8, 1, 2, 16, 16, 4>("p8c8l8s2k16t4"),
@@ -458,6 +465,14 @@ int dma32_plan(const Shape &sh)
                        : tiles256 <= 128  ? "p8c8l8s2k16t4"
                        : tiles256 <= 1024 ? "p4c8l8s2k16t4"
                                           : "p8c8l8s2k16";
+    // 96-channel tiles where they pad fewer channels than 64-channel ones
+    // (C_o = 96: 0 against 32 of 128) and still give four workgroups per CU:
+    // 11x11 C_i=3 C_o=96 stride 4, 60.7 -> 74.8 TFLOP/s; 3x3 C=64 -> 96 at
+    // 56x56, 70.0 -> 84.0.  The 8 x 12 lane tile (2 waves per SIMD) measured
+    // 68.7 and 80.2.
+    const int64_t pad64 = (sh.Co + 63) / 64 * 64 - sh.Co, pad96 = (sh.Co + 95) / 96 * 96 - sh.Co;
+    if (pad96 < pad64 && ((sh.P + 127) / 128) * ((sh.Co + 95) / 96) >= 1024)
+        name = aligned ? "p4c12l8s2k16" : "p4c12l8s2k16g4";
     if (const char *e = getenv("IM2WIN_FP32_KERNEL")) {
         if (strcmp(e, "regs") == 0)
             return -1;

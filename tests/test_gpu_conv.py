@@ -199,9 +199,16 @@ VARIANT_CASES = [
     ("IM2WIN_FP16_KERNEL", ["pipe", "regs"], (1, 64, 20, 20, 300, 3, 3, 1), torch.float16, True),
     ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c128p256t16s3", "k3c256p256t32s2w8", "k3c256p192t32s2w8"],
      (2, 64, 24, 24, 300, 3, 3, 1), torch.float16, False),
-    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p6c8l8s2k16", "p4c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16g4", "regs"],
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p6c8l8s2k16", "p4c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16g4",
+                            "p4c12l8s2k16", "p8c12l8s2k16", "p4c12l8s2k16g4", "p8c12l8s2k16g4", "regs"],
      (2, 16, 17, 19, 100, 3, 3, 1), torch.float32, True),
-    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16g4", "regs"], (3, 3, 40, 61, 70, 11, 11, 4), torch.float32, True),
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16g4", "p4c12l8s2k16g4", "p8c12l8s2k16g4", "regs"],
+     (3, 3, 40, 61, 70, 11, 11, 4), torch.float32, True),
+    # 96-channel tiles: C_o = 96 exactly and C_o = 200 (a ragged third tile)
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p4c12l8s2k16", "p8c12l8s2k16", "regs"],
+     (2, 8, 20, 22, 96, 3, 3, 1), torch.float32, True),
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16g4", "p4c12l8s2k16g4", "regs"], (2, 3, 30, 29, 200, 5, 5, 2), torch.float32,
+     True),
     # taps split over the waves: another summation order, K = 144 ragged in
     # 64-tap stages
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16t4", "p4c8l8s2k16t4"], (2, 16, 17, 19, 100, 3, 3, 1), torch.float32,
