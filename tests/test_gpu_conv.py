@@ -202,7 +202,8 @@ VARIANT_CASES = [
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p6c8l8s2k16", "p4c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16g4",
                             "p4c12l8s2k16", "p8c12l8s2k16", "p4c12l8s2k16g4", "p8c12l8s2k16g4", "regs"],
      (2, 16, 17, 19, 100, 3, 3, 1), torch.float32, True),
-    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16g4", "p4c12l8s2k16g4", "p8c12l8s2k16g4", "regs"],
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16g4", "p6c8l8s2k16g4", "p4c8l8s2k16g4", "p4c12l8s2k16g4", "p8c12l8s2k16g4",
+                            "regs"],
      (3, 3, 40, 61, 70, 11, 11, 4), torch.float32, True),
     # 96-channel tiles: C_o = 96 exactly and C_o = 200 (a ragged third tile)
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p4c12l8s2k16", "p8c12l8s2k16", "regs"],

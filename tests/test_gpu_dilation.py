@@ -151,7 +151,8 @@ VARIANTS = [
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p6c8l8s2k16", "p4c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16t4",
                             "p4c8l8s2k16t4", "regs"],
      (2, 16, 14, 17, 72, 3, 3, 1, 2, 2, 2), torch.float32),
-    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16g4", "p4c12l8s2k16g4", "regs"], (2, 3, 20, 20, 16, 3, 3, 1, 0, 0, 4),
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16g4", "p6c8l8s2k16g4", "p4c8l8s2k16g4", "p4c12l8s2k16g4", "regs"],
+     (2, 3, 20, 20, 16, 3, 3, 1, 0, 0, 4),
      torch.float32),
     ("IM2WIN_FP32_KERNEL", ["p4c12l8s2k16", "p8c12l8s2k16"], (2, 16, 14, 17, 96, 3, 3, 1, 2, 2, 2), torch.float32),
     ("IM2WIN_FP16_TILE", ["c32p128s3", "c64p128s3", "c128p128s2", "c256p256s2w8", "c128p256s2w8", "c128p128s1"],
