@@ -95,3 +95,20 @@ def test_transform_linear_block_order_same_bytes(shape, monkeypatch):
     run = Run(x, w, s, torch.float16, conv=False)
     _compare(run, x)
     assert torch.equal(run.ws[:run.window_bytes()], ref.ws[:ref.window_bytes()])
+
+
+# Unaligned windows (C_i * elt not a multiple of 16 bytes) take the element
+# gather: odd channel counts, strips that end inside a granule, K_h = H, a
+# tall filter over a wide input, stride > K.
+UNALIGNED = [(2, 3, 12, 12, 3, 3, 1), (3, 5, 11, 13, 5, 3, 2), (1, 7, 9, 31, 9, 2, 3), (2, 1, 8, 8, 8, 8, 1),
+             (2, 3, 227, 40, 11, 11, 4), (1, 3, 30, 300, 27, 5, 1), (2, 6, 10, 10, 2, 2, 3)]
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "f16", "bf16"])
+@pytest.mark.parametrize("shape", UNALIGNED, ids=lambda s: "x".join(map(str, s)))
+def test_transform_unaligned(shape, dtype):
+    N, Ci, H, W, Kh, Kw, s = shape
+    say("unaligned transform", shape, dtype)
+    x, w = workloads.draw(N, Ci, H, W, 2, Kh, Kw, seed=5 + sum(shape))
+    run = Run(x, w, s, dtype, conv=False)
+    _compare(run, x)
