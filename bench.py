@@ -20,8 +20,9 @@ same matrix-core kernels), an `fp32_mfma` block (the alternate fp32 path on
 the matrix cores) and a `dilated` block (the layer with filter dilation 2 and
 'same' padding, fp32 and fp16), all timed outside the step (extensions of the
 path), a `cold` block (pack+conv with L2 and Infinity Cache flushed before
-each call) and a `clock` block (the shader clock sampled while the step
-runs).
+each call), a `clock` block (the shader clock sampled while the step
+runs) and a `graph` block (the step captured in a HIP graph and replayed,
+against call-by-call launches).
 """
 from __future__ import annotations
 
@@ -388,6 +389,43 @@ def cpu_baseline(l, x, w, budget_s=10.0):
                               "sample": "1 image of the same layer on 1 thread"}}
 
 
+def measure_graph(l, paths, nums, torch, reps=50):
+    """The step (both transforms and both pack+conv calls) captured once in a
+    HIP graph and replayed: time per step over `reps` back-to-back replays
+    (HIP events around the whole loop), against the same step launched call
+    by call.  The library launches on the current stream, so capture records
+    its kernels; it records no memset nodes."""
+    def step():
+        for name in ("f32", "f16"):
+            paths[name].transform()
+            paths[name].run_conv()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, capture_error_mode="relaxed"):
+        step()
+    torch.cuda.synchronize()
+    res = {"reps": reps}
+    for name, fn in (("graph", g.replay), ("eager", step)):
+        for _ in range(10):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        res[name] = {"ms_per_step": round(ms, 5), "TFLOP/s": round(2 * nums["flops"] / (ms * 1e-3) / 1e12, 3)}
+    del g
+    return res
+
+
 def measure_cold(l, paths, nums, torch, reps=10):
     """Pack+conv time with cold caches: before each timed call a 1 GiB
     buffer is overwritten (untimed), which evicts the window tensor and the
@@ -629,6 +667,7 @@ def main():
         rec["fp32_mfma"] = measure_fp32_mfma(l, x, w, pkg, torch)
         rec["dilated"] = measure_dilated(l, x, w, pkg, torch)
         rec["cold"] = measure_cold(l, paths, nums, torch)
+        rec["graph"] = measure_graph(l, paths, nums, torch)
         if not args.sweep:
             mb = measure_minibatch(l, paths, pkg, torch)
             for name in ("f32", "f16"):
