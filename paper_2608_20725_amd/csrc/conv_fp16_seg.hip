@@ -91,6 +91,28 @@ struct SegTile {
         }
     }
 
+    // 16 bytes of LDS from a 2-byte-aligned offset.  An unaligned ds_read_b128
+    // stalls the LDS pipe (~11 cycles per read measured on the 3-channel
+    // stem); three aligned 8-byte reads of the span and a byte-align of each
+    // dword in registers give the same bytes.
+    __device__ static inline void read16(const char *lds, uint32_t o, v8 &dst)
+    {
+        const uint32_t base = o & ~7u, sh = o & 7u;
+        const uint2 a0 = *reinterpret_cast<const uint2 *>(lds + base);
+        const uint2 a1 = *reinterpret_cast<const uint2 *>(lds + base + 8);
+        const uint2 a2 = *reinterpret_cast<const uint2 *>(lds + base + 16);
+        const uint32_t w[6] = {a0.x, a0.y, a1.x, a1.y, a2.x, a2.y};
+        const bool hi4 = sh >= 4;
+        const uint32_t b = sh & 3u;
+        uint32_t out[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t lo = hi4 ? w[i + 1] : w[i], hi = hi4 ? w[i + 2] : w[i + 1];
+            out[i] = __builtin_amdgcn_alignbyte(hi, lo, b);
+        }
+        __builtin_memcpy(&dst, out, 16);
+    }
+
     __device__ inline void compute(uint32_t st, const char *aslot, const char *seg)
     {
         const bool tail = st * BK + BK > K;
@@ -106,8 +128,7 @@ struct SegTile {
             }
 #pragma unroll
             for (int j = 0; j < C::WN; ++j) {
-                // a window starts at any element: 2-byte aligned 16-byte read
-                __builtin_memcpy(&bf[j], seg + bb[j] + 2 * k, 16);
+                read16(seg, bb[j] + 2 * k, bf[j]);  // a window starts at any element
                 if (tail) {
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
@@ -129,7 +150,8 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_seg(SegArgs a)
 {
     __shared__ __attribute__((aligned(1024))) char r0[C::ASTAGE];
     __shared__ __attribute__((aligned(1024))) char r1[C::ASTAGE];
-    __shared__ __attribute__((aligned(1024))) char seg[C::GMAX * 16];
+    // 16 bytes of slack: a fragment read spans up to 8 bytes past its 16
+    __shared__ __attribute__((aligned(1024))) char seg[C::GMAX * 16 + 16];
 
     SegTile<C, E> w;
     const uint32_t tid = threadIdx.x;
