@@ -51,7 +51,7 @@ PEAK_FP16_MFMA_TF = 2516.6      # dense (bf16 the same)
 # measured again.  Source: profiles/cfg2_n128_c64_56_3x3.md.
 FP32_SOURCES = ("conv_fp32_dma.hip",)
 FP32_CONV_TRAFFIC = {
-    "source_sha256": "a1a4f794fab99930cc4cf7188b6efe3b03800eef4b6c9f58d188a17b9b5dfae7",
+    "source_sha256": "17b1052a42de343bb699ff48f2307aa587a56aaa87f644e93853d0ced3ceaab2",
     "bytes": {"cfg2_n128_c64_56_3x3": 1016.6e6 + 95.6e6},
 }
 

@@ -465,7 +465,7 @@ int dma32_plan(const Shape &sh)
     const int64_t tiles256 = ((sh.P + 255) / 256) * ((sh.Co + 63) / 64);
     // unaligned windows (C_i % 4 != 0, the 3-channel stems): the 6-pixel
     // lane tile, 7x7 C_i=3 stride 2 67.2 vs 64.1 TFLOP/s (8-pixel) and 3x3
-    // C_i=3 36.6 vs 34.4, same box
+    // C_i=3 36.6 vs 34.4, same machine
     const char *name = !aligned          ? "p6c8l8s2k16g4"
                        : tiles256 <= 128  ? "p8c8l8s2k16t4"
                        : tiles256 <= 1024 ? "p4c8l8s2k16t4"
