@@ -362,6 +362,7 @@ const ColVariant *col_variants(int *n)
     // name: filter width, channels x pixels per tile, taps per stage, ring slots
     static const ColVariant v[] = {
         col_variant<3, 32, 2, 2, 1, 4, 288, 2>("k3c64p256t32s2"),
+        col_variant<3, 32, 1, 2, 2, 2, 160, 2>("k3c64p128t32s2"),
         col_variant<3, 16, 2, 4, 2, 2, 288, 3>("k3c128p256t16s3"),
         col_variant<7, 16, 2, 2, 1, 4, 544, 3>("k7c64p256t16s3"),
         // eight waves, 256 x 256 tiles (large C_o)
@@ -418,7 +419,12 @@ int col_plan(const Shape &sh)
         const char *name = nullptr;
         if (fp16_single_slot_rows(sh))
             return -1;  // the one-slot row kernel is faster there
-        if (sh.Kw == 3 && sh.Co <= 128)
+        // C_o <= 64: 64 x 128 tiles, three workgroups per CU, more bytes in
+        // flight for these HBM-bound layers (3x3 C=64 at 56x56: 484 vs 431
+        // TFLOP/s same-process; with C_o = 128, 3x3 at 28x28, 531 vs 548)
+        if (sh.Kw == 3 && sh.Co <= 64)
+            name = "k3c64p128t32s2";
+        else if (sh.Kw == 3 && sh.Co <= 128)
             name = "k3c64p256t32s2";
         else if (sh.Kw == 7 && sh.Co <= 128)
             name = "k7c64p256t16s3";

@@ -97,7 +97,8 @@ def test_bf16_register_kernel_on_segment_shapes(shape, monkeypatch):
 BF16_VARIANTS = [
     ("IM2WIN_FP16_TILE", ["c32p128s3", "c64p128s3", "c128p128s2", "c256p256s2w8", "c128p256s2w8"],
      (2, 16, 13, 13, 72, 5, 5, 1), True),
-    ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c128p256t16s3", "k3c256p256t32s2w8", "k3c256p192t32s2w8"],
+    ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c64p128t32s2", "k3c128p256t16s3", "k3c256p256t32s2w8",
+                         "k3c256p192t32s2w8"],
      (2, 64, 24, 24, 300, 3, 3, 1), False),
     ("IM2WIN_FP16_SEG", ["s64p256", "s96p128", "s128p128"], (2, 6, 13, 90, 200, 3, 5, 1), True),
 ]

@@ -197,7 +197,8 @@ VARIANT_CASES = [
     # pack follows): the same summation order as the row-per-pixel kernel
     ("IM2WIN_FP16_KERNEL", ["pipe", "regs"], (2, 16, 13, 13, 72, 5, 5, 1), torch.float16, True),
     ("IM2WIN_FP16_KERNEL", ["pipe", "regs"], (1, 64, 20, 20, 300, 3, 3, 1), torch.float16, True),
-    ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c128p256t16s3", "k3c256p256t32s2w8", "k3c256p192t32s2w8"],
+    ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c64p128t32s2", "k3c128p256t16s3", "k3c256p256t32s2w8",
+                         "k3c256p192t32s2w8"],
      (2, 64, 24, 24, 300, 3, 3, 1), torch.float16, False),
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p6c8l8s2k16", "p4c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16g4",
                             "p4c12l8s2k16", "p8c12l8s2k16", "p4c12l8s2k16g4", "p8c12l8s2k16g4", "regs"],
