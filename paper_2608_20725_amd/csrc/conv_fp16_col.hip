@@ -365,6 +365,7 @@ const ColVariant *col_variants(int *n)
         col_variant<3, 32, 1, 2, 2, 2, 160, 2>("k3c64p128t32s2"),
         col_variant<3, 16, 2, 4, 2, 2, 288, 3>("k3c128p256t16s3"),
         col_variant<7, 16, 2, 2, 1, 4, 544, 3>("k7c64p256t16s3"),
+        col_variant<7, 16, 1, 2, 2, 2, 288, 2>("k7c64p128t16s2"),
         // eight waves, 256 x 256 tiles (large C_o)
         col_variant<3, 32, 4, 2, 2, 4, 320, 2>("k3c256p256t32s2w8"),
         col_variant<3, 32, 2, 3, 4, 2, 256, 2>("k3c256p192t32s2w8"),
@@ -426,6 +427,12 @@ int col_plan(const Shape &sh)
             name = "k3c64p128t32s2";
         else if (sh.Kw == 3 && sh.Co <= 128)
             name = "k3c64p256t32s2";
+        // 7x7: with stride 1 and C_o <= 64 the 64 x 128 tile (two-slot ring,
+        // 49 KiB, three workgroups per CU) measured 785 vs 713 TFLOP/s
+        // (7x7 C=64 at 60x60, 64 images); with stride 2 (7x7 C=64 at 224x224)
+        // it lost, 668 vs 701
+        else if (sh.Kw == 7 && sh.s == 1 && sh.Co <= 64)
+            name = "k7c64p128t16s2";
         else if (sh.Kw == 7 && sh.Co <= 128)
             name = "k7c64p256t16s3";
         else if (sh.Kw == 3 && tiles(192) >= 160 && tiles(192) <= 256)
