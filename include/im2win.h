@@ -54,7 +54,16 @@
  * (each pointer must lie in one device allocation that holds the whole
  * buffer) -> overlap -> workspace size -> device -> launch.  The first failing
  * check's status is returned; nothing is printed and no exception leaves the
- * library.  Numerics: fp32 conv accumulates in fp32 (FMA); fp16 and bf16 conv
+ * library.  Kernel choice: each conv call picks its kernel from the layer's
+ * shape (conv_im2win_kernel_name reports which).  Tuning variables in the
+ * environment can force another, to measure kernels against each other:
+ * IM2WIN_FP16_KERNEL (pipe | regs), IM2WIN_FP16_COL, IM2WIN_FP16_TILE,
+ * IM2WIN_FP16_SEG, IM2WIN_FP32_KERNEL (a variant name | regs),
+ * IM2WIN_FP32_TILE, IM2WIN_FP32_MFMA_TILE (variant names),
+ * IM2WIN_TRANSFORM_ORDER and IM2WIN_TILE_ORDER (xcd | linear).  A value
+ * that names no kernel, contradictory values, or a forced kernel that cannot
+ * run the layer make the call return IM2WIN_EINVAL (checked after the
+ * workspace size, before the device).  Numerics: fp32 conv accumulates in fp32 (FMA); fp16 and bf16 conv
  * take 16-bit operands, accumulate in fp32 and round to nearest-even on store.
  */
 #ifndef IM2WIN_H
@@ -305,17 +314,39 @@ int64_t conv_chunked_workspace_bytes(int64_t N, int64_t C_i, int64_t H_i, int64_
  *                   conv.  The aux stream first waits for the work already on
  *                   hip_stream and hip_stream finally waits for the aux
  *                   stream, so all of the call is ordered before later work on
- *                   hip_stream.  The ordering uses two HIP events that the
- *                   library creates on first use per host thread and device
- *                   and keeps (no device memory is allocated).
- * The output is bit-identical to conv_im2win_fp32/fp16/bf16 on the full batch.
- * Errors as for the other calls; input, filter, output and workspace must not
+ *                   hip_stream.  The ordering uses two HIP events created and
+ *                   destroyed within the call (no device memory is allocated).
+ * The kernel is chosen once, for a full chunk of n_chunk images (see
+ * conv_im2win_kernel_name), and runs every chunk, the last one included, so
+ * every output is bit-identical to what conv_im2win_fp32/fp16/bf16 give for it
+ * in a batch of n_chunk images.  Against a full-batch call (whose kernel,
+ * picked for N images, may sum in another order) it agrees within the error
+ * bound of the exact result.  Errors as for the other calls; input, filter, output and workspace must not
  * overlap, and the two streams must differ.
  */
 int conv_im2win_chunked(const void *in_nhwc, const void *filt_khkwcico, void *out_nhwc, void *ws,
                         int64_t ws_bytes, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o,
                         int64_t K_h, int64_t K_w, int64_t stride, int64_t n_chunk, im2win_dtype_t dt,
                         void *hip_stream, void *hip_stream_aux);
+
+/*
+ * Names the kernel the conv call of this layer runs, e.g.
+ * "conv_fp16_col k3c64p128t32s2" (kernel family, then variant): the choice
+ * the call makes from the shape and the tuning variables above.
+ *   dt                 IM2WIN_F32 (vector ALUs, or the matrix cores when
+ *                      fp32_matrix_cores is non-zero: conv_im2win_fp32_mfma),
+ *                      IM2WIN_F16 or IM2WIN_BF16 (same kernels)
+ *   dilation           1 for the plain layer (conv_im2win_dilated otherwise)
+ *   buf, buf_len       host buffer receiving a NUL-terminated name (64 bytes
+ *                      always suffice)
+ * For the mini-batch call, pass N = n_chunk: every chunk runs the kernel of a
+ * full chunk.  Host only.  Returns IM2WIN_OK, the status the conv call would
+ * return for bad dims or tuning variables, or IM2WIN_ERANGE when buf_len is
+ * too short.
+ */
+int conv_im2win_kernel_name(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h,
+                            int64_t K_w, int64_t stride, int64_t dilation, im2win_dtype_t dt,
+                            int fp32_matrix_cores, char *buf, int64_t buf_len);
 
 /* A static, human-readable name for a status code. */
 const char *conv_im2win_strerror(int status);

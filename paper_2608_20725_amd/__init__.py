@@ -30,7 +30,7 @@ __all__ = [
     "conv_im2win_transform", "conv_im2win_transform_padded", "conv_im2win_fp32", "conv_im2win_fp16",
     "conv_im2win_bf16", "conv_im2win_fp32_mfma", "conv_output_dims_dilated", "conv_workspace_bytes_dilated",
     "conv_im2win_transform_dilated", "conv_im2win_dilated",
-    "conv_im2win_strerror", "im2win_conv2d",
+    "conv_im2win_strerror", "conv_im2win_kernel_name", "im2win_conv2d",
 ]
 
 F32 = 0
@@ -94,6 +94,8 @@ def load_library():
     lib.conv_chunked_workspace_bytes.argtypes = [_i64] * 9 + [ctypes.c_int, ctypes.c_int]
     lib.conv_im2win_chunked.restype = ctypes.c_int
     lib.conv_im2win_chunked.argtypes = [_vp, _vp, _vp, _vp, _i64] + [_i64] * 9 + [ctypes.c_int, _vp, _vp]
+    lib.conv_im2win_kernel_name.restype = ctypes.c_int
+    lib.conv_im2win_kernel_name.argtypes = [_i64] * 9 + [ctypes.c_int, ctypes.c_int, ctypes.c_char_p, _i64]
     lib.conv_im2win_strerror.restype = ctypes.c_char_p
     lib.conv_im2win_strerror.argtypes = [ctypes.c_int]
     _lib = lib
@@ -135,6 +137,16 @@ def _nbytes(t) -> int:
 def _check(rc: int, what: str):
     if rc != 0:
         raise Im2winError(rc, what)
+
+
+def conv_im2win_kernel_name(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dtype, dilation: int = 1,
+                            fp32_matrix_cores: bool = False) -> str:
+    """The kernel (family and variant) the conv call of this layer runs."""
+    buf = ctypes.create_string_buffer(64)
+    _check(load_library().conv_im2win_kernel_name(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dilation,
+                                                  _dtype_code(dtype), 1 if fp32_matrix_cores else 0,
+                                                  buf, len(buf)), "conv_im2win_kernel_name")
+    return buf.value.decode()
 
 
 def conv_output_dims(H_i: int, W_i: int, K_h: int, K_w: int, stride: int):

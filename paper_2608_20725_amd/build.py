@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libim2win.so")
-SOURCES = ["api.cpp", "chunked.cpp", "transform.hip", "conv_fp32.hip", "conv_fp16.hip", "conv_fp16_col.hip", "conv_fp32_dma.hip", "conv_fp16_seg.hip", "conv_fp32_mfma.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "chunked.cpp", "transform.hip", "conv_fp32.hip", "conv_fp16.hip", "conv_fp16_col.hip", "conv_fp32_dma.hip", "conv_fp16_seg.hip", "conv_fp32_mfma.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -25,21 +25,44 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + srcs + ["-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+def _run(cmd):
     p = subprocess.run(cmd, capture_output=True, text=True)
     # the host pass does not know the gfx950 feature name: drop that warning
     noise = [l for l in (p.stdout + p.stderr).splitlines()
              if l.strip() and "packed-fp32-ops" not in l]
-    if p.returncode != 0:
-        sys.stderr.write("\n".join(noise) + "\n")
+    return p.returncode, noise
+
+
+def build(verbose: bool = False) -> str:
+    """Compiles every source to an object (in parallel), then links them."""
+    from concurrent.futures import ThreadPoolExecutor
+    objdir = os.path.join(ROOT, "_build", "obj")
+    os.makedirs(objdir, exist_ok=True)
+    compile_flags = [f for f in FLAGS if f != "-shared"]
+    jobs = []
+    for s in SOURCES:
+        obj = os.path.join(objdir, os.path.splitext(s)[0] + ".o")
+        jobs.append((obj, [HIPCC] + compile_flags + ["-c", os.path.join(CSRC, s), "-o", obj]))
+    workers = max(1, min(len(jobs), os.cpu_count() or 1, 16))
+    with ThreadPoolExecutor(workers) as ex:
+        results = list(ex.map(lambda j: _run(j[1]), jobs))
+    failed = False
+    for (obj, cmd), (rc, noise) in zip(jobs, results):
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        if noise and (verbose or rc != 0):
+            sys.stderr.write("\n".join(noise) + "\n")
+        failed |= rc != 0
+    if failed:
         raise RuntimeError("hipcc failed building libim2win.so")
-    if verbose and noise:
-        print("\n".join(noise))
+    tmp = LIB + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + [j[0] for j in jobs] + ["-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    rc, noise = _run(cmd)
+    if rc != 0:
+        sys.stderr.write("\n".join(noise) + "\n")
+        raise RuntimeError("linking libim2win.so failed")
     os.replace(tmp, LIB)
     return LIB
 

@@ -93,16 +93,14 @@ int make_shape(int64_t N, int64_t Ci, int64_t Hi, int64_t Wi, int64_t Co, int64_
     return make_shape_dil(N, Ci, Hi, Wi, Co, Kh, Kw, s, 1, dt, sh);
 }
 
-TileGrid make_tilegrid(int64_t gx, int64_t gy)
+TileGrid make_tilegrid(int64_t gx, int64_t gy, bool linear)
 {
     // XCD order against launch order on MI355X (128 images): fp16 3x3 C=128
     // at 28x28 487 -> 583 TFLOP/s, 3x3 C=512 at 7x7 276 -> 309, 1x1 C=1024
     // at 14x14 632 -> 655; fp32 5x5 C_o=256 at 24x24 81.9 -> 86.5.  With one
     // channel tile there is nothing to share and launch order measured
     // slightly ahead (56x56 C=64: 457 vs 449 fp16, 78.5 vs 76.6 fp32).
-    const char *e = getenv("IM2WIN_TILE_ORDER");
-    const bool linear = gy <= 1 || (e && strcmp(e, "linear") == 0);
-    return TileGrid{(uint32_t)gx, (uint32_t)gy, linear ? 0u : 1u};
+    return TileGrid{(uint32_t)gx, (uint32_t)gy, (linear || gy <= 1) ? 0u : 1u};
 }
 
 int64_t packed_filter_bytes(const Shape &sh, int dt)
@@ -212,10 +210,13 @@ int transform_pad_dil(const void *in_nhwc, void *ws, int64_t ws_bytes, int64_t N
         return IM2WIN_EOVERLAP;
     if (ws_bytes < workspace_bytes(sh, dt))
         return IM2WIN_EWORKSPACE;
+    Tuning tu;
+    if ((rc = read_tuning(&tu)) != IM2WIN_OK)
+        return rc;
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
     const Pad pad{H_i, W_i, pad_h, pad_w};
-    return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream, &pad));
+    return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream, tu, &pad));
 }
 
 // The fp32 convolution, filter dilated by d (1: none): on the vector ALUs,
@@ -244,14 +245,19 @@ int conv32(void *ws, int64_t ws_bytes, const float *filt_khkwcico, float *out_nh
         return IM2WIN_EOVERLAP;
     if (ws_bytes < workspace_bytes(sh, IM2WIN_F32))
         return IM2WIN_EWORKSPACE;
+    Tuning tu;
+    Plan32 plan;
+    if ((rc = read_tuning(&tu)) != IM2WIN_OK || (rc = plan_fp32(sh, tu, mfma, &plan)) != IM2WIN_OK)
+        return rc;
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
     void *packed = (char *)ws + sh.pad_end;
-    if (mfma && fp32_mfma_ok(sh))
-        return launch_status(launch_conv_fp32_mfma(sh, filt_khkwcico, packed, out_nhwc, ws, (hipStream_t)hip_stream));
-    if ((rc = launch_status(launch_pack_fp32(sh, filt_khkwcico, packed, (hipStream_t)hip_stream))) != IM2WIN_OK)
+    const hipStream_t st = (hipStream_t)hip_stream;
+    if (plan.fam == Fam32::Mfma)
+        return launch_status(launch_conv_fp32_mfma(sh, plan, tu, filt_khkwcico, packed, out_nhwc, ws, st));
+    if ((rc = launch_status(launch_pack_fp32(sh, plan, filt_khkwcico, packed, st))) != IM2WIN_OK)
         return rc;
-    return launch_status(launch_conv_fp32(sh, ws, packed, out_nhwc, (hipStream_t)hip_stream));
+    return launch_status(launch_conv_fp32(sh, plan, tu, ws, packed, out_nhwc, st));
 }
 
 }  // namespace
@@ -345,9 +351,12 @@ int conv_im2win_transform(const void *in_nhwc, void *ws, int64_t ws_bytes, int64
         return IM2WIN_EOVERLAP;
     if (ws_bytes < workspace_bytes(sh, (int)dt))
         return IM2WIN_EWORKSPACE;
+    Tuning tu;
+    if ((rc = read_tuning(&tu)) != IM2WIN_OK)
+        return rc;
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
-    return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream));
+    return launch_status(launch_transform(sh, in_nhwc, ws, (hipStream_t)hip_stream, tu));
 }
 
 int conv_im2win_transform_padded(const void *in_nhwc, void *ws, int64_t ws_bytes, int64_t N,
@@ -412,12 +421,17 @@ int conv16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico, uint16_t *
         return IM2WIN_EOVERLAP;
     if (ws_bytes < workspace_bytes(sh, dt))
         return IM2WIN_EWORKSPACE;
+    Tuning tu;
+    Plan16 plan;
+    if ((rc = read_tuning(&tu)) != IM2WIN_OK || (rc = plan_fp16(sh, tu, &plan)) != IM2WIN_OK)
+        return rc;
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
     void *packed = (char *)ws + sh.pad_end;
-    if ((rc = launch_status(launch_pack_fp16(sh, filt_khkwcico, packed, (hipStream_t)hip_stream))) != IM2WIN_OK)
+    const hipStream_t st = (hipStream_t)hip_stream;
+    if ((rc = launch_status(launch_pack_fp16(sh, plan, filt_khkwcico, packed, st))) != IM2WIN_OK)
         return rc;
-    return launch_status(launch_conv_fp16(sh, ws, packed, out_nhwc, (hipStream_t)hip_stream, op));
+    return launch_status(launch_conv_fp16(sh, plan, tu, ws, packed, out_nhwc, st, op));
 }
 
 }  // namespace
@@ -456,6 +470,38 @@ int conv_im2win_dilated(void *ws, int64_t ws_bytes, const void *filt_khkwcico, v
     default:
         return IM2WIN_EINVAL;
     }
+}
+
+int conv_im2win_kernel_name(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h,
+                            int64_t K_w, int64_t stride, int64_t dilation, im2win_dtype_t dt, int fp32_matrix_cores,
+                            char *buf, int64_t buf_len)
+{
+    if (!buf || buf_len < 1)
+        return IM2WIN_EINVAL;
+    buf[0] = 0;
+    Shape sh;
+    int rc = make_shape_dil(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dilation, (int)dt, &sh);
+    if (rc != IM2WIN_OK)
+        return rc;
+    Tuning tu;
+    if ((rc = read_tuning(&tu)) != IM2WIN_OK)
+        return rc;
+    char name[64];
+    if (dt == IM2WIN_F32) {
+        Plan32 p;
+        if ((rc = plan_fp32(sh, tu, fp32_matrix_cores != 0, &p)) != IM2WIN_OK)
+            return rc;
+        plan32_name(sh, p, name, (int)sizeof name);
+    } else {
+        Plan16 p;
+        if ((rc = plan_fp16(sh, tu, &p)) != IM2WIN_OK)
+            return rc;
+        plan16_name(sh, p, name, (int)sizeof name);
+    }
+    if ((int64_t)strlen(name) >= buf_len)
+        return IM2WIN_ERANGE;
+    strcpy(buf, name);
+    return IM2WIN_OK;
 }
 
 const char *conv_im2win_strerror(int status)

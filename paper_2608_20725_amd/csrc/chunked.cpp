@@ -6,9 +6,12 @@
 // stream, alternate chunks run on the two streams, so two chunks are in flight
 // and the transform of one overlaps the convolution of the other.
 //
-// Every chunk is convolved by the same kernels, in the same summation order, as
-// the full batch would be, so the output is bit-identical to the full-batch
-// entry points.
+// The kernel plan is made once, from the shape of a full chunk, and used for the
+// filter pack and for every chunk, the last (possibly smaller) one included, so
+// the packed filter always has the layout the kernel reads.  The output equals,
+// bit for bit, that of the full-batch entry points run on a chunk-sized batch;
+// against a full-batch call it may differ in the last bits where the larger
+// batch selects another kernel (another summation order).
 #include "common.hpp"
 
 #include "../../include/im2win.h"
@@ -50,28 +53,61 @@ int make_plan(int64_t N, int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int
     return IM2WIN_OK;
 }
 
-// Events for ordering the two streams, kept per host thread and device
-// (created on first use, reused by every later call from that thread).
-struct Events {
-    hipEvent_t start = nullptr, done = nullptr;
-    bool ready = false;
-};
-
-int events_for_device(Events **out)
+// Enqueues the filter pack and every chunk (arguments checked by the caller).
+int enqueue_chunks(const void *in, const void *filt, void *out, char *wsb, const Plan &p, const Plan16 &p16,
+                   const Plan32 &p32, const Tuning &tu, int64_t N, int64_t C_i, int64_t H_i, int64_t W_i,
+                   int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, int dt, hipStream_t st, hipStream_t aux,
+                   hipEvent_t ev_start, hipEvent_t ev_done)
 {
-    constexpr int kMaxDev = 64;
-    static thread_local Events ev[kMaxDev];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev)
-        return IM2WIN_ENODEV;
-    Events &e = ev[dev];
-    if (!e.ready) {
-        if (hipEventCreateWithFlags(&e.start, hipEventDisableTiming) != hipSuccess ||
-            hipEventCreateWithFlags(&e.done, hipEventDisableTiming) != hipSuccess)
+    int rc;
+    Shape full;
+    make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dt, &full);
+    const int64_t elt = full.elt;
+    void *packed = wsb + p.packed_off;
+    // the filter is packed once, for the plan every chunk runs
+    if (dt == IM2WIN_F32)
+        rc = launch_status(launch_pack_fp32(p.chunk, p32, static_cast<const float *>(filt), packed, st));
+    else
+        rc = launch_status(launch_pack_fp16(p.chunk, p16, static_cast<const uint16_t *>(filt), packed, st));
+    if (rc != IM2WIN_OK)
+        return rc;
+    // With two streams, chunk c runs (transform, then conv) on stream c % 2
+    // in slot c % 2: two chunks are in flight at once, the transform of one
+    // overlapping the conv of the other, and a slot is reused only by later
+    // work on the same stream.  The aux stream starts after everything already
+    // queued on `st` (the input, the packed filter, earlier users of this
+    // workspace) and `st` finally waits for the aux stream.
+    if (aux != nullptr) {
+        if (hipEventRecord(ev_start, st) != hipSuccess || hipStreamWaitEvent(aux, ev_start, 0) != hipSuccess)
             return IM2WIN_ELAUNCH;
-        e.ready = true;
     }
-    *out = &e;
+    const int64_t in_img = H_i * W_i * C_i * elt, out_img = full.Ho * full.Wo * C_o * elt;
+    const int64_t nchunks = (N + p.n_chunk - 1) / p.n_chunk;
+    for (int64_t c = 0; c < nchunks; ++c) {
+        const int64_t i0 = c * p.n_chunk;
+        const int64_t n = N - i0 < p.n_chunk ? N - i0 : p.n_chunk;
+        Shape sh = p.chunk;
+        if (n != p.n_chunk)
+            make_shape(n, C_i, H_i, W_i, C_o, K_h, K_w, stride, dt, &sh);
+        const int slot = (int)(c % p.nslots);
+        char *wsl = wsb + slot * p.slot_bytes;
+        const char *inc = static_cast<const char *>(in) + i0 * in_img;
+        char *outc = static_cast<char *>(out) + i0 * out_img;
+        hipStream_t cs = (aux != nullptr && slot == 1) ? aux : st;
+        if ((rc = launch_status(launch_transform(sh, inc, wsl, cs, tu))) != IM2WIN_OK)
+            return rc;
+        if (dt == IM2WIN_F32)
+            rc = launch_status(launch_conv_fp32(sh, p32, tu, wsl, packed, reinterpret_cast<float *>(outc), cs));
+        else
+            rc = launch_status(launch_conv_fp16(sh, p16, tu, wsl, packed, reinterpret_cast<uint16_t *>(outc), cs,
+                                                dt == IM2WIN_BF16 ? Op16::BF16 : Op16::F16));
+        if (rc != IM2WIN_OK)
+            return rc;
+    }
+    if (aux != nullptr) {
+        if (hipEventRecord(ev_done, aux) != hipSuccess || hipStreamWaitEvent(st, ev_done, 0) != hipSuccess)
+            return IM2WIN_ELAUNCH;
+    }
     return IM2WIN_OK;
 }
 
@@ -105,59 +141,34 @@ int run_chunked(const void *in, const void *filt, void *out, void *ws, int64_t w
         return IM2WIN_EOVERLAP;
     if (ws_bytes < p.ws_bytes)
         return IM2WIN_EWORKSPACE;
+    Tuning tu;
+    Plan16 p16{};
+    Plan32 p32{};
+    if ((rc = read_tuning(&tu)) != IM2WIN_OK)
+        return rc;
+    if ((rc = dt == IM2WIN_F32 ? plan_fp32(p.chunk, tu, false, &p32) : plan_fp16(p.chunk, tu, &p16)) != IM2WIN_OK)
+        return rc;
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
-    Events *ev = nullptr;
-    if (aux != nullptr && (rc = events_for_device(&ev)) != IM2WIN_OK)
-        return rc;
-
-    char *wsb = static_cast<char *>(ws);
-    void *packed = wsb + p.packed_off;
-    // the filter is packed once; its layout does not depend on the batch size
-    if (dt == IM2WIN_F32)
-        rc = launch_status(launch_pack_fp32(p.chunk, static_cast<const float *>(filt), packed, st));
-    else
-        rc = launch_status(launch_pack_fp16(p.chunk, static_cast<const uint16_t *>(filt), packed, st));
-    if (rc != IM2WIN_OK)
-        return rc;
-    // With two streams, chunk c runs (transform, then conv) on stream c % 2
-    // in slot c % 2: two chunks are in flight at once, the transform of one
-    // overlapping the conv of the other, and a slot is reused only by later
-    // work on the same stream.  The aux stream starts after everything already
-    // queued on `st` (the input, the packed filter, earlier users of this
-    // workspace) and `st` finally waits for the aux stream.
+    // Two events order the streams; they are made here and released at the
+    // end of the call (a recorded event that is destroyed is released once
+    // it completes, and the waits already enqueued on it stay in force).
+    hipEvent_t ev_start = nullptr, ev_done = nullptr;
     if (aux != nullptr) {
-        if (hipEventRecord(ev->start, st) != hipSuccess || hipStreamWaitEvent(aux, ev->start, 0) != hipSuccess)
-            return IM2WIN_ELAUNCH;
+        if (hipEventCreateWithFlags(&ev_start, hipEventDisableTiming) != hipSuccess)
+            return launch_status(hipErrorOutOfMemory);
+        if (hipEventCreateWithFlags(&ev_done, hipEventDisableTiming) != hipSuccess) {
+            (void)hipEventDestroy(ev_start);
+            return launch_status(hipErrorOutOfMemory);
+        }
     }
-    const int64_t in_img = H_i * W_i * C_i * elt, out_img = full.Ho * full.Wo * C_o * elt;
-    const int64_t nchunks = (N + p.n_chunk - 1) / p.n_chunk;
-    for (int64_t c = 0; c < nchunks; ++c) {
-        const int64_t i0 = c * p.n_chunk;
-        const int64_t n = N - i0 < p.n_chunk ? N - i0 : p.n_chunk;
-        Shape sh = p.chunk;
-        if (n != p.n_chunk)
-            make_shape(n, C_i, H_i, W_i, C_o, K_h, K_w, stride, dt, &sh);
-        const int slot = (int)(c % p.nslots);
-        char *wsl = wsb + slot * p.slot_bytes;
-        const char *inc = static_cast<const char *>(in) + i0 * in_img;
-        char *outc = static_cast<char *>(out) + i0 * out_img;
-        hipStream_t cs = (aux != nullptr && slot == 1) ? aux : st;
-        if ((rc = launch_status(launch_transform(sh, inc, wsl, cs))) != IM2WIN_OK)
-            return rc;
-        if (dt == IM2WIN_F32)
-            rc = launch_status(launch_conv_fp32(sh, wsl, packed, reinterpret_cast<float *>(outc), cs));
-        else
-            rc = launch_status(launch_conv_fp16(sh, wsl, packed, reinterpret_cast<uint16_t *>(outc), cs,
-                                                dt == IM2WIN_BF16 ? Op16::BF16 : Op16::F16));
-        if (rc != IM2WIN_OK)
-            return rc;
-    }
+    rc = enqueue_chunks(in, filt, out, static_cast<char *>(ws), p, p16, p32, tu, N, C_i, H_i, W_i, C_o, K_h, K_w,
+                        stride, dt, st, aux, ev_start, ev_done);
     if (aux != nullptr) {
-        if (hipEventRecord(ev->done, aux) != hipSuccess || hipStreamWaitEvent(st, ev->done, 0) != hipSuccess)
-            return IM2WIN_ELAUNCH;
+        (void)hipEventDestroy(ev_start);
+        (void)hipEventDestroy(ev_done);
     }
-    return IM2WIN_OK;
+    return rc;
 }
 
 }  // namespace

@@ -107,9 +107,9 @@ struct TileGrid {
     }
 };
 
-// gx * gy tiles (< 2^31, the caller's grid checks); IM2WIN_TILE_ORDER=linear
-// selects the launch order (to measure what the XCD-aware order gains).
-TileGrid make_tilegrid(int64_t gx, int64_t gy);
+// gx * gy tiles (< 2^31, the caller's grid checks); `linear` selects the
+// launch order (to measure what the XCD-aware order gains).
+TileGrid make_tilegrid(int64_t gx, int64_t gy, bool linear);
 
 inline WinCols make_wincols(const Shape &sh)
 {
@@ -145,6 +145,22 @@ __device__ inline uint32_t ld_b32(__amdgpu_buffer_rsrc_t r, uint32_t off)
     return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
 }
 
+// Workgroup barrier of the load rings.  It does not wait for outstanding
+// global loads (__syncthreads() would, and a ring would hold only one stage
+// in flight); it does wait for this wave's outstanding LDS reads
+// (lgkmcnt(0)).  The barrier is what hands a slot that has just been read
+// to the next stage's direct-to-LDS loads, and the compiler may sink the
+// last matrix operations of a stage, with the wait for their operands,
+// below it: a read still in flight there can return the next stage's bytes.
+// simm16: vmcnt 63 (bits 3:0 and 15:14, no wait), expcnt 7 (no wait), lgkmcnt 0.
+__device__ inline void ring_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 __device__ inline uint32_t ld_b16(__amdgpu_buffer_rsrc_t r, uint32_t off)
 {
     return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
@@ -168,9 +184,66 @@ int check_device();
 int launch_status(hipError_t e);
 }  // namespace im2win
 
-// Kernel launchers (one per translation unit).  Each returns a hipError_t from
-// the launch itself; the shape has been validated.
+// Tuning overrides, read from the environment once per call and checked:
+// a value that names no kernel makes the call fail with IM2WIN_EINVAL, and
+// so does a kernel forced onto a layer it cannot run.  They exist to measure
+// the kernels against each other (the ablation of the paper's techniques);
+// without them every layer runs the kernel its shape selects.
+//   IM2WIN_FP16_KERNEL     pipe (row-per-pixel kernels) | regs (register-staged)
+//   IM2WIN_FP16_COL        a column-staged variant name
+//   IM2WIN_FP16_TILE       a row-per-pixel tile name (implies pipe)
+//   IM2WIN_FP16_SEG        a segment-staged variant name
+//   IM2WIN_FP32_KERNEL     a DMA-staged variant name | regs
+//   IM2WIN_FP32_TILE       a register-staged tile name (implies regs)
+//   IM2WIN_FP32_MFMA_TILE  a matrix-core fp32 tile name
+//   IM2WIN_TRANSFORM_ORDER linear | xcd
+//   IM2WIN_TILE_ORDER      linear | xcd
 namespace im2win {
+
+struct Tuning {
+    enum { kAuto = 0, kPipe = 1, kRegs = 2 };
+    int fp16_kernel;                   // kAuto, kPipe, kRegs
+    int fp16_col, fp16_tile, fp16_seg; // variant index, -1: not forced
+    int fp32_kernel;                   // DMA variant index, -1: not forced, -2: register-staged kernel
+    int fp32_tile;                     // register-staged tile index, -1: not forced
+    int fp32_mfma_tile;                // -1: not forced
+    bool transform_linear, tile_linear;
+};
+int read_tuning(Tuning *t);
+
+// Variant tables of each kernel family: index of a name, -1 if none.
+int col_find(const char *name);
+int pipe_find(const char *name);
+int seg_find(const char *name);
+int dma32_find(const char *name);
+int regs32_find(const char *name);
+int mfma32_find(const char *name);
+
+// The kernel one conv call runs, chosen once on the host from the layer and
+// the tuning variables, and handed to both the filter pack and the conv
+// launch (the packed-filter layout follows the kernel).  A plan chosen for a
+// layer of N images also runs any layer that differs only in having fewer
+// images (the fit checks do not grow as N shrinks), which the mini-batch
+// path relies on.
+enum class Fam16 { Col, Pipe, Seg, Regs };
+struct Plan16 {
+    Fam16 fam;
+    int v;  // variant index within the family (Regs: 0..2 tile by C_o)
+};
+enum class Fam32 { Dma, Regs, Mfma };
+struct Plan32 {
+    Fam32 fam;
+    int v;  // variant or tile index within the family
+};
+// IM2WIN_OK, or IM2WIN_EINVAL for a forced kernel that cannot run the layer.
+int plan_fp16(const Shape &sh, const Tuning &t, Plan16 *p);
+int plan_fp32(const Shape &sh, const Tuning &t, bool mfma, Plan32 *p);
+// "family variant", e.g. "conv_fp16_col k3c64p128t32s2"; at most 63 characters.
+void plan16_name(const Shape &sh, const Plan16 &p, char *buf, int len);
+void plan32_name(const Shape &sh, const Plan32 &p, char *buf, int len);
+
+// Kernel launchers.  Each returns a hipError_t from the launch itself; the
+// shape has been validated and the plan made for it.
 // The gather form of the transform indexes elements with 32 bits.
 bool transform_range_ok(const Shape &sh);
 // Zero padding folded into the transform: the Shape describes the padded
@@ -179,40 +252,58 @@ bool transform_range_ok(const Shape &sh);
 struct Pad {
     int64_t Hi, Wi, ph, pw;
 };
-hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st,
+hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st, const Tuning &t,
                             const Pad *pad = nullptr);
-hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hipStream_t st);
-hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed, float *out,
-                            hipStream_t st);
+hipError_t launch_pack_fp32(const Shape &sh, const Plan32 &p, const float *filt, void *packed, hipStream_t st);
+// Dma and Regs plans (Mfma plans pack and launch through launch_conv_fp32_mfma).
+hipError_t launch_conv_fp32(const Shape &sh, const Plan32 &p, const Tuning &t, const void *ws,
+                            const void *packed, float *out, hipStream_t st);
 // fp32 on the matrix cores: whether the layer can run there (C_i a multiple
 // of 4, offsets in range), the bytes of its packed filter, and the launch
 // (filter pack, then conv).
 bool fp32_mfma_ok(const Shape &sh);
+int mfma32_default(const Shape &sh);
 int64_t fp32_mfma_packed_bytes(const Shape &sh);
-hipError_t launch_conv_fp32_mfma(const Shape &sh, const float *filt, void *packed, float *out, const void *ws,
-                                 hipStream_t st);
-// fp32 kernel with stages loaded straight into LDS: the variant for this
-// layer, or -1 when the register-staged kernel runs instead.
-int dma32_plan(const Shape &sh);
-hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const void *ws, const void *packed,
+hipError_t launch_conv_fp32_mfma(const Shape &sh, const Plan32 &p, const Tuning &t, const float *filt,
+                                 void *packed, float *out, const void *ws, hipStream_t st);
+// DMA-staged fp32 kernel (stages loaded straight into LDS): the default
+// variant for this layer, or -1 when the register-staged kernel runs; and
+// whether a variant can run the layer.
+int dma32_default(const Shape &sh);
+bool dma32_fits(const Shape &sh, int v);
+const char *dma32_name(int v);
+hipError_t launch_conv_fp32_dma(const Shape &sh, int v, const Tuning &t, const void *ws, const void *packed,
                                 float *out, hipStream_t st);
+// Register-staged fp32 kernel: whether a tile can run the layer, its name.
+bool regs32_fits(const Shape &sh, int v);
+const char *regs32_name(int v);
+const char *mfma32_name(int v);
 // Operand type of the 16-bit matrix-core kernels (every one of them is
 // instantiated for both).
 enum class Op16 { F16, BF16 };
-hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed, hipStream_t st);
-hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed, uint16_t *out,
-                            hipStream_t st, Op16 op);
-// Column-staged fp16 kernel: the variant for this layer, or -1 when the
-// row-per-pixel kernels run instead.  The filter pack layout follows it.
-int col_plan(const Shape &sh);
+hipError_t launch_pack_fp16(const Shape &sh, const Plan16 &p, const uint16_t *filt, void *packed,
+                            hipStream_t st);
+hipError_t launch_conv_fp16(const Shape &sh, const Plan16 &p, const Tuning &t, const void *ws,
+                            const void *packed, uint16_t *out, hipStream_t st, Op16 op);
+// Column-staged fp16 kernel: the default variant for this layer (-1: the
+// row-per-pixel kernels run), whether a variant can run it, its name and
+// taps per stage (the packed-filter tile).
+int col_default(const Shape &sh);
+bool col_fits(const Shape &sh, int v);
+const char *col_name(int v);
+int col_stage_taps(int v);
 // The layer runs the one-slot row-per-pixel fp16 kernel (many tiles, C_o >= 128).
 bool fp16_single_slot_rows(const Shape &sh);
-int col_stage_taps(int plan);  // taps per stage of that variant (packed-filter tile)
 // Segment-staged fp16 kernel for windows that are not 16-byte aligned: the
-// variant for this layer, or -1 when the register-staged kernel runs.
-int seg_plan(const Shape &sh);
-hipError_t launch_conv_fp16_seg(const Shape &sh, int plan, const void *ws, const void *packed,
+// default variant (-1: the register-staged kernel runs), fit, name.
+int seg_default(const Shape &sh);
+bool seg_fits(const Shape &sh, int v);
+const char *seg_name(int v);
+hipError_t launch_conv_fp16_seg(const Shape &sh, int v, const void *ws, const void *packed,
                                 uint16_t *out, hipStream_t st, Op16 op);
-hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const void *packed,
+hipError_t launch_conv_fp16_col(const Shape &sh, int v, const Tuning &t, const void *ws, const void *packed,
                                 uint16_t *out, hipStream_t st, Op16 op);
+// Row-per-pixel fp16 tiles: default for the layer, name.
+int pipe_default(const Shape &sh);
+const char *pipe_name(int v);
 } // namespace im2win

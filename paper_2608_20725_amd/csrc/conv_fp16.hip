@@ -357,18 +357,6 @@ __device__ inline void wait_vmcnt()
 
 typedef __attribute__((address_space(3))) void *lds_ptr;
 
-// Workgroup barrier for the ring.  __syncthreads() carries a release fence
-// that waits for every outstanding memory operation, including the stages
-// still in flight, which would collapse the ring to one stage; the explicit
-// vmcnt wait before it already covers the stage about to be read.  The empty
-// asm statements keep the compiler from moving LDS accesses across it.
-__device__ inline void ring_barrier()
-{
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
 __device__ inline uint32_t rsw(uint32_t r) { return (r ^ (r >> 3)) & 7u; }
 
 // State of one workgroup of the pipelined kernel.  Ring slots are separate
@@ -643,32 +631,55 @@ bool fp16_single_slot_rows(const Shape &sh)
     return sh.Ci % 8 == 0 && sh.Co >= 128 && tiles >= 1024;
 }
 
-namespace {
-
-// IM2WIN_FP16_KERNEL=regs: the register-staged kernel on every layer (the
-// ablation of direct-to-LDS loads); the filter pack follows it.
-bool regs_forced()
+int pipe_find(const char *name)
 {
-    const char *e = getenv("IM2WIN_FP16_KERNEL");
-    return e && strcmp(e, "regs") == 0;
+    int n;
+    const PipeVariant *v = pipe_variants(&n);
+    for (int t = 0; t < n; ++t)
+        if (strcmp(name, v[t].name) == 0)
+            return t;
+    return -1;
 }
 
-}  // namespace
+const char *pipe_name(int v)
+{
+    int n;
+    return pipe_variants(&n)[v].name;
+}
 
-hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed, hipStream_t st)
+int pipe_default(const Shape &sh)
+{
+    // Defaults, measured per layer on MI355X: shapes that leave LDS for
+    // two workgroups per CU (32x128, 64x128, 128x128); 64x128 also when a
+    // 128x128 grid would give fewer workgroups than CUs (S11: 280 vs 220
+    // TFLOP/s); 256x256 over eight waves when its grid fills 128 to 256
+    // CUs (cfg4 616 vs 575, S4 670 vs 646; with fewer tiles it starves
+    // the chip, with more the second round runs partly empty).
+    auto tiles = [&](int64_t bm, int64_t bn) { return ((sh.P + bn - 1) / bn) * ((sh.Co + bm - 1) / bm); };
+    if (sh.Co <= 32)
+        return pipe_find("c32p128s3");
+    if (fp16_single_slot_rows(sh))
+        return pipe_find("c128p128s1");
+    if (sh.Co <= 64 || tiles(128, 128) < 256)
+        return pipe_find("c64p128s3");
+    if (tiles(256, 256) >= 128 && tiles(256, 256) <= 256 && sh.Co >= 256)
+        return pipe_find("c256p256s2w8");
+    return pipe_find("c128p128s2");
+}
+
+hipError_t launch_pack_fp16(const Shape &sh, const Plan16 &p, const uint16_t *filt, void *packed, hipStream_t st)
 {
     PackArgs a;
     a.filt = filt;
     a.packed = static_cast<uint16_t *>(packed);
-    const int plan = col_plan(sh);
-    if (plan >= 0) {
+    if (p.fam == Fam16::Col) {
         a.nv = (uint32_t)sh.Kw; a.tlen = (uint32_t)(sh.Kh * sh.Ci); a.tpad = (uint32_t)sh.Tp;
-        a.tb = (uint32_t)col_stage_taps(plan);
+        a.tb = (uint32_t)col_stage_taps(p.v);
     } else {
         a.nv = 1; a.tlen = (uint32_t)sh.K; a.tpad = (uint32_t)sh.K_pad;
         // pipelined and segment-staged kernels: 64-tap tiles; register-staged
         // kernel: one tile of K_pad taps
-        a.tb = ((sh.Ci % 8 == 0 && !regs_forced()) || seg_plan(sh) >= 0) ? (uint32_t)BK : a.tpad;
+        a.tb = p.fam == Fam16::Regs ? a.tpad : (uint32_t)BK;
     }
     a.grans = (uint64_t)sh.Co_pad * a.nv * a.tpad / 8;
     a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad;
@@ -680,12 +691,13 @@ hipError_t launch_pack_fp16(const Shape &sh, const uint16_t *filt, void *packed,
     return hipLaunchKernel((const void *)&pack_filter_fp16, dim3((uint32_t)blocks), dim3(256), args, 0, st);
 }
 
-hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed, uint16_t *out,
-                            hipStream_t st, Op16 op)
+hipError_t launch_conv_fp16(const Shape &sh, const Plan16 &p, const Tuning &t, const void *ws,
+                            const void *packed, uint16_t *out, hipStream_t st, Op16 op)
 {
-    const int plan = col_plan(sh);
-    if (plan >= 0)
-        return launch_conv_fp16_col(sh, plan, ws, packed, out, st, op);
+    if (p.fam == Fam16::Col)
+        return launch_conv_fp16_col(sh, p.v, t, ws, packed, out, st, op);
+    if (p.fam == Fam16::Seg)
+        return launch_conv_fp16_seg(sh, p.v, ws, packed, out, st, op);
     C16Args a;
     a.ws = static_cast<const uint16_t *>(ws);
     a.packed = static_cast<const uint16_t *>(packed);
@@ -697,66 +709,29 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
     a.Co = (uint32_t)sh.Co; a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.wc = make_wincols(sh);
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     void *args[] = {&a};
-    // every window starts on a 16-byte boundary (unless the register-staged
-    // kernel is forced)
-    const bool aligned = (sh.Ci % 8) == 0 && !regs_forced();
-    if (aligned) {
+    if (p.fam == Fam16::Pipe) {
         int n;
-        const PipeVariant *v = pipe_variants(&n);
-        // Defaults, measured per layer on MI355X: shapes that leave LDS for
-        // two workgroups per CU (32x128, 64x128, 128x128); 64x128 also when a
-        // 128x128 grid would give fewer workgroups than CUs (S11: 280 vs 220
-        // TFLOP/s); 256x256 over eight waves when its grid fills 128 to 256
-        // CUs (cfg4 616 vs 575, S4 670 vs 646; with fewer tiles it starves
-        // the chip, with more the second round runs partly empty).
-        auto find = [&](const char *name) {
-            for (int t = 0; t < n; ++t)
-                if (strcmp(name, v[t].name) == 0)
-                    return t;
-            return 0;
-        };
-        auto tiles = [&](int64_t bm, int64_t bn) { return ((sh.P + bn - 1) / bn) * ((sh.Co + bm - 1) / bm); };
-        int pick;
-        if (sh.Co <= 32)
-            pick = find("c32p128s3");
-        else if (fp16_single_slot_rows(sh))
-            pick = find("c128p128s1");
-        else if (sh.Co <= 64 || tiles(128, 128) < 256)
-            pick = find("c64p128s3");
-        else if (tiles(256, 256) >= 128 && tiles(256, 256) <= 256 && sh.Co >= 256)
-            pick = find("c256p256s2w8");
-        else
-            pick = find("c128p128s2");
-        // IM2WIN_FP16_TILE=<name> overrides the tile shape (for tuning).
-        if (const char *e = getenv("IM2WIN_FP16_TILE")) {
-            for (int t = 0; t < n; ++t)
-                if (strcmp(e, v[t].name) == 0)
-                    pick = t;
-        }
-        const PipeVariant &p = v[pick];
-        const int64_t gx = (sh.P + p.bn - 1) / p.bn, gy = (sh.Co + p.bm - 1) / p.bm;
+        const PipeVariant &v = pipe_variants(&n)[p.v];
+        const int64_t gx = (sh.P + v.bn - 1) / v.bn, gy = (sh.Co + v.bm - 1) / v.bm;
         if (gx * gy > 0x7fffffff)
             return hipErrorInvalidValue;
-        a.tg = make_tilegrid(gx, gy);
-        return hipLaunchKernel(p.f[op == Op16::BF16], dim3((uint32_t)(gx * gy)), dim3(p.nt), args, 0, st);
+        a.tg = make_tilegrid(gx, gy, t.tile_linear);
+        return hipLaunchKernel(v.f[op == Op16::BF16], dim3((uint32_t)(gx * gy)), dim3(v.nt), args, 0, st);
     }
-    const int sp = seg_plan(sh);
-    if (sp >= 0)
-        return launch_conv_fp16_seg(sh, sp, ws, packed, out, st, op);
     const void *f;
     int bm, bn;
     const bool unal = sh.K >= 128;
     if (op == Op16::BF16) {
-        if (sh.Co <= 32)
+        if (p.v == 0)
             pick_regs<BF16Op, 1, 2, 1, 4>(unal, &f, &bm, &bn);
-        else if (sh.Co <= 64)
+        else if (p.v == 1)
             pick_regs<BF16Op, 2, 2, 1, 4>(unal, &f, &bm, &bn);
         else
             pick_regs<BF16Op, 2, 2, 2, 2>(unal, &f, &bm, &bn);
     } else {
-        if (sh.Co <= 32)
+        if (p.v == 0)
             pick_regs<F16Op, 1, 2, 1, 4>(unal, &f, &bm, &bn);
-        else if (sh.Co <= 64)
+        else if (p.v == 1)
             pick_regs<F16Op, 2, 2, 1, 4>(unal, &f, &bm, &bn);
         else
             pick_regs<F16Op, 2, 2, 2, 2>(unal, &f, &bm, &bn);
@@ -764,7 +739,7 @@ hipError_t launch_conv_fp16(const Shape &sh, const void *ws, const void *packed,
     const int64_t gx = (sh.P + bn - 1) / bn, gy = (sh.Co + bm - 1) / bm;
     if (gx * gy > 0x7fffffff)
         return hipErrorInvalidValue;
-    a.tg = make_tilegrid(gx, gy);
+    a.tg = make_tilegrid(gx, gy, t.tile_linear);
     return hipLaunchKernel(f, dim3((uint32_t)(gx * gy)), dim3(256), args, 0, st);
 }
 

@@ -39,6 +39,7 @@
 
 #include <stdlib.h>
 #include <string.h>
+#include <type_traits>
 
 namespace im2win {
 namespace {
@@ -63,6 +64,7 @@ template <int KW_, int BT_, int WM_, int WN_, int WGM_, int WGN_, int NRMAX_, in
 struct ColCfg {
     static constexpr int KW = KW_, BT = BT_, WM = WM_, WN = WN_, WGM = WGM_, WGN = WGN_;
     static constexpr int NS = NS_;              // ring slots
+    static constexpr bool SERIAL = false;       // see Serialized
     static constexpr int NW = WGM * WGN;        // waves
     static constexpr int NT = 64 * NW;
     static constexpr int BM = 32 * WM * WGM;    // channels per tile
@@ -86,6 +88,16 @@ struct ColCfg {
     static_assert(AROWS % RPI == 0, "A and B rows meet at a block boundary");
 };
 
+// The same tile with its ring serialized: a stage's loads are issued only
+// after every wave has finished multiplying the previous stage, and waited
+// for in full, so no load is ever in flight while LDS is read.  Same sums in
+// the same order; a check variant for the ring's waits and barriers (its
+// output must match the ring's bit for bit).
+template <class Base>
+struct Serialized : Base {
+    static constexpr bool SERIAL = true;
+};
+
 template <class C>
 __device__ inline uint32_t sw(uint32_t r)
 {
@@ -96,16 +108,6 @@ template <int VM>
 __device__ inline void wait_vmcnt()
 {
     __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// Workgroup barrier that does not wait for outstanding memory operations
-// (__syncthreads() would also wait for the stage still in flight); the
-// explicit vmcnt wait before it covers the stage about to be read.
-__device__ inline void ring_barrier()
-{
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
 }
 
 // E: the operand type (F16Op or BF16Op).
@@ -178,6 +180,15 @@ struct ColTile {
     template <int N>
     __device__ inline void step(uint32_t st, char (&cur)[N], char (&next)[N])
     {
+        if constexpr (C::SERIAL) {
+            wait_vmcnt<0>();
+            ring_barrier();
+            if (st < nst)
+                compute(cur);
+            ring_barrier();
+            issue(st + C::NS - 1, next);
+            return;
+        }
         wait_vmcnt<(C::NS - 2) * C::IB>();
         ring_barrier();
         issue(st + C::NS - 1, next);
@@ -349,10 +360,11 @@ struct ColVariant {
     int kw, bm, bn, nrmax, bt, nt;
 };
 
-template <int KW, int BT, int WM, int WN, int WGM, int WGN, int NRMAX, int NS>
+template <int KW, int BT, int WM, int WN, int WGM, int WGN, int NRMAX, int NS, bool SERIAL = false>
 ColVariant col_variant(const char *name)
 {
-    using C = ColCfg<KW, BT, WM, WN, WGM, WGN, NRMAX, NS>;
+    using B = ColCfg<KW, BT, WM, WN, WGM, WGN, NRMAX, NS>;
+    using C = typename std::conditional<SERIAL, Serialized<B>, B>::type;
     return ColVariant{name, {(const void *)&conv_fp16_col<C, F16Op>, (const void *)&conv_fp16_col<C, BF16Op>}, KW,
                       C::BM, C::BN, NRMAX, BT, C::NT};
 }
@@ -369,6 +381,10 @@ const ColVariant *col_variants(int *n)
         // eight waves, 256 x 256 tiles (large C_o)
         col_variant<3, 32, 4, 2, 2, 4, 320, 2>("k3c256p256t32s2w8"),
         col_variant<3, 32, 2, 3, 4, 2, 256, 2>("k3c256p192t32s2w8"),
+        // serialized rings of three of the above (check variants)
+        col_variant<3, 32, 1, 2, 2, 2, 160, 2, true>("k3c64p128t32s2-serial"),
+        col_variant<7, 16, 2, 2, 1, 4, 544, 3, true>("k7c64p256t16s3-serial"),
+        col_variant<3, 32, 2, 3, 4, 2, 256, 2, true>("k3c256p192t32s2w8-serial"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
@@ -388,76 +404,88 @@ int64_t col_rows_needed(const Shape &sh, int bn)
 
 }  // namespace
 
-int col_plan(const Shape &sh)
+int col_find(const char *name)
 {
-    if (sh.Ci % 8 != 0)
-        return -1;  // windows not 16-byte aligned
-    if (sh.d != 1)
-        return -1;  // the column table assumes consecutive strip columns
-    if (const char *e = getenv("IM2WIN_FP16_KERNEL"))
-        if (strcmp(e, "pipe") == 0 || strcmp(e, "regs") == 0)
-            return -1;
     int n;
     const ColVariant *v = col_variants(&n);
-    int pick = -1;
-    if (const char *e = getenv("IM2WIN_FP16_COL")) {
-        for (int t = 0; t < n; ++t)
-            if (strcmp(e, v[t].name) == 0)
-                pick = t;
-    }
-    if (pick < 0) {
-        // Defaults, measured per layer on MI355X: the column-staged kernel
-        // wins where the window rows dominate a stage (C_o <= 128); with
-        // more channels the K_w*BM filter rows of a stage dominate it and the
-        // row-per-pixel kernel, whose stages hold 64 taps of BM filter rows,
-        // is faster.
-        // With C_o > 128 the eight-wave 256-channel variants (whose filter
-        // rows arrive as one contiguous run per stage) beat the row kernel
-        // when their grid fills most of the 256 CUs in one round: cfg4 (192
-        // tiles of 256 x 192) 808 vs 633 TFLOP/s; with ~100-130 tiles they
-        // lose (S5: 536 vs 636), so those layers keep the row kernel.
-        auto tiles = [&](int64_t bn) { return ((sh.P + bn - 1) / bn) * ((sh.Co + 255) / 256); };
-        const char *name = nullptr;
-        if (fp16_single_slot_rows(sh))
-            return -1;  // the one-slot row kernel is faster there
-        // C_o <= 64: 64 x 128 tiles, three workgroups per CU, more bytes in
-        // flight for these HBM-bound layers (3x3 C=64 at 56x56: 484 vs 431
-        // TFLOP/s same-process; with C_o = 128, 3x3 at 28x28, 531 vs 548)
-        if (sh.Kw == 3 && sh.Co <= 64)
-            name = "k3c64p128t32s2";
-        else if (sh.Kw == 3 && sh.Co <= 128)
-            name = "k3c64p256t32s2";
-        // 7x7: with stride 1 and C_o <= 64 the 64 x 128 tile (two-slot ring,
-        // 49 KiB, three workgroups per CU) measured 785 vs 713 TFLOP/s
-        // (7x7 C=64 at 60x60, 64 images); with stride 2 (7x7 C=64 at 224x224)
-        // it lost, 668 vs 701
-        else if (sh.Kw == 7 && sh.s == 1 && sh.Co <= 64)
-            name = "k7c64p128t16s2";
-        else if (sh.Kw == 7 && sh.Co <= 128)
-            name = "k7c64p256t16s3";
-        else if (sh.Kw == 3 && tiles(192) >= 160 && tiles(192) <= 256)
-            name = "k3c256p192t32s2w8";
-        else if (sh.Kw == 3 && tiles(256) >= 160 && tiles(256) <= 256)
-            name = "k3c256p256t32s2w8";
-        else
-            return -1;
-        for (int t = 0; t < n; ++t)
-            if (strcmp(name, v[t].name) == 0)
-                pick = t;
-    }
-    if (pick < 0 || v[pick].kw != sh.Kw)
-        return -1;
+    for (int t = 0; t < n; ++t)
+        if (strcmp(name, v[t].name) == 0)
+            return t;
+    return -1;
+}
+
+const char *col_name(int v)
+{
+    int n;
+    return col_variants(&n)[v].name;
+}
+
+bool col_fits(const Shape &sh, int pick)
+{
+    int n;
+    const ColVariant *v = col_variants(&n);
+    if (pick < 0 || pick >= n)
+        return false;
+    if (sh.Ci % 8 != 0)
+        return false;  // windows not 16-byte aligned
+    if (sh.d != 1)
+        return false;  // the column table assumes consecutive strip columns
+    if (v[pick].kw != sh.Kw)
+        return false;
     if (col_rows_needed(sh, v[pick].bn) > v[pick].nrmax)
-        return -1;
+        return false;
     // the packed filter is addressed with 31-bit offsets
     if (sh.Co_pad * sh.Kw * sh.Tp * 2 >= (int64_t)kMaxRecords)
-        return -1;
+        return false;
     // every offset inside a tile must fit 31 bits (checked per layer: the
     // strips of one tile plus the last column's slice)
     const int64_t strips_per_tile = (v[pick].bn - 1) / sh.Wo + 2;
     if ((strips_per_tile * sh.L + sh.Tp) * 2 >= (int64_t)kOOB)
+        return false;
+    return true;
+}
+
+int col_default(const Shape &sh)
+{
+    if (sh.Ci % 8 != 0 || sh.d != 1)
         return -1;
-    return pick;
+    // Defaults, measured per layer on MI355X: the column-staged kernel
+    // wins where the window rows dominate a stage (C_o <= 128); with
+    // more channels the K_w*BM filter rows of a stage dominate it and the
+    // row-per-pixel kernel, whose stages hold 64 taps of BM filter rows,
+    // is faster.
+    // With C_o > 128 the eight-wave 256-channel variants (whose filter
+    // rows arrive as one contiguous run per stage) beat the row kernel
+    // when their grid fills most of the 256 CUs in one round: cfg4 (192
+    // tiles of 256 x 192) 808 vs 633 TFLOP/s; with ~100-130 tiles they
+    // lose (S5: 536 vs 636), so those layers keep the row kernel.
+    auto tiles = [&](int64_t bn) { return ((sh.P + bn - 1) / bn) * ((sh.Co + 255) / 256); };
+    const char *name = nullptr;
+    if (fp16_single_slot_rows(sh))
+        return -1;  // the one-slot row kernel is faster there
+    // C_o <= 64: 64 x 128 tiles, three workgroups per CU, more bytes in
+    // flight for these HBM-bound layers (3x3 C=64 at 56x56: 484 vs 431
+    // TFLOP/s same-process; with C_o = 128, 3x3 at 28x28, 531 vs 548)
+    if (sh.Kw == 3 && sh.Co <= 64)
+        name = "k3c64p128t32s2";
+    else if (sh.Kw == 3 && sh.Co <= 128)
+        name = "k3c64p256t32s2";
+    // 7x7: with stride 1 and C_o <= 64 the 64 x 128 tile (two-slot ring,
+    // 49 KiB, three workgroups per CU) measured 785 vs 713 TFLOP/s
+    // (7x7 C=64 at 60x60, 64 images); with stride 2 (7x7 C=64 at 224x224)
+    // it lost, 668 vs 701
+    else if (sh.Kw == 7 && sh.s == 1 && sh.Co <= 64)
+        name = "k7c64p128t16s2";
+    else if (sh.Kw == 7 && sh.Co <= 128)
+        name = "k7c64p256t16s3";
+    else if (sh.Kw == 3 && tiles(192) >= 160 && tiles(192) <= 256)
+        name = "k3c256p192t32s2w8";
+    else if (sh.Kw == 3 && tiles(256) >= 160 && tiles(256) <= 256)
+        name = "k3c256p256t32s2w8";
+    else
+        return -1;
+    const int pick = col_find(name);
+    return col_fits(sh, pick) ? pick : -1;
 }
 
 int col_stage_taps(int plan)
@@ -466,7 +494,7 @@ int col_stage_taps(int plan)
     return col_variants(&n)[plan].bt;
 }
 
-hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const void *packed,
+hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const Tuning &t, const void *ws, const void *packed,
                                 uint16_t *out, hipStream_t st, Op16 op)
 {
     int n;
@@ -486,7 +514,7 @@ hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const void *ws, const
     const int64_t gx = (sh.P + v.bn - 1) / v.bn, gy = (sh.Co + v.bm - 1) / v.bm;
     if (gx * gy > 0x7fffffff)
         return hipErrorInvalidValue;
-    a.tg = make_tilegrid(gx, gy);
+    a.tg = make_tilegrid(gx, gy, t.tile_linear);
     void *args[] = {&a};
     return hipLaunchKernel(v.f[op == Op16::BF16], dim3((uint32_t)(gx * gy)), dim3(v.nt), args, 0, st);
 }

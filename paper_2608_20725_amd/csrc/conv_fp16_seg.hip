@@ -19,6 +19,8 @@
 #include "common.hpp"
 #include "epilogue16.hpp"
 
+#include <type_traits>
+
 #include <stdlib.h>
 #include <string.h>
 
@@ -47,6 +49,7 @@ struct SegCfg {
     static constexpr int BM = 32 * WM * WGM, BN = 32 * WN * WGN;
     static constexpr int GMAX = GMAX_;  // 16-byte granules of window segments a tile may need
     static constexpr int RMAX = RMAX_;  // strips a tile may touch
+    static constexpr bool SERIAL = false;  // see Serialized
     static constexpr int ASTAGE = BM * 128;        // filter rows of one stage
     static constexpr int IA = BM / 8 / NW;         // filter loads per wave per stage
     static constexpr int IBMAX = GMAX / 64 / NW;   // segment loads per wave, at most
@@ -56,19 +59,21 @@ struct SegCfg {
     static_assert(RMAX >= 2 && RMAX <= 64 && (RMAX & (RMAX - 1)) == 0, "one lane per strip, scanned in log2 steps");
 };
 
+// The same tile with the filter ring serialized: a stage's filter loads are
+// issued only after every wave has finished with the previous stage, so no
+// load is in flight while LDS is read.  Same sums in the same order; a check
+// variant for the ring's waits and barriers.
+template <class Base>
+struct Serialized : Base {
+    static constexpr bool SERIAL = true;
+};
+
 __device__ inline uint32_t rsw(uint32_t r) { return (r ^ (r >> 3)) & 7u; }
 
 template <int VM>
 __device__ inline void wait_vmcnt()
 {
     __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-__device__ inline void ring_barrier()
-{
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
 }
 
 // E: the operand type (F16Op or BF16Op).
@@ -255,18 +260,36 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_seg(SegArgs a)
     w.issue_a(0, r0);
     // two-slot filter ring: wait for stage st (and, at st = 0, the
     // segments), then load stage st+1 into the other slot, then multiply
-    for (uint32_t st = 0; st < w.nst; st += 2) {
-        wait_vmcnt<0>();
-        ring_barrier();
-        if (st + 1 < w.nst)
-            w.issue_a(st + 1, r1);
-        w.compute(st, r0, seg);
-        if (st + 1 < w.nst) {
+    if constexpr (C::SERIAL) {
+        for (uint32_t st = 0; st < w.nst; st += 2) {
             wait_vmcnt<0>();
             ring_barrier();
-            if (st + 2 < w.nst)
-                w.issue_a(st + 2, r0);
-            w.compute(st + 1, r1, seg);
+            w.compute(st, r0, seg);
+            ring_barrier();
+            if (st + 1 < w.nst) {
+                w.issue_a(st + 1, r1);
+                wait_vmcnt<0>();
+                ring_barrier();
+                w.compute(st + 1, r1, seg);
+                ring_barrier();
+                if (st + 2 < w.nst)
+                    w.issue_a(st + 2, r0);
+            }
+        }
+    } else {
+        for (uint32_t st = 0; st < w.nst; st += 2) {
+            wait_vmcnt<0>();
+            ring_barrier();
+            if (st + 1 < w.nst)
+                w.issue_a(st + 1, r1);
+            w.compute(st, r0, seg);
+            if (st + 1 < w.nst) {
+                wait_vmcnt<0>();
+                ring_barrier();
+                if (st + 2 < w.nst)
+                    w.issue_a(st + 2, r0);
+                w.compute(st + 1, r1, seg);
+            }
         }
     }
     wait_vmcnt<0>();
@@ -281,10 +304,11 @@ struct SegVariant {
     int bm, bn, gmax, rmax, nt;
 };
 
-template <int WM, int WN, int WGM, int WGN, int GMAX, int RMAX>
+template <int WM, int WN, int WGM, int WGN, int GMAX, int RMAX, bool SERIAL = false>
 SegVariant seg_variant(const char *name)
 {
-    using C = SegCfg<WM, WN, WGM, WGN, GMAX, RMAX>;
+    using B = SegCfg<WM, WN, WGM, WGN, GMAX, RMAX>;
+    using C = typename std::conditional<SERIAL, Serialized<B>, B>::type;
     return SegVariant{name, {(const void *)&conv_fp16_seg<C, F16Op>, (const void *)&conv_fp16_seg<C, BF16Op>}, C::BM,
                       C::BN, GMAX, RMAX, C::NT};
 }
@@ -296,6 +320,8 @@ const SegVariant *seg_variants(int *n)
         seg_variant<2, 2, 1, 4, 2560, 16>("s64p256"),
         seg_variant<3, 1, 1, 4, 2560, 16>("s96p128"),
         seg_variant<2, 2, 2, 2, 2560, 16>("s128p128"),
+        // serialized filter ring (check variant)
+        seg_variant<2, 2, 1, 4, 2560, 16, true>("s64p256-serial"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
@@ -319,34 +345,49 @@ int64_t seg_granules_needed(const Shape &sh, int bn, int64_t runs_max)
 
 }  // namespace
 
-int seg_plan(const Shape &sh)
+int seg_find(const char *name)
 {
-    if (sh.Ci % 8 == 0)
-        return -1;  // 16-byte-aligned windows have their own kernels
-    if (sh.d != 1)
-        return -1;  // strip segments assume windows s*K_h*C_i apart
-    if (const char *e = getenv("IM2WIN_FP16_KERNEL"))
-        if (strcmp(e, "regs") == 0)
-            return -1;
     int n;
     const SegVariant *v = seg_variants(&n);
-    int pick = sh.Co <= 64 ? 0 : sh.Co <= 96 ? 1 : 2;
-    if (const char *e = getenv("IM2WIN_FP16_SEG")) {
-        for (int t = 0; t < n; ++t)
-            if (strcmp(e, v[t].name) == 0)
-                pick = t;
-    }
+    for (int t = 0; t < n; ++t)
+        if (strcmp(name, v[t].name) == 0)
+            return t;
+    return -1;
+}
+
+const char *seg_name(int v)
+{
+    int n;
+    return seg_variants(&n)[v].name;
+}
+
+bool seg_fits(const Shape &sh, int pick)
+{
+    int n;
+    const SegVariant *v = seg_variants(&n);
+    if (pick < 0 || pick >= n)
+        return false;
+    if (sh.d != 1)
+        return false;  // strip segments assume windows s*K_h*C_i apart
     // strips a tile of bn pixels can touch, wherever it starts in a strip
     const int64_t runs = (v[pick].bn - 1 + sh.Wo - 1) / sh.Wo + 1;
     if (runs > v[pick].rmax || seg_granules_needed(sh, v[pick].bn, runs) > v[pick].gmax)
-        return -1;
+        return false;
     // byte offsets inside the tile's strips stay below the buffer limit, and
     // pixel indices of the strips after the tile's last one fit 32 bits
     if ((runs * sh.L + sh.K_pad + 8) * 2 >= (int64_t)kMaxRecords)
-        return -1;
+        return false;
     if (sh.P + (int64_t)v[pick].rmax * sh.Wo >= (int64_t)1 << 32)
-        return -1;
-    return pick;
+        return false;
+    return true;
+}
+
+int seg_default(const Shape &sh)
+{
+    if (sh.Ci % 8 == 0)
+        return -1;  // 16-byte-aligned windows have their own kernels
+    const int pick = sh.Co <= 64 ? 0 : sh.Co <= 96 ? 1 : 2;
+    return seg_fits(sh, pick) ? pick : -1;
 }
 
 hipError_t launch_conv_fp16_seg(const Shape &sh, int plan, const void *ws, const void *packed,

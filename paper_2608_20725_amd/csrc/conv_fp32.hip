@@ -480,7 +480,27 @@ const void *kernel_for(const Tile &t, int waves, bool v4)
 
 }  // namespace
 
-hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hipStream_t st)
+int regs32_find(const char *name)
+{
+    const int ntiles = (int)(sizeof kTiles / sizeof kTiles[0]);
+    for (int t = 0; t < ntiles; ++t)
+        if (strcmp(name, kTiles[t].name) == 0)
+            return t;
+    return -1;
+}
+
+const char *regs32_name(int v) { return kTiles[v].name; }
+
+bool regs32_fits(const Shape &sh, int v)
+{
+    const int ntiles = (int)(sizeof kTiles / sizeof kTiles[0]);
+    if (v < 0 || v >= ntiles)
+        return false;
+    // the LDS-filter tiles address the packed filter with 31-bit offsets
+    return kTiles[v].tp != 0 || sh.K_pad32 * sh.Co_pad32 * 4 <= (int64_t)kMaxRecords;
+}
+
+hipError_t launch_pack_fp32(const Shape &sh, const Plan32 &p, const float *filt, void *packed, hipStream_t st)
 {
     Pack32Args a;
     a.filt = filt;
@@ -488,7 +508,7 @@ hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hi
     a.quads = (uint64_t)sh.K_pad32 * sh.Co_pad32 / 4;
     a.K = (uint32_t)sh.K; a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
     a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
-    a.pair_swap = dma32_plan(sh) >= 0;  // the conv call picks its kernel by the same rule
+    a.pair_swap = p.fam == Fam32::Dma;  // the DMA-staged kernel reads channel pairs swapped
     uint64_t blocks = (a.quads + 255) / 256;
     if (blocks > 65536)
         blocks = 65536;
@@ -496,12 +516,11 @@ hipError_t launch_pack_fp32(const Shape &sh, const float *filt, void *packed, hi
     return hipLaunchKernel((const void *)&pack_filter_fp32, dim3((uint32_t)blocks), dim3(256), args, 0, st);
 }
 
-hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed, float *out,
-                            hipStream_t st)
+hipError_t launch_conv_fp32(const Shape &sh, const Plan32 &p, const Tuning &t, const void *ws,
+                            const void *packed, float *out, hipStream_t st)
 {
-    const int plan = dma32_plan(sh);
-    if (plan >= 0)
-        return launch_conv_fp32_dma(sh, plan, ws, packed, out, st);
+    if (p.fam == Fam32::Dma)
+        return launch_conv_fp32_dma(sh, p.v, t, ws, packed, out, st);
     C32Args a;
     a.ws = static_cast<const float *>(ws);
     a.packed = static_cast<const float *>(packed);
@@ -512,18 +531,7 @@ hipError_t launch_conv_fp32(const Shape &sh, const void *ws, const void *packed,
     a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.wc = make_wincols(sh);
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
 
-    const int ntiles = (int)(sizeof kTiles / sizeof kTiles[0]);
-    int ti = 0;
-    // IM2WIN_FP32_TILE=<name> overrides the tile (for tuning).
-    if (const char *e = getenv("IM2WIN_FP32_TILE")) {
-        for (int t = 0; t < ntiles; ++t)
-            if (strcmp(e, kTiles[t].name) == 0)
-                ti = t;
-    }
-    // the LDS-filter tiles address the packed filter with 31-bit offsets
-    if (kTiles[ti].tp == 0 && sh.K_pad32 * sh.Co_pad32 * 4 > (int64_t)kMaxRecords)
-        ti = kScalarTile;
-    const Tile &tile = kTiles[ti];
+    const Tile &tile = kTiles[p.v];
     // Channel groups per workgroup: the largest of 8, 4, 2, 1 waves (TN
     // channels each) that leaves no more idle channels than any smaller one.
     int waves = 1;

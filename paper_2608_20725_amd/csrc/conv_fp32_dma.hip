@@ -29,6 +29,8 @@
 // filter rows (padding), so they add exactly 0.
 #include "common.hpp"
 
+#include <type_traits>
+
 #include <stdlib.h>
 #include <string.h>
 
@@ -56,6 +58,7 @@ struct D32Args {
 template <int TM_, int TN_, int LC_, int WCH_, int NS_, int KC_ = 16, int GR_ = 16, int KS_ = 1, int NW_ = 4>
 struct DCfg {
     static constexpr int TM = TM_, TN = TN_, LC = LC_, WCH = WCH_, NS = NS_, KC = KC_;
+    static constexpr bool SERIAL = false;  // see Serialized
     // bytes one lane moves per window load: 16 when every window starts on a
     // 16-byte boundary (C_i a multiple of 4), else 4 (any fp32 window)
     static constexpr int GR = GR_;
@@ -96,19 +99,19 @@ struct DCfg {
     static_assert((NS - 2) * IB <= 63, "vmcnt range");
 };
 
+// The same tile with its ring serialized: a stage's loads are issued only
+// after every wave has finished with the previous stage, and waited for in
+// full, so no load is in flight while LDS is read.  Same sums in the same
+// order; a check variant for the ring's waits and barriers.
+template <class Base>
+struct Serialized : Base {
+    static constexpr bool SERIAL = true;
+};
+
 template <int VM>
 __device__ inline void wait_vmcnt()
 {
     __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// Workgroup barrier that leaves the stages in flight alone (__syncthreads()
-// would also wait for them); the explicit vmcnt wait covers the stage read.
-__device__ inline void ring_barrier()
-{
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
 }
 
 template <class C>
@@ -209,6 +212,15 @@ struct DTile {
     template <int N>
     __device__ inline void step(uint32_t st, char (&cur)[N], char (&next)[N])
     {
+        if constexpr (C::SERIAL) {
+            wait_vmcnt<0>();
+            ring_barrier();
+            if (st < nst)
+                compute(cur);
+            ring_barrier();
+            issue(st + C::NS - 1, next);
+            return;
+        }
         wait_vmcnt<(C::NS - 2) * C::IB>();
         ring_barrier();
         issue(st + C::NS - 1, next);
@@ -399,10 +411,11 @@ struct DVariant {
     int bm, cw, gr, nt;
 };
 
-template <int TM, int TN, int LC, int WCH, int NS, int KC, int GR = 16, int KS = 1, int NW = 4>
+template <int TM, int TN, int LC, int WCH, int NS, int KC, int GR = 16, int KS = 1, int NW = 4, bool SERIAL = false>
 DVariant d_variant(const char *name)
 {
-    using C = DCfg<TM, TN, LC, WCH, NS, KC, GR, KS, NW>;
+    using B = DCfg<TM, TN, LC, WCH, NS, KC, GR, KS, NW>;
+    using C = typename std::conditional<SERIAL, Serialized<B>, B>::type;
     return DVariant{name, (const void *)&conv_fp32_dma<C>, C::BM, C::CW, GR, C::NT};
 }
 
@@ -446,6 +459,10 @@ const DVariant *d_variants(int *n)
         d_variant<4, 8, 8, 1, 2, 16, 4>("p4c8l8s2k16g4"),
         d_variant<8, 8, 8, 1, 2, 16, 16, 4>("p8c8l8s2k16t4"),
         d_variant<4, 8, 8, 1, 2, 16, 16, 4>("p4c8l8s2k16t4"),
+        // serialized rings of three of the above (check variants)
+        d_variant<8, 8, 8, 1, 2, 16, 16, 1, 4, true>("p8c8l8s2k16-serial"),
+        d_variant<6, 8, 8, 1, 2, 16, 4, 1, 4, true>("p6c8l8s2k16g4-serial"),
+        d_variant<4, 8, 8, 1, 2, 16, 16, 4, 4, true>("p4c8l8s2k16t4-serial"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
@@ -453,15 +470,38 @@ const DVariant *d_variants(int *n)
 
 }  // namespace
 
-int dma32_plan(const Shape &sh)
+int dma32_find(const char *name)
 {
-    // filter offsets, up to one 64-tap stage past K_pad32, need 31 bits
-    if ((sh.K_pad32 + 64) * sh.Co_pad32 * 4 > (int64_t)kMaxRecords)
-        return -1;
-    // 16-byte window loads need every window on a 16-byte boundary
-    const bool aligned = sh.Ci % 4 == 0;
     int n;
     const DVariant *v = d_variants(&n);
+    for (int t = 0; t < n; ++t)
+        if (strcmp(name, v[t].name) == 0)
+            return t;
+    return -1;
+}
+
+const char *dma32_name(int v)
+{
+    int n;
+    return d_variants(&n)[v].name;
+}
+
+bool dma32_fits(const Shape &sh, int pick)
+{
+    int n;
+    const DVariant *v = d_variants(&n);
+    if (pick < 0 || pick >= n)
+        return false;
+    // filter offsets, up to one 64-tap stage past K_pad32, need 31 bits
+    if ((sh.K_pad32 + 64) * sh.Co_pad32 * 4 > (int64_t)kMaxRecords)
+        return false;
+    // 16-byte window loads need every window on a 16-byte boundary
+    return v[pick].gr == 4 || sh.Ci % 4 == 0;
+}
+
+int dma32_default(const Shape &sh)
+{
+    const bool aligned = sh.Ci % 4 == 0;
     const int64_t tiles256 = ((sh.P + 255) / 256) * ((sh.Co + 63) / 64);
     // unaligned windows (C_i % 4 != 0, the 3-channel stems): the 6-pixel
     // lane tile, 7x7 C_i=3 stride 2 67.2 vs 64.1 TFLOP/s (8-pixel) and 3x3
@@ -478,24 +518,11 @@ int dma32_plan(const Shape &sh)
     const int64_t pad64 = (sh.Co + 63) / 64 * 64 - sh.Co, pad96 = (sh.Co + 95) / 96 * 96 - sh.Co;
     if (pad96 < pad64 && ((sh.P + 127) / 128) * ((sh.Co + 95) / 96) >= 1024)
         name = aligned ? "p4c12l8s2k16" : "p4c12l8s2k16g4";
-    if (const char *e = getenv("IM2WIN_FP32_KERNEL")) {
-        if (strcmp(e, "regs") == 0)
-            return -1;
-        name = e;
-    }
-    int pick = -1;
-    for (int t = 0; t < n; ++t) {
-        if (v[t].gr == 16 && !aligned)
-            continue;
-        if (pick < 0 && v[t].gr == (aligned ? 16 : 4))
-            pick = t;  // the first that fits, if the name matches none
-        if (strcmp(name, v[t].name) == 0)
-            return t;
-    }
-    return pick;
+    const int pick = dma32_find(name);
+    return dma32_fits(sh, pick) ? pick : -1;
 }
 
-hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const void *ws, const void *packed,
+hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const Tuning &t, const void *ws, const void *packed,
                                 float *out, hipStream_t st)
 {
     int n;
@@ -512,7 +539,7 @@ hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const void *ws, const
     const int64_t gx = (sh.P + v.bm - 1) / v.bm, gy = (sh.Co + v.cw - 1) / v.cw;
     if (gx * gy > 0x7fffffff)
         return hipErrorInvalidValue;
-    a.tg = make_tilegrid(gx, gy);
+    a.tg = make_tilegrid(gx, gy, t.tile_linear);
     void *args[] = {&a};
     return hipLaunchKernel(v.f, dim3((uint32_t)(gx * gy)), dim3(v.nt), args, 0, st);
 }

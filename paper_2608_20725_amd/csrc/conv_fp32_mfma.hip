@@ -101,14 +101,6 @@ __device__ inline void wait_vmcnt()
     __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// Workgroup barrier that leaves the stages in flight alone.
-__device__ inline void ring_barrier()
-{
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
 // 16-byte chunk c of row r sits in slot c ^ rsw(r): the 16 lanes that read
 // one chunk of 16 consecutive rows touch 16 different slots of the 64 banks.
 __device__ inline uint32_t rsw(uint32_t r) { return (r ^ (r >> 3)) & 7u; }
@@ -346,8 +338,39 @@ bool fp32_mfma_ok(const Shape &sh)
 
 int64_t fp32_mfma_packed_bytes(const Shape &sh) { return co_pad_mfma(sh.Co) * k_pad_mfma(sh.K) * 4; }
 
-hipError_t launch_conv_fp32_mfma(const Shape &sh, const float *filt, void *packed, float *out, const void *ws,
-                                 hipStream_t st)
+int mfma32_find(const char *name)
+{
+    int n;
+    const MVariant *v = m_variants(&n);
+    for (int t = 0; t < n; ++t)
+        if (strcmp(name, v[t].name) == 0)
+            return t;
+    return -1;
+}
+
+const char *mfma32_name(int v)
+{
+    int n;
+    return m_variants(&n)[v].name;
+}
+
+int mfma32_default(const Shape &sh)
+{
+    int n;
+    const MVariant *v = m_variants(&n);
+    // The largest tile whose grid gives every CU two workgroups (512), else
+    // the one with the most workgroups: on few-pixel layers the matrix cores
+    // otherwise sit idle (3x3 C=512 at 7x7: 100 tiles of 128 x 128).
+    auto tiles = [&](const MVariant &t) { return ((sh.P + t.bn - 1) / t.bn) * ((sh.Co + t.bm - 1) / t.bm); };
+    if (sh.Co <= 32)
+        return 2;
+    if (sh.Co <= 64)
+        return tiles(v[1]) >= 512 ? 1 : 3;
+    return tiles(v[0]) >= 512 ? 0 : tiles(v[3]) >= 512 ? 3 : 4;
+}
+
+hipError_t launch_conv_fp32_mfma(const Shape &sh, const Plan32 &plan, const Tuning &t, const float *filt,
+                                 void *packed, float *out, const void *ws, hipStream_t st)
 {
     P32Args p;
     p.filt = filt;
@@ -368,22 +391,7 @@ hipError_t launch_conv_fp32_mfma(const Shape &sh, const float *filt, void *packe
 
     int n;
     const MVariant *v = m_variants(&n);
-    // The largest tile whose grid gives every CU two workgroups (512), else
-    // the one with the most workgroups: on few-pixel layers the matrix cores
-    // otherwise sit idle (3x3 C=512 at 7x7: 100 tiles of 128 x 128).
-    auto tiles = [&](const MVariant &t) { return ((sh.P + t.bn - 1) / t.bn) * ((sh.Co + t.bm - 1) / t.bm); };
-    int pick;
-    if (sh.Co <= 32)
-        pick = 2;
-    else if (sh.Co <= 64)
-        pick = tiles(v[1]) >= 512 ? 1 : 3;
-    else
-        pick = tiles(v[0]) >= 512 ? 0 : tiles(v[3]) >= 512 ? 3 : 4;
-    if (const char *env = getenv("IM2WIN_FP32_MFMA_TILE")) {
-        for (int t = 0; t < n; ++t)
-            if (strcmp(env, v[t].name) == 0)
-                pick = t;
-    }
+    const int pick = plan.v;
     M32Args a;
     a.ws = static_cast<const float *>(ws);
     a.packed = p.packed;
@@ -398,7 +406,7 @@ hipError_t launch_conv_fp32_mfma(const Shape &sh, const float *filt, void *packe
     const int64_t gx = (sh.P + v[pick].bn - 1) / v[pick].bn, gy = (sh.Co + v[pick].bm - 1) / v[pick].bm;
     if (gx * gy > 0x7fffffff)
         return hipErrorInvalidValue;
-    a.tg = make_tilegrid(gx, gy);
+    a.tg = make_tilegrid(gx, gy, t.tile_linear);
     void *args[] = {&a};
     return hipLaunchKernel(v[pick].f, dim3((uint32_t)(gx * gy)), dim3(v[pick].nt), args, 0, st);
 }

@@ -1,0 +1,183 @@
+// Kernel choice: the tuning variables and the plan each conv call runs.
+//
+// A conv call makes its plan once, on the host, from the layer's shape and
+// the (checked) tuning variables, and hands the same plan to the filter pack
+// and to the conv launch, so the packed-filter layout always matches the
+// kernel that reads it.  conv_im2win_kernel_name reports the plan.
+#include "../../include/im2win.h"
+#include "common.hpp"
+
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+namespace im2win {
+
+namespace {
+
+// Variable unset or empty: not forced (-1).  Otherwise the index `find`
+// gives, or IM2WIN_EINVAL for a name no kernel has.
+int read_name(const char *var, int (*find)(const char *), int *out)
+{
+    *out = -1;
+    const char *e = getenv(var);
+    if (!e || !*e)
+        return IM2WIN_OK;
+    *out = find(e);
+    return *out >= 0 ? IM2WIN_OK : IM2WIN_EINVAL;
+}
+
+// linear | xcd (the default); anything else is an error.
+int read_order(const char *var, bool *linear)
+{
+    *linear = false;
+    const char *e = getenv(var);
+    if (!e || !*e || strcmp(e, "xcd") == 0)
+        return IM2WIN_OK;
+    if (strcmp(e, "linear") == 0) {
+        *linear = true;
+        return IM2WIN_OK;
+    }
+    return IM2WIN_EINVAL;
+}
+
+}  // namespace
+
+int read_tuning(Tuning *t)
+{
+    int rc;
+    t->fp16_kernel = Tuning::kAuto;
+    if (const char *e = getenv("IM2WIN_FP16_KERNEL")) {
+        if (strcmp(e, "pipe") == 0)
+            t->fp16_kernel = Tuning::kPipe;
+        else if (strcmp(e, "regs") == 0)
+            t->fp16_kernel = Tuning::kRegs;
+        else if (*e)
+            return IM2WIN_EINVAL;
+    }
+    if ((rc = read_name("IM2WIN_FP16_COL", col_find, &t->fp16_col)) != IM2WIN_OK ||
+        (rc = read_name("IM2WIN_FP16_TILE", pipe_find, &t->fp16_tile)) != IM2WIN_OK ||
+        (rc = read_name("IM2WIN_FP16_SEG", seg_find, &t->fp16_seg)) != IM2WIN_OK ||
+        (rc = read_name("IM2WIN_FP32_TILE", regs32_find, &t->fp32_tile)) != IM2WIN_OK ||
+        (rc = read_name("IM2WIN_FP32_MFMA_TILE", mfma32_find, &t->fp32_mfma_tile)) != IM2WIN_OK)
+        return rc;
+    const char *e = getenv("IM2WIN_FP32_KERNEL");
+    if (e && strcmp(e, "regs") == 0)
+        t->fp32_kernel = -2;
+    else if ((rc = read_name("IM2WIN_FP32_KERNEL", dma32_find, &t->fp32_kernel)) != IM2WIN_OK)
+        return rc;
+    if ((rc = read_order("IM2WIN_TRANSFORM_ORDER", &t->transform_linear)) != IM2WIN_OK ||
+        (rc = read_order("IM2WIN_TILE_ORDER", &t->tile_linear)) != IM2WIN_OK)
+        return rc;
+    // contradictory choices
+    const int fam16 = (t->fp16_col >= 0) + (t->fp16_seg >= 0) + (t->fp16_tile >= 0 || t->fp16_kernel == Tuning::kPipe) +
+                      (t->fp16_kernel == Tuning::kRegs);
+    if (fam16 > 1)
+        return IM2WIN_EINVAL;
+    if (t->fp32_tile >= 0 && t->fp32_kernel >= 0)
+        return IM2WIN_EINVAL;
+    return IM2WIN_OK;
+}
+
+int plan_fp16(const Shape &sh, const Tuning &t, Plan16 *p)
+{
+    const bool aligned = sh.Ci % 8 == 0;  // every window starts on a 16-byte boundary
+    // register-staged tile by output channels
+    const int regs_tile = sh.Co <= 32 ? 0 : sh.Co <= 64 ? 1 : 2;
+    if (t.fp16_kernel == Tuning::kRegs) {
+        *p = Plan16{Fam16::Regs, regs_tile};
+        return IM2WIN_OK;
+    }
+    if (t.fp16_col >= 0) {
+        if (!col_fits(sh, t.fp16_col))
+            return IM2WIN_EINVAL;
+        *p = Plan16{Fam16::Col, t.fp16_col};
+        return IM2WIN_OK;
+    }
+    if (t.fp16_seg >= 0) {
+        if (aligned || !seg_fits(sh, t.fp16_seg))
+            return IM2WIN_EINVAL;
+        *p = Plan16{Fam16::Seg, t.fp16_seg};
+        return IM2WIN_OK;
+    }
+    if (t.fp16_tile >= 0 || t.fp16_kernel == Tuning::kPipe) {
+        if (!aligned)
+            return IM2WIN_EINVAL;
+        *p = Plan16{Fam16::Pipe, t.fp16_tile >= 0 ? t.fp16_tile : pipe_default(sh)};
+        return IM2WIN_OK;
+    }
+    if (aligned) {
+        const int c = col_default(sh);
+        *p = c >= 0 ? Plan16{Fam16::Col, c} : Plan16{Fam16::Pipe, pipe_default(sh)};
+        return IM2WIN_OK;
+    }
+    const int sg = seg_default(sh);
+    *p = sg >= 0 ? Plan16{Fam16::Seg, sg} : Plan16{Fam16::Regs, regs_tile};
+    return IM2WIN_OK;
+}
+
+int plan_fp32(const Shape &sh, const Tuning &t, bool mfma, Plan32 *p)
+{
+    if (mfma) {
+        if (fp32_mfma_ok(sh)) {
+            *p = Plan32{Fam32::Mfma, t.fp32_mfma_tile >= 0 ? t.fp32_mfma_tile : mfma32_default(sh)};
+            return IM2WIN_OK;
+        }
+        // layers the matrix-core kernel cannot take run the vector-ALU
+        // kernels (documented); a forced matrix-core tile is an error
+        if (t.fp32_mfma_tile >= 0)
+            return IM2WIN_EINVAL;
+    }
+    if (t.fp32_kernel >= 0) {
+        if (!dma32_fits(sh, t.fp32_kernel))
+            return IM2WIN_EINVAL;
+        *p = Plan32{Fam32::Dma, t.fp32_kernel};
+        return IM2WIN_OK;
+    }
+    if (t.fp32_kernel == -2 || t.fp32_tile >= 0) {
+        const int v = t.fp32_tile >= 0 ? t.fp32_tile : 0;
+        if (!regs32_fits(sh, v)) {
+            if (t.fp32_tile >= 0)
+                return IM2WIN_EINVAL;
+            *p = Plan32{Fam32::Regs, regs32_find("m4n16p2")};  // filter read from global memory
+            return IM2WIN_OK;
+        }
+        *p = Plan32{Fam32::Regs, v};
+        return IM2WIN_OK;
+    }
+    const int d = dma32_default(sh);
+    if (d >= 0) {
+        *p = Plan32{Fam32::Dma, d};
+        return IM2WIN_OK;
+    }
+    *p = Plan32{Fam32::Regs, regs32_fits(sh, 0) ? 0 : regs32_find("m4n16p2")};
+    return IM2WIN_OK;
+}
+
+void plan16_name(const Shape &sh, const Plan16 &p, char *buf, int len)
+{
+    switch (p.fam) {
+    case Fam16::Col: snprintf(buf, len, "conv_fp16_col %s", col_name(p.v)); break;
+    case Fam16::Pipe: snprintf(buf, len, "conv_fp16_pipe %s", pipe_name(p.v)); break;
+    case Fam16::Seg: snprintf(buf, len, "conv_fp16_seg %s", seg_name(p.v)); break;
+    case Fam16::Regs: {
+        static const char *tiles[] = {"c32p256", "c64p256", "c128p128"};
+        // unaligned 16-byte loads for windows of 128 taps or more, element
+        // loads for shorter ones
+        snprintf(buf, len, "conv_fp16_kernel %s%s", tiles[p.v], sh.K >= 128 ? "u" : "e");
+        break;
+    }
+    }
+}
+
+void plan32_name(const Shape &sh, const Plan32 &p, char *buf, int len)
+{
+    (void)sh;
+    switch (p.fam) {
+    case Fam32::Dma: snprintf(buf, len, "conv_fp32_dma %s", dma32_name(p.v)); break;
+    case Fam32::Regs: snprintf(buf, len, "conv_fp32_kernel %s", regs32_name(p.v)); break;
+    case Fam32::Mfma: snprintf(buf, len, "conv_fp32_mfma %s", mfma32_name(p.v)); break;
+    }
+}
+
+}  // namespace im2win

@@ -187,7 +187,8 @@ bool transform_range_ok(const Shape &sh)
     return (uint64_t)sh.win_elems + 16 < (1ull << 32);
 }
 
-hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st, const Pad *pad)
+hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream_t st, const Tuning &t,
+                            const Pad *pad)
 {
     TArgs a;
     a.in = static_cast<const char *>(in);
@@ -218,8 +219,7 @@ hipError_t launch_transform(const Shape &sh, const void *in, void *ws, hipStream
     a.div_Wq = make_fastdiv((uint32_t)sh.Wq);
     // IM2WIN_TRANSFORM_ORDER=linear deals blocks in launch order (to measure
     // what the XCD-aware order gains)
-    const char *order = getenv("IM2WIN_TRANSFORM_ORDER");
-    a.xcd_order = (order && strcmp(order, "linear") == 0) ? 0u : 1u;
+    a.xcd_order = t.transform_linear ? 0u : 1u;
     void *args[] = {&a};
     const bool vec = (sh.Ci * sh.elt) % 16 == 0;
     if (vec) {

@@ -93,23 +93,26 @@ def check_full(run, x, w):
 
 
 def sample_points(N, Ho, Wo, Co, seed, full_images=(0, -1), n_random=4096, max_mac=None, K=None):
-    """All outputs of the listed images (if their MAC count allows) plus
-    `n_random` seeded random outputs."""
+    """All outputs of the listed images (as many as `max_mac` multiply-adds
+    allow, at least the first) plus `n_random` seeded random outputs."""
     rng = np.random.default_rng(seed)
     pts = []
     imgs = sorted({i % N for i in full_images})
-    if max_mac is None or K is None or len(imgs) * Ho * Wo * Co * K <= max_mac:
-        for i in imgs:
-            g = np.stack(np.meshgrid([i], np.arange(Ho), np.arange(Wo), np.arange(Co),
-                                     indexing="ij"), -1).reshape(-1, 4)
-            pts.append(g)
+    if max_mac is not None and K is not None:
+        # as many of the listed images as the MAC budget allows, at least one
+        per = Ho * Wo * Co * K
+        imgs = imgs[:max(1, int(max_mac // per))]
+    for i in imgs:
+        g = np.stack(np.meshgrid([i], np.arange(Ho), np.arange(Wo), np.arange(Co),
+                                 indexing="ij"), -1).reshape(-1, 4)
+        pts.append(g)
     r = np.stack([rng.integers(0, N, n_random), rng.integers(0, Ho, n_random),
                   rng.integers(0, Wo, n_random), rng.integers(0, Co, n_random)], -1)
     pts.append(r)
     return np.concatenate(pts).astype(np.int64)
 
 
-def check_sampled(run, x, w, seed=0, max_mac=4e9):
+def check_sampled(run, x, w, seed=0, max_mac=6e9):
     """Outputs of images 0 and N-1 plus random outputs, each against the
     oracle computed one by one (only the images they touch go to the oracle)."""
     K = run.Kh * run.Kw * run.Ci
@@ -127,3 +130,20 @@ def check_sampled(run, x, w, seed=0, max_mac=4e9):
     r = rel_err(got, ref, absref)
     assert r <= TOL[run.dtype], "max |err|/sum|x||w| = %.3g on %d sampled outputs" % (r, len(pts))
     return r, len(pts)
+
+
+FAMILY = {"pipe": "conv_fp16_pipe", "regs": None}
+
+
+def assert_kernel(shape, dtype, var, value, dilation=1):
+    """The library reports that the forced kernel is the one the call runs."""
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    got = pkg.conv_im2win_kernel_name(N, Ci, H, W, Co, Kh, Kw, s, dtype, dilation=dilation)
+    if value == "regs":
+        want = "conv_fp32_kernel" if var.startswith("IM2WIN_FP32") else "conv_fp16_kernel"
+        assert got.split()[0] == want, got
+    elif value == "pipe":
+        assert got.split()[0] == "conv_fp16_pipe", got
+    else:
+        assert got.split()[1] == value, got
+    return got

@@ -25,7 +25,7 @@ def test_more_than_one_gpu_is_refused():
 
 @pytest.mark.gpu
 def test_bench_json_line_fields():
-    p = _run(["--layer", "cfg1_tiny_c3_32_3x3", "--steps", "3", "--warmup", "2"], timeout=300)
+    p = _run(["--layer", "cfg1_tiny_c3_32_3x3", "--steps", "3", "--warmup", "2", "--no-extras"], timeout=300)
     assert p.returncode == 0, p.stderr[-2000:]
     lines = [l for l in p.stdout.splitlines() if l.strip()]
     assert len(lines) == 1, "exactly one JSON line"
@@ -42,6 +42,19 @@ def test_bench_json_line_fields():
     assert rl["peak"] == 157.3 and rl["achieved"] > 0
     assert abs(rl["frac"] - rl["achieved"] / rl["peak"]) < 1e-3
     assert rl["traffic"] is None   # counters are recorded for the benchmark workload only
+    r16 = r["roofline_f16"]
+    assert r16["bound"] == "mfma" and r16["peak"] == 2516.6 and r16["achieved"] > 0
+    assert abs(r16["frac"] - r16["achieved"] / r16["peak"]) < 1e-3
+    assert 0 < r16["frac_attainable"] and r16["attainable"] <= 2516.6
+    # value: conv-only FLOPs of both precisions over their summed conv time
+    co = r["conv_only"]
+    t = co["f32"]["conv_ms_per_step"] + co["f16"]["conv_ms_per_step"]
+    assert abs(r["value"] - (co["f32"]["GFLOP_per_step"] + co["f16"]["GFLOP_per_step"]) / t) < 2e-2 * r["value"]
+    (lay,) = r["layers"]
+    assert lay["f32"]["kernel"].startswith("conv_fp32_") and lay["f16"]["kernel"].startswith("conv_fp16_")
+    ws = r["workspace"]["cfg1_tiny_c3_32_3x3"]
+    for dt in ("f32", "f16"):
+        assert ws[dt]["peak_bytes_im2win"] > 0 and ws[dt]["peak_bytes_im2col"] > 0
     cb = r["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0 and cb["sample"]
     assert cb["single_thread"]["value"] > 0

@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import Run, TOL, check_full, check_sampled, oracle_inputs, rel_err, say
+from gpu_util import Run, TOL, assert_kernel, check_full, check_sampled, oracle_inputs, rel_err, say
 from test_gpu_conv import EDGE, SEG_SHAPES, _id
 from paper_2608_20725_amd import workloads
 
@@ -115,6 +115,7 @@ def test_bf16_kernel_variants(case, monkeypatch):
         monkeypatch.setenv(var, name)
         if var == "IM2WIN_FP16_TILE":
             monkeypatch.setenv("IM2WIN_FP16_KERNEL", "pipe")
+        assert_kernel(shape, BF, var, name)
         run = Run(x, w, s, BF)
         check_full(run, x, w)
         out = run.out_np()

@@ -1,13 +1,17 @@
 """Mini-batch im2win (conv_im2win_chunked): chunks of n_chunk images through a
 one- or two-slot workspace, with and without a second stream.  The output must
-equal the full-batch call bit for bit and match the oracle; the bytes after the
-workspace must stay untouched."""
+match the oracle, and equal the full-batch call bit for bit wherever both run
+the same kernel; the bytes after the workspace must stay untouched.  At full
+size: the benchmark's configuration (56x56 C=64, 128 images, 32-image chunks,
+two streams) and chunkings whose smaller last chunk would select another
+kernel (and packed-filter layout) on its own."""
 import numpy as np
 import pytest
 import torch
 
 import paper_2608_20725_amd as pkg
-from gpu_util import Run, check_full, say
+from gpu_util import Run, TOL, check_full, oracle_inputs, rel_err, sample_points, say
+import oracle
 from paper_2608_20725_amd import workloads
 
 pytestmark = pytest.mark.gpu
@@ -47,12 +51,76 @@ def test_chunked_equals_full_batch(shape, dtype):
     check_full(full, x, w)
     ref = full.out.cpu()
     aux = torch.cuda.Stream()
+    full_kernel = pkg.conv_im2win_kernel_name(N, Ci, H, W, Co, Kh, Kw, s, dtype)
     for n_chunk, two in CHUNKS:
         say("chunked", shape, dtype, n_chunk, two)
         out = _run_chunked(x, w, s, dtype, n_chunk, two, aux if two else None)
-        got = out.cpu()
-        bits = torch.int32 if dtype == torch.float32 else torch.int16
-        assert torch.equal(got.view(bits), ref.view(bits)), (n_chunk, two)
+        check_out(out, x, w, s, dtype)
+        chunk_kernel = pkg.conv_im2win_kernel_name(min(n_chunk, N), Ci, H, W, Co, Kh, Kw, s, dtype)
+        if chunk_kernel == full_kernel:
+            got = out.cpu()
+            bits = torch.int32 if dtype == torch.float32 else torch.int16
+            assert torch.equal(got.view(bits), ref.view(bits)), (n_chunk, two)
+
+
+def check_out(out, x, w, s, dtype):
+    """Every output of a small layer against the oracle."""
+    xo, wo = oracle_inputs(x, w, dtype)
+    ref, absref = oracle.conv(xo, wo, s, with_abs=True)
+    y = out.float().cpu().numpy().astype(np.float64)
+    assert not np.isnan(y).any(), "output element left unwritten"
+    r = rel_err(y, ref, absref)
+    assert r <= TOL[dtype], r
+
+
+def check_out_sampled(out, x, w, s, dtype, images, seed):
+    """All outputs of `images` plus 4096 random ones against the oracle,
+    computed point by point on the images they touch."""
+    N, Ho, Wo, Co = out.shape
+    Kh, Kw, Ci, _ = w.shape
+    pts = sample_points(N, Ho, Wo, Co, seed, full_images=images)
+    imgs = np.unique(pts[:, 0])
+    remap = {int(i): k for k, i in enumerate(imgs)}
+    xo, wo = oracle_inputs(x[torch.from_numpy(imgs)], w, dtype)
+    local = pts.copy()
+    local[:, 0] = [remap[int(i)] for i in pts[:, 0]]
+    ref, absref = oracle.conv_points(xo, wo, s, local)
+    y = out.float().cpu().numpy()
+    assert not np.isnan(y).any(), "output element left unwritten"
+    got = y[pts[:, 0], pts[:, 1], pts[:, 2], pts[:, 3]].astype(np.float64)
+    r = rel_err(got, ref, absref)
+    assert r <= TOL[dtype], "max |err|/sum|x||w| = %.3g on %d sampled outputs" % (r, len(pts))
+    return r, len(pts)
+
+
+# (layer shape, n_chunk, dtype): the benchmark's mini-batch configuration in
+# both precisions, and chunkings whose last chunk on its own would pick
+# another kernel: 3x3 C=128 at 56x56 (48-image chunks run the one-slot row
+# kernel, a 32-image batch the column-staged one with another filter
+# layout), and 56x56 C=64 fp32 in 100-image chunks (the 256-pixel tile;
+# 28 images alone take the tap-split tile).
+FULL_SIZE = [
+    ((128, 64, 56, 56, 64, 3, 3, 1), 32, torch.float32),
+    ((128, 64, 56, 56, 64, 3, 3, 1), 32, torch.float16),
+    ((128, 128, 56, 56, 128, 3, 3, 1), 48, torch.float16),
+    ((128, 128, 56, 56, 128, 3, 3, 1), 48, torch.bfloat16),
+    ((128, 64, 56, 56, 64, 3, 3, 1), 100, torch.float32),
+]
+
+
+@pytest.mark.parametrize("case", FULL_SIZE, ids=lambda c: "x".join(map(str, c[0])) + "-c%d-%s" % (c[1], str(c[2])[6:]))
+def test_chunked_full_size_against_oracle(case):
+    shape, n_chunk, dtype = case
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    last = N - (N - 1) // n_chunk * n_chunk
+    say("chunked full size", shape, n_chunk, dtype, "chunk kernel",
+        pkg.conv_im2win_kernel_name(n_chunk, Ci, H, W, Co, Kh, Kw, s, dtype),
+        "last chunk alone", pkg.conv_im2win_kernel_name(last, Ci, H, W, Co, Kh, Kw, s, dtype))
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=29)
+    out = _run_chunked(x, w, s, dtype, n_chunk, True, torch.cuda.Stream())
+    # images in the first chunk, across the first chunk boundary, and in the last chunk
+    r, n = check_out_sampled(out, x, w, s, dtype, (0, n_chunk - 1, n_chunk, N - last, N - 1), seed=n_chunk)
+    say("  max rel err %.3g over %d outputs" % (r, n))
 
 
 def test_chunked_back_to_back_reuses_workspace():

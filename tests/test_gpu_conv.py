@@ -12,7 +12,7 @@ import torch
 
 import oracle
 import paper_2608_20725_amd as pkg
-from gpu_util import Run, TOL, check_full, check_sampled, oracle_inputs, rel_err, say
+from gpu_util import Run, TOL, assert_kernel, check_full, check_sampled, oracle_inputs, rel_err, say
 from oracle_checks import TINY
 from paper_2608_20725_amd import workloads
 
@@ -105,12 +105,18 @@ def test_conv_layers_full_batch_sampled(layer, dtype):
     """Every configured layer at its full batch, in the launch configuration
     the benchmark times: all outputs of images 0 and N-1 (when affordable) and
     4096 random outputs, each against the oracle."""
-    say("conv full", layer.name, dtype)
+    say("conv full", layer.name, dtype, pkg.conv_im2win_kernel_name(
+        layer.N, layer.C_i, layer.H, layer.W, layer.C_o, layer.K_h, layer.K_w, layer.stride, dtype))
     x, w = workloads.draw_layer(layer)
     run = Run(x, w, layer.stride, dtype)
     r, n = check_sampled(run, x, w, seed=layer.seed)
     say("  max rel err %.3g over %d outputs" % (r, n))
     run.check_out_guards()
+    # run-to-run determinism at full size: the same bits again
+    first = run.out.clone()
+    run.rerun_conv()
+    bits = torch.int16 if dtype == torch.float16 else torch.int32
+    assert torch.equal(first.view(bits), run.out.view(bits))
 
 
 @pytest.mark.parametrize("dtype", DTYPES, ids=DT_IDS)
@@ -234,6 +240,7 @@ def test_kernel_variants_agree(case, monkeypatch):
         monkeypatch.setenv(var, name)
         if var == "IM2WIN_FP16_TILE":
             monkeypatch.setenv("IM2WIN_FP16_KERNEL", "pipe")
+        assert_kernel(shape, dtype, var, name)
         run = Run(x, w, s, dtype)
         check_full(run, x, w)
         out = run.out_np()
@@ -242,6 +249,43 @@ def test_kernel_variants_agree(case, monkeypatch):
         elif same_order:
             assert np.array_equal(out.view(np.uint8), first.view(np.uint8)), name
 
+
+
+# Differential check of the load rings: each ring kernel against the same
+# tile with its ring serialized (a stage's loads issued only after every wave
+# has finished with the previous one, and waited for in full, so nothing is
+# in flight while LDS is read).  Both compute the same sums in the same
+# order, so a missing wait or barrier in the ring would show as a bit
+# difference.  Shapes with many stages and many tiles per CU.
+SERIAL_CASES = [
+    # (variable, ring variant, shape, dtype)
+    ("IM2WIN_FP16_COL", "k3c64p128t32s2", (8, 64, 56, 56, 64, 3, 3, 1), torch.float16),
+    ("IM2WIN_FP16_COL", "k7c64p256t16s3", (2, 64, 60, 120, 64, 7, 7, 2), torch.float16),
+    ("IM2WIN_FP16_COL", "k3c256p192t32s2w8", (16, 512, 14, 14, 512, 3, 3, 1), torch.bfloat16),
+    ("IM2WIN_FP16_SEG", "s64p256", (8, 3, 100, 100, 64, 3, 3, 1), torch.float16),
+    ("IM2WIN_FP32_KERNEL", "p8c8l8s2k16", (8, 64, 56, 56, 64, 3, 3, 1), torch.float32),
+    ("IM2WIN_FP32_KERNEL", "p6c8l8s2k16g4", (8, 3, 100, 100, 64, 7, 7, 2), torch.float32),
+    ("IM2WIN_FP32_KERNEL", "p4c8l8s2k16t4", (16, 256, 14, 14, 256, 3, 3, 1), torch.float32),
+]
+
+
+@pytest.mark.parametrize("case", SERIAL_CASES, ids=lambda c: c[1] + "-" + _id(c[2]))
+def test_ring_matches_serialized_ring(case, monkeypatch):
+    var, name, shape, dtype = case
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=53)
+    outs = []
+    for v in (name, name + "-serial"):
+        monkeypatch.setenv(var, v)
+        say("ring", v, shape, dtype)
+        assert_kernel(shape, dtype, var, v)
+        run = Run(x, w, s, dtype)
+        if not outs:
+            check_sampled(run, x, w, seed=3)
+        run.check_out_guards()
+        outs.append(run.out.clone())
+    bits = torch.int32 if dtype == torch.float32 else torch.int16
+    assert torch.equal(outs[0].view(bits), outs[1].view(bits))
 
 
 # The XCD-aware tile order (several channel tiles) against launch order

@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import paper_2608_20725_amd as pkg
-from gpu_util import GUARD, SENTINEL, TOL, WS_GUARD, oracle_inputs, rel_err, say
+from gpu_util import GUARD, SENTINEL, TOL, WS_GUARD, oracle_inputs, rel_err, say, assert_kernel
 from paper_2608_20725_amd import workloads
 
 pytestmark = pytest.mark.gpu
@@ -172,6 +172,7 @@ def test_dilated_kernel_variants(case, monkeypatch):
         monkeypatch.setenv(var, name)
         if var == "IM2WIN_FP16_TILE":
             monkeypatch.setenv("IM2WIN_FP16_KERNEL", "pipe")
+        assert_kernel((N, Ci, H + 2 * ph, W + 2 * pw, Co, Kh, Kw, s), dtype, var, name, dilation=d)
         run = DilRun(x, w, s, ph, pw, d, dtype)
         _check_conv(run, x, w)
         run.check_guards()
