@@ -330,6 +330,29 @@ int conv_im2win_chunked(const void *in_nhwc, const void *filt_khkwcico, void *ou
                         void *hip_stream, void *hip_stream_aux);
 
 /*
+ * Allocation-free mini-batch call, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid it): conv_im2win_chunked on one stream and one workspace slot, with
+ * the workspace in a static device buffer of IM2WIN_STATIC_SCRATCH_BYTES that
+ * the library holds on every GPU it runs on until the process ends.
+ *   in_nhwc, filt_khkwcico, out_nhwc, N .. n_chunk, dt, hip_stream
+ *           as for conv_im2win_chunked (the caller still allocates the input,
+ *           filter and output)
+ * Returns IM2WIN_EWORKSPACE, before anything is enqueued, when
+ * conv_chunked_workspace_bytes(..., n_chunk, 0, dt) exceeds
+ * IM2WIN_STATIC_SCRATCH_BYTES (choose a smaller n_chunk).  The call makes no
+ * device allocation and creates no events; its first call on a device looks
+ * up that device's buffer once.  All calls on one GPU share its buffer and
+ * the buffer keeps the last call's contents: calls that overlap on one GPU
+ * (on different streams, or from several host threads without ordering)
+ * race.  Output, numerics and other errors as for conv_im2win_chunked.
+ */
+#define IM2WIN_STATIC_SCRATCH_BYTES ((int64_t)128 << 20)
+int conv_im2win_chunked_noalloc(const void *in_nhwc, const void *filt_khkwcico, void *out_nhwc, int64_t N,
+                                int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+                                int64_t stride, int64_t n_chunk, im2win_dtype_t dt, void *hip_stream);
+
+/*
  * Names the kernel the conv call of this layer runs, e.g.
  * "conv_fp16_col k3c64p128t32s2" (kernel family, then variant): the choice
  * the call makes from the shape and the tuning variables above.

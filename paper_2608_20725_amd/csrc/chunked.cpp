@@ -16,6 +16,7 @@
 
 #include "../../include/im2win.h"
 
+#include <mutex>
 #include <string.h>
 
 namespace im2win {
@@ -111,42 +112,57 @@ int enqueue_chunks(const void *in, const void *filt, void *out, char *wsb, const
     return IM2WIN_OK;
 }
 
-int run_chunked(const void *in, const void *filt, void *out, void *ws, int64_t ws_bytes, int64_t N,
-                int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
-                int64_t stride, int64_t n_chunk, int dt, hipStream_t st, hipStream_t aux)
+// Checks the arguments of a mini-batch call (the workspace only when `ws` is
+// given) and makes its plans.
+int check_chunked(const void *in, const void *filt, void *out, void *ws, int64_t ws_bytes, int64_t N, int64_t C_i,
+                  int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride,
+                  int64_t n_chunk, int dt, hipStream_t st, hipStream_t aux, Plan *p, Tuning *tu, Plan16 *p16,
+                  Plan32 *p32)
 {
-    if (!in || !filt || !out || !ws)
+    if (!in || !filt || !out)
         return IM2WIN_EINVAL;
-    Plan p;
-    int rc = make_plan(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, n_chunk, aux != nullptr, dt, &p);
+    int rc = make_plan(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, n_chunk, aux != nullptr, dt, p);
     if (rc != IM2WIN_OK)
         return rc;
     if (aux != nullptr && aux == st)
         return IM2WIN_EINVAL;
-    if (!aligned16(in) || !aligned16(filt) || !aligned16(out) || !aligned16(ws))
+    if (!aligned16(in) || !aligned16(filt) || !aligned16(out) || (ws && !aligned16(ws)))
         return IM2WIN_EALIGN;
     Shape full;
     make_shape(N, C_i, H_i, W_i, C_o, K_h, K_w, stride, dt, &full);
     const int64_t elt = full.elt;
     const int64_t in_bytes = N * H_i * W_i * C_i * elt, f_bytes = full.K * C_o * elt,
                   o_bytes = full.P * C_o * elt;
-    if (ws_bytes < 0)
+    if (ws && ws_bytes < 0)
         return IM2WIN_EWORKSPACE;
     if ((rc = check_extent(in, in_bytes)) != IM2WIN_OK || (rc = check_extent(filt, f_bytes)) != IM2WIN_OK ||
-        (rc = check_extent(out, o_bytes)) != IM2WIN_OK || (rc = check_extent(ws, ws_bytes)) != IM2WIN_OK)
+        (rc = check_extent(out, o_bytes)) != IM2WIN_OK || (ws && (rc = check_extent(ws, ws_bytes)) != IM2WIN_OK))
         return rc;
-    if (overlaps(in, in_bytes, ws, ws_bytes) || overlaps(in, in_bytes, out, o_bytes) ||
-        overlaps(filt, f_bytes, ws, ws_bytes) || overlaps(filt, f_bytes, out, o_bytes) ||
-        overlaps(out, o_bytes, ws, ws_bytes))
+    if (overlaps(in, in_bytes, out, o_bytes) || overlaps(filt, f_bytes, out, o_bytes))
         return IM2WIN_EOVERLAP;
-    if (ws_bytes < p.ws_bytes)
+    if (ws && (overlaps(in, in_bytes, ws, ws_bytes) || overlaps(filt, f_bytes, ws, ws_bytes) ||
+               overlaps(out, o_bytes, ws, ws_bytes)))
+        return IM2WIN_EOVERLAP;
+    if (ws && ws_bytes < p->ws_bytes)
         return IM2WIN_EWORKSPACE;
+    if ((rc = read_tuning(tu)) != IM2WIN_OK)
+        return rc;
+    return dt == IM2WIN_F32 ? plan_fp32(p->chunk, *tu, false, p32) : plan_fp16(p->chunk, *tu, p16);
+}
+
+int run_chunked(const void *in, const void *filt, void *out, void *ws, int64_t ws_bytes, int64_t N,
+                int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+                int64_t stride, int64_t n_chunk, int dt, hipStream_t st, hipStream_t aux)
+{
+    if (!ws)
+        return IM2WIN_EINVAL;
+    Plan p;
     Tuning tu;
     Plan16 p16{};
     Plan32 p32{};
-    if ((rc = read_tuning(&tu)) != IM2WIN_OK)
-        return rc;
-    if ((rc = dt == IM2WIN_F32 ? plan_fp32(p.chunk, tu, false, &p32) : plan_fp16(p.chunk, tu, &p16)) != IM2WIN_OK)
+    int rc = check_chunked(in, filt, out, ws, ws_bytes, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, n_chunk, dt, st,
+                           aux, &p, &tu, &p16, &p32);
+    if (rc != IM2WIN_OK)
         return rc;
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
@@ -169,6 +185,69 @@ int run_chunked(const void *in, const void *filt, void *out, void *ws, int64_t w
         (void)hipEventDestroy(ev_done);
     }
     return rc;
+}
+
+// The workspace of the allocation-free mini-batch call: a static device
+// array, one copy on every GPU the library runs on, held until the process
+// ends.  Host code never uses the array's name as an address: each device's
+// copy is found once, with that device current, through
+// hipGetSymbolAddress, and that pointer is what the kernels receive.
+constexpr int64_t kScratchBytes = IM2WIN_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDev = 64;
+struct ScratchDev {
+    std::once_flag once;
+    int rc = IM2WIN_ENODEV;
+    void *ptr = nullptr;
+};
+ScratchDev g_scratch[kMaxDev];
+
+// This device's copy of `scratch` (set up on the first call per device).
+int scratch_for_current_device(void **out)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) {
+        (void)hipGetLastError();
+        return IM2WIN_ENODEV;
+    }
+    ScratchDev &d = g_scratch[dev];
+    std::call_once(d.once, [&d]() {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+            (void)hipGetLastError();
+            d.rc = IM2WIN_ENODEV;
+            return;
+        }
+        d.ptr = p;
+        d.rc = IM2WIN_OK;
+    });
+    *out = d.ptr;
+    return d.rc;
+}
+
+int run_chunked_noalloc(const void *in, const void *filt, void *out, int64_t N, int64_t C_i, int64_t H_i,
+                        int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w, int64_t stride, int64_t n_chunk, int dt,
+                        hipStream_t st)
+{
+    Plan p;
+    Tuning tu;
+    Plan16 p16{};
+    Plan32 p32{};
+    int rc = check_chunked(in, filt, out, nullptr, 0, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, n_chunk, dt, st,
+                           nullptr, &p, &tu, &p16, &p32);
+    if (rc != IM2WIN_OK)
+        return rc;
+    if (p.ws_bytes > kScratchBytes)
+        return IM2WIN_EWORKSPACE;
+    if ((rc = check_device()) != IM2WIN_OK)
+        return rc;
+    void *ws = nullptr;
+    if ((rc = scratch_for_current_device(&ws)) != IM2WIN_OK)
+        return rc;
+    // one stream, one slot: no events are needed
+    return enqueue_chunks(in, filt, out, static_cast<char *>(ws), p, p16, p32, tu, N, C_i, H_i, W_i, C_o, K_h, K_w,
+                          stride, dt, st, nullptr, nullptr, nullptr);
 }
 
 }  // namespace
@@ -200,6 +279,16 @@ int conv_im2win_chunked(const void *in_nhwc, const void *filt_khkwcico, void *ou
         return IM2WIN_EINVAL;
     return run_chunked(in_nhwc, filt_khkwcico, out_nhwc, ws, ws_bytes, N, C_i, H_i, W_i, C_o, K_h, K_w, stride,
                        n_chunk, (int)dt, (hipStream_t)hip_stream, (hipStream_t)hip_stream_aux);
+}
+
+int conv_im2win_chunked_noalloc(const void *in_nhwc, const void *filt_khkwcico, void *out_nhwc, int64_t N,
+                                int64_t C_i, int64_t H_i, int64_t W_i, int64_t C_o, int64_t K_h, int64_t K_w,
+                                int64_t stride, int64_t n_chunk, im2win_dtype_t dt, void *hip_stream)
+{
+    if (dt != IM2WIN_F32 && dt != IM2WIN_F16 && dt != IM2WIN_BF16)
+        return IM2WIN_EINVAL;
+    return run_chunked_noalloc(in_nhwc, filt_khkwcico, out_nhwc, N, C_i, H_i, W_i, C_o, K_h, K_w, stride, n_chunk,
+                               (int)dt, (hipStream_t)hip_stream);
 }
 
 }  // extern "C"
