@@ -81,6 +81,29 @@ struct WinCols {
     }
 };
 
+// Order of a kernel's K loop.  A kernel walks its taps in blocks of G (a
+// stage, or part of one); linear order takes block b as taps b*G .. b*G+G-1.
+// Column order (nv filter columns of T = K_h*C_i taps each, T a multiple of
+// G) takes block b as taps v*T + tb*G .. of filter column v = b % nv, with
+// tb = b / nv: the nv column slices of one tap range follow each other.
+// Neighbouring windows share input columns (a column is slice v of one
+// window and slice v + s of the previous one), so in column order the bytes
+// one tile reads for slice v come back for slice v + s a few blocks later,
+// while they are still in L2, instead of s*T/G blocks later.  Each output
+// is still one fixed sequence of taps, so results stay deterministic.
+struct TapOrder {
+    uint32_t nv, T, G;  // nv = 1: linear
+
+    __host__ __device__ inline uint32_t map(uint32_t k) const
+    {
+        if (nv == 1)
+            return k;
+        const uint32_t b = k / G, off = k - b * G;
+        const uint32_t tb = b / nv, v = b - tb * nv;
+        return v * T + tb * G + off;
+    }
+};
+
 // Tile of a workgroup in a 1-D launch of gx * gy output tiles (gx along
 // pixels, gy along channels).  The hardware deals the workgroups of a launch
 // to the 8 XCDs round-robin (block b to XCD b % 8), each XCD with its own L2.
@@ -110,6 +133,16 @@ struct TileGrid {
 // gx * gy tiles (< 2^31, the caller's grid checks); `linear` selects the
 // launch order (to measure what the XCD-aware order gains).
 TileGrid make_tilegrid(int64_t gx, int64_t gy, bool linear);
+
+// Column order for blocks of G taps when the layer allows it (K_w > 1,
+// K_h*C_i a multiple of G) and `linear` is not set; else linear order.
+inline TapOrder make_taporder(int64_t Kw, int64_t Kh, int64_t Ci, uint32_t G, bool linear)
+{
+    const int64_t T = Kh * Ci;
+    if (linear || Kw <= 1 || T % G != 0)
+        return TapOrder{1u, (uint32_t)T, G};
+    return TapOrder{(uint32_t)Kw, (uint32_t)T, G};
+}
 
 inline WinCols make_wincols(const Shape &sh)
 {
@@ -198,6 +231,9 @@ int launch_status(hipError_t e);
 //   IM2WIN_FP32_MFMA_TILE  a matrix-core fp32 tile name
 //   IM2WIN_TRANSFORM_ORDER linear | xcd
 //   IM2WIN_TILE_ORDER      linear | xcd
+//   IM2WIN_TAP_ORDER       linear | column: the K-loop order of the DMA-staged
+//                          fp32 kernel (column by default) and of the
+//                          row-per-pixel fp16 kernel (linear by default)
 namespace im2win {
 
 struct Tuning {
@@ -208,6 +244,8 @@ struct Tuning {
     int fp32_tile;                     // register-staged tile index, -1: not forced
     int fp32_mfma_tile;                // -1: not forced
     bool transform_linear, tile_linear;
+    enum { kDefault = 0, kLinear = 1, kColumn = 2 };
+    int tap_order;  // kDefault: each kernel's own (column for the DMA fp32 kernel, linear for the others)
 };
 int read_tuning(Tuning *t);
 

@@ -48,6 +48,7 @@ struct C16Args {
     uint32_t pk_bytes;       // bytes of the packed filter
     TileGrid tg;             // pixel x channel tiles of the 1-D launch
     FastDiv div_Wo;
+    TapOrder to;             // order of the row kernel's 64-tap stages
 };
 
 // ---------------------------------------------------------------------------
@@ -371,6 +372,7 @@ struct Pipe {
     uint32_t voff[C::I];    // byte offset of this lane's chunk at tap 0 (kOOB: no pixel)
     uint32_t vchunk[C::I];  // first tap of this lane's chunk within a stage
     uint32_t wave, lane, K, nst, apitch;
+    TapOrder to;
     uint32_t arow, brow;
     floatx16 acc[WM][WN];
 
@@ -378,16 +380,18 @@ struct Pipe {
     // range and the slot is filled with zeros.
     __device__ inline void issue(uint32_t s, char *stage)
     {
-        const uint32_t k0 = s * BK;
+        // first tap of the stage (column order only when every stage is
+        // whole: K_h*C_i a multiple of 64)
+        const uint32_t k0 = to.map(s * BK);
         const bool tail = k0 + BK > K;
         const bool past = s >= nst;
 #pragma unroll
         for (int j = 0; j < C::I; ++j) {
             const uint32_t b = wave + C::NW * j;
             const bool filt = b < (uint32_t)C::BMc / 8;
-            // filter rows: stage s is tile s of the packed filter (apitch
-            // bytes each); window rows: taps k0 .. k0+63 of the window
-            uint32_t off = voff[j] + (filt ? s * apitch : 2u * k0);
+            // filter rows: taps k0 .. k0+63 are tile k0/64 of the packed
+            // filter (apitch bytes each); window rows: taps k0 .. k0+63
+            uint32_t off = voff[j] + (filt ? (k0 / BK) * apitch : 2u * k0);
             if (past || (!filt && tail && k0 + vchunk[j] >= K))
                 off = kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(filt ? rf : rw, (lds_ptr)(stage + 1024 * b), 16, off,
@@ -495,6 +499,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
     // the packed filter in 64-tap tiles of C_o_pad rows: row ch0 of tile 0 on
     w.rf = make_rsrc(a.packed + (uint64_t)ch0 * BK, a.pk_bytes - ch0 * (uint32_t)BK * 2u);
     w.apitch = a.Co_pad * (uint32_t)BK * 2u;
+    w.to = a.to;
     for (uint32_t t = tid; t < C::BNp; t += C::NT) {
         const uint32_t p = p0 + t;
         uint32_t off = 0;
@@ -708,6 +713,12 @@ hipError_t launch_conv_fp16(const Shape &sh, const Plan16 &p, const Tuning &t, c
     a.pk_bytes = (uint32_t)(sh.Co_pad * sh.K_pad * 2);  // < 2^31 (checked with the shape)
     a.Co = (uint32_t)sh.Co; a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.wc = make_wincols(sh);
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
+    // Linear tap order unless IM2WIN_TAP_ORDER=column asks for the row
+    // kernel's stages in column order: on the row kernel's layers column
+    // order measured from +3 % (3x3 64 -> 128 at 112x112) to -10 % (3x3
+    // 256 -> 512 at 12x12), where the filter tiles' L2 reuse suffers.  The
+    // register-staged kernel always walks its taps in linear order.
+    a.to = make_taporder(sh.Kw, sh.Kh, sh.Ci, (uint32_t)BK, t.tap_order != Tuning::kColumn || p.fam != Fam16::Pipe);
     void *args[] = {&a};
     if (p.fam == Fam16::Pipe) {
         int n;

@@ -381,6 +381,9 @@ const ColVariant *col_variants(int *n)
         // eight waves, 256 x 256 tiles (large C_o)
         col_variant<3, 32, 4, 2, 2, 4, 320, 2>("k3c256p256t32s2w8"),
         col_variant<3, 32, 2, 3, 4, 2, 256, 2>("k3c256p192t32s2w8"),
+        // 32-tap stages for 7-wide filters (two slots, 128 KiB: one
+        // workgroup per CU)
+        col_variant<7, 32, 2, 2, 1, 4, 544, 2>("k7c64p256t32s2"),
         // serialized rings of three of the above (check variants)
         col_variant<3, 32, 1, 2, 2, 2, 160, 2, true>("k3c64p128t32s2-serial"),
         col_variant<7, 16, 2, 2, 1, 4, 544, 3, true>("k7c64p256t16s3-serial"),
@@ -461,8 +464,11 @@ int col_default(const Shape &sh)
     // lose (S5: 536 vs 636), so those layers keep the row kernel.
     auto tiles = [&](int64_t bn) { return ((sh.P + bn - 1) / bn) * ((sh.Co + 255) / 256); };
     const char *name = nullptr;
-    if (fp16_single_slot_rows(sh))
-        return -1;  // the one-slot row kernel is faster there
+    // the one-slot row kernel is faster on many-tile layers with C_o >= 128,
+    // except 3x3 layers with C_o <= 128 (3x3 64 -> 128 at 112x112: column
+    // kernel 664 vs 636 TFLOP/s)
+    if (fp16_single_slot_rows(sh) && !(sh.Kw == 3 && sh.Co <= 128))
+        return -1;
     // C_o <= 64: 64 x 128 tiles, three workgroups per CU, more bytes in
     // flight for these HBM-bound layers (3x3 C=64 at 56x56: 484 vs 431
     // TFLOP/s same-process; with C_o = 128, 3x3 at 28x28, 531 vs 548)
@@ -476,12 +482,20 @@ int col_default(const Shape &sh)
     // it lost, 668 vs 701
     else if (sh.Kw == 7 && sh.s == 1 && sh.Co <= 64)
         name = "k7c64p128t16s2";
+    // with stride 2 and C_o <= 64 (7x7 C=64 at 224x224) 32-tap stages in a
+    // two-slot ring beat the three-slot 16-tap ring: 705 vs 684 TFLOP/s
+    else if (sh.Kw == 7 && sh.Co <= 64)
+        name = "k7c64p256t32s2";
     else if (sh.Kw == 7 && sh.Co <= 128)
         name = "k7c64p256t16s3";
     else if (sh.Kw == 3 && tiles(192) >= 160 && tiles(192) <= 256)
         name = "k3c256p192t32s2w8";
     else if (sh.Kw == 3 && tiles(256) >= 160 && tiles(256) <= 256)
         name = "k3c256p256t32s2w8";
+    // 3x3 C=256 at 14x14 (128 images): four 64 x 128 channel tiles per
+    // pixel tile beat the 128 x 128 row kernel, 583 vs 529 TFLOP/s
+    else if (sh.Kw == 3 && sh.Co <= 256)
+        name = "k3c64p128t32s2";
     else
         return -1;
     const int pick = col_find(name);

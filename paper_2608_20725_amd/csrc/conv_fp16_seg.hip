@@ -320,6 +320,9 @@ const SegVariant *seg_variants(int *n)
         seg_variant<2, 2, 1, 4, 2560, 16>("s64p256"),
         seg_variant<3, 1, 1, 4, 2560, 16>("s96p128"),
         seg_variant<2, 2, 2, 2, 2560, 16>("s128p128"),
+        // smaller segment areas (more workgroups per CU) for short windows
+        seg_variant<2, 1, 1, 4, 1024, 16>("s64p128g1024"),
+        seg_variant<2, 2, 1, 4, 2048, 16>("s64p256g2048"),
         // serialized filter ring (check variant)
         seg_variant<2, 2, 1, 4, 2560, 16, true>("s64p256-serial"),
     };

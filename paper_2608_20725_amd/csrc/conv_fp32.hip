@@ -44,6 +44,7 @@ struct C32Args {
     uint32_t P, K, K_pad, Co, Co_pad, Wo, L;
     WinCols wc;              // window start of an output column in its strip
     FastDiv div_Wo;
+    TapOrder to;             // order of the 16-tap blocks (the DMA-staged kernel's)
 };
 
 // ---------------------------------------------------------------------------
@@ -392,16 +393,18 @@ __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
     cfloat *fp = (cfloat *)a.packed + jw;
     for (uint32_t st = 0; st < nst; ++st) {
         if (st + 1 < nst) {
-            stg.load(rs, rowoff, p0, (st + 1) * KC, a);
+            // first tap of stage st+1 (KC divides the 16-tap blocks of the order)
+            const uint32_t k1 = a.to.map((st + 1) * KC);
+            stg.load(rs, rowoff, p0, k1, a);
             if (FL)
-                fst.load(rf, (st + 1) * KC, jb, a.Co_pad);
+                fst.load(rf, k1, jb, a.Co_pad);
         }
         if (active) {
             if constexpr (FL)
                 stage_fma_lds<TM, TN, KC, G::LDA, CW>(acc, As[st & 1], Fs[st & 1], wave, lane);
             else
                 stage_fma<TM, TN, KC, TP, G::LDA>(acc, As[st & 1],
-                                                  fp + (uint64_t)st * KC * a.Co_pad, a.Co_pad, lane);
+                                                  fp + (uint64_t)a.to.map(st * KC) * a.Co_pad, a.Co_pad, lane);
         }
         if (st + 1 < nst) {
             stg.store(As[(st + 1) & 1]);
@@ -530,6 +533,9 @@ hipError_t launch_conv_fp32(const Shape &sh, const Plan32 &p, const Tuning &t, c
     a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
     a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.wc = make_wincols(sh);
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
+    // the DMA-staged kernel's tap order (16-tap blocks), so both sum every
+    // output in the same order
+    a.to = make_taporder(sh.Kw, sh.Kh, sh.Ci, 16u, t.tap_order == Tuning::kLinear);
 
     const Tile &tile = kTiles[p.v];
     // Channel groups per workgroup: the largest of 8, 4, 2, 1 waves (TN

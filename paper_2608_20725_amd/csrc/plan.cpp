@@ -28,11 +28,11 @@ int read_name(const char *var, int (*find)(const char *), int *out)
 }
 
 // linear | xcd (the default); anything else is an error.
-int read_order(const char *var, bool *linear)
+int read_order(const char *var, const char *other, bool *linear)
 {
     *linear = false;
     const char *e = getenv(var);
-    if (!e || !*e || strcmp(e, "xcd") == 0)
+    if (!e || !*e || strcmp(e, other) == 0)
         return IM2WIN_OK;
     if (strcmp(e, "linear") == 0) {
         *linear = true;
@@ -66,9 +66,18 @@ int read_tuning(Tuning *t)
         t->fp32_kernel = -2;
     else if ((rc = read_name("IM2WIN_FP32_KERNEL", dma32_find, &t->fp32_kernel)) != IM2WIN_OK)
         return rc;
-    if ((rc = read_order("IM2WIN_TRANSFORM_ORDER", &t->transform_linear)) != IM2WIN_OK ||
-        (rc = read_order("IM2WIN_TILE_ORDER", &t->tile_linear)) != IM2WIN_OK)
+    if ((rc = read_order("IM2WIN_TRANSFORM_ORDER", "xcd", &t->transform_linear)) != IM2WIN_OK ||
+        (rc = read_order("IM2WIN_TILE_ORDER", "xcd", &t->tile_linear)) != IM2WIN_OK)
         return rc;
+    t->tap_order = Tuning::kDefault;
+    if (const char *e = getenv("IM2WIN_TAP_ORDER")) {
+        if (strcmp(e, "linear") == 0)
+            t->tap_order = Tuning::kLinear;
+        else if (strcmp(e, "column") == 0)
+            t->tap_order = Tuning::kColumn;
+        else if (*e)
+            return IM2WIN_EINVAL;
+    }
     // contradictory choices
     const int fam16 = (t->fp16_col >= 0) + (t->fp16_seg >= 0) + (t->fp16_tile >= 0 || t->fp16_kernel == Tuning::kPipe) +
                       (t->fp16_kernel == Tuning::kRegs);

@@ -95,15 +95,16 @@ def check_out_sampled(out, x, w, s, dtype, images, seed):
 
 # (layer shape, n_chunk, dtype): the benchmark's mini-batch configuration in
 # both precisions, and chunkings whose last chunk on its own would pick
-# another kernel: 3x3 C=128 at 56x56 (48-image chunks run the one-slot row
-# kernel, a 32-image batch the column-staged one with another filter
-# layout), and 56x56 C=64 fp32 in 100-image chunks (the 256-pixel tile;
-# 28 images alone take the tap-split tile).
+# another kernel: 3x3 C=512 at 14x14 in 128-image chunks (a full chunk runs
+# the column-staged 256 x 192 tile, the 32 images of the last chunk alone
+# would run the row kernel, whose packed filter has another layout), and
+# 56x56 C=64 fp32 in 100-image chunks (the 256-pixel tile; 28 images alone
+# take the tap-split tile).
 FULL_SIZE = [
     ((128, 64, 56, 56, 64, 3, 3, 1), 32, torch.float32),
     ((128, 64, 56, 56, 64, 3, 3, 1), 32, torch.float16),
-    ((128, 128, 56, 56, 128, 3, 3, 1), 48, torch.float16),
-    ((128, 128, 56, 56, 128, 3, 3, 1), 48, torch.bfloat16),
+    ((160, 512, 14, 14, 512, 3, 3, 1), 128, torch.float16),
+    ((160, 512, 14, 14, 512, 3, 3, 1), 128, torch.bfloat16),
     ((128, 64, 56, 56, 64, 3, 3, 1), 100, torch.float32),
 ]
 

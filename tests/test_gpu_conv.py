@@ -288,6 +288,44 @@ def test_ring_matches_serialized_ring(case, monkeypatch):
     assert torch.equal(outs[0].view(bits), outs[1].view(bits))
 
 
+# The K-loop tap order (IM2WIN_TAP_ORDER): linear, or column slices of one
+# tap range in turn.  Both are fixed orders that the oracle bounds; the
+# DMA-staged fp32 kernel (column by default) and the register-staged one
+# follow the same order, so they agree bit for bit in either.
+TAP_CASES = [
+    # (shape, dtype, forced variables)
+    ((2, 16, 17, 19, 100, 3, 3, 1), torch.float32, {"IM2WIN_FP32_KERNEL": "p8c8l8s2k16"}),
+    ((2, 16, 23, 41, 40, 7, 7, 2), torch.float32, {"IM2WIN_FP32_KERNEL": "p4c12l8s2k16"}),
+    ((2, 64, 14, 14, 200, 3, 3, 1), torch.float32, {"IM2WIN_FP32_KERNEL": "p4c8l8s2k16t4"}),
+    ((2, 64, 20, 20, 96, 3, 3, 1), torch.float16, {"IM2WIN_FP16_KERNEL": "pipe"}),
+    ((2, 64, 20, 20, 200, 5, 5, 2), torch.bfloat16, {"IM2WIN_FP16_TILE": "c128p128s1"}),
+]
+
+
+@pytest.mark.parametrize("case", TAP_CASES, ids=lambda c: _id(c[0]) + "-" + str(c[1])[6:])
+def test_tap_orders(case, monkeypatch):
+    shape, dtype, env = case
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=59)
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    bits = torch.int32 if dtype == torch.float32 else torch.int16
+    for order in ("linear", "column"):
+        monkeypatch.setenv("IM2WIN_TAP_ORDER", order)
+        say("tap order", order, shape, dtype, env)
+        run = Run(x, w, s, dtype)
+        check_full(run, x, w)
+        run.check_out_guards()
+        if env.get("IM2WIN_FP32_KERNEL", "").endswith("k16"):
+            # the register-staged kernel sums in the same order as the
+            # DMA-staged ones that do not split a stage's taps
+            first = run.out.clone()
+            monkeypatch.setenv("IM2WIN_FP32_KERNEL", "regs")
+            run2 = Run(x, w, s, dtype)
+            monkeypatch.setenv("IM2WIN_FP32_KERNEL", env["IM2WIN_FP32_KERNEL"])
+            assert torch.equal(first.view(bits), run2.out.view(bits))
+
+
 # The XCD-aware tile order (several channel tiles) against launch order
 # (IM2WIN_TILE_ORDER=linear): each tile computes the same sums whichever
 # workgroup takes it, so the outputs agree bit for bit.  Grids with a ragged

@@ -12,7 +12,8 @@ from paper_2608_20725_amd import workloads
 
 EINVAL = -1
 VARS = ("IM2WIN_FP16_KERNEL", "IM2WIN_FP16_COL", "IM2WIN_FP16_TILE", "IM2WIN_FP16_SEG", "IM2WIN_FP32_KERNEL",
-        "IM2WIN_FP32_TILE", "IM2WIN_FP32_MFMA_TILE", "IM2WIN_TRANSFORM_ORDER", "IM2WIN_TILE_ORDER")
+        "IM2WIN_FP32_TILE", "IM2WIN_FP32_MFMA_TILE", "IM2WIN_TRANSFORM_ORDER", "IM2WIN_TILE_ORDER",
+        "IM2WIN_TAP_ORDER")
 
 
 @pytest.fixture(autouse=True)
@@ -126,6 +127,11 @@ def test_orders_accept_both_names(monkeypatch):
         monkeypatch.setenv("IM2WIN_TILE_ORDER", v)
         monkeypatch.setenv("IM2WIN_TRANSFORM_ORDER", v)
         assert name((1, 64, 10, 10, 64, 3, 3, 1), "f16")
+    for v in ("linear", "column"):
+        monkeypatch.setenv("IM2WIN_TAP_ORDER", v)
+        assert name((1, 64, 10, 10, 64, 3, 3, 1), "f32")
+    monkeypatch.setenv("IM2WIN_TAP_ORDER", "xcd")   # the tile orders' word is not a tap order
+    assert status((1, 64, 10, 10, 64, 3, 3, 1), "f32") == EINVAL
 
 
 # The mini-batch path makes its plan for a full chunk and runs it on the
@@ -133,8 +139,8 @@ def test_orders_accept_both_names(monkeypatch):
 # on the last chunk would pick another kernel (and, for the 16-bit path,
 # another packed-filter layout), the case the single plan exists for.
 @pytest.mark.parametrize("shape,n_chunk,dt", [
-    ((128, 128, 56, 56, 128, 3, 3, 1), 48, "f16"),
-    ((128, 128, 56, 56, 128, 3, 3, 1), 48, "bf16"),
+    ((160, 512, 14, 14, 512, 3, 3, 1), 128, "f16"),
+    ((160, 512, 14, 14, 512, 3, 3, 1), 128, "bf16"),
     ((128, 64, 56, 56, 64, 3, 3, 1), 100, "f32"),
 ])
 def test_chunk_plan_differs_from_last_chunk_standalone(shape, n_chunk, dt):
