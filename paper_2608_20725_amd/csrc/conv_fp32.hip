@@ -44,7 +44,7 @@ struct C32Args {
     uint32_t P, K, K_pad, Co, Co_pad, Wo, L;
     WinCols wc;              // window start of an output column in its strip
     FastDiv div_Wo;
-    TapOrder to;             // order of the 16-tap blocks (the DMA-staged kernel's)
+    TapOrder to;             // order of the tap blocks (the DMA-staged kernel's)
 };
 
 // ---------------------------------------------------------------------------
@@ -393,7 +393,7 @@ __global__ __launch_bounds__(64 * WAVES) void conv_fp32_kernel(C32Args a)
     cfloat *fp = (cfloat *)a.packed + jw;
     for (uint32_t st = 0; st < nst; ++st) {
         if (st + 1 < nst) {
-            // first tap of stage st+1 (KC divides the 16-tap blocks of the order)
+            // first tap of stage st+1 (KC divides the tap blocks of the order)
             const uint32_t k1 = a.to.map((st + 1) * KC);
             stg.load(rs, rowoff, p0, k1, a);
             if (FL)
@@ -535,7 +535,7 @@ hipError_t launch_conv_fp32(const Shape &sh, const Plan32 &p, const Tuning &t, c
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     // the DMA-staged kernel's tap order (16-tap blocks), so both sum every
     // output in the same order
-    a.to = make_taporder(sh.Kw, sh.Kh, sh.Ci, 16u, t.tap_order == Tuning::kLinear);
+    a.to = make_taporder(sh.Kw, sh.Kh, sh.Ci, kTapBlock32, t.tap_order == Tuning::kLinear);
 
     const Tile &tile = kTiles[p.v];
     // Channel groups per workgroup: the largest of 8, 4, 2, 1 waves (TN
