@@ -60,7 +60,12 @@
  * IM2WIN_FP16_KERNEL (pipe | regs), IM2WIN_FP16_COL, IM2WIN_FP16_TILE,
  * IM2WIN_FP16_SEG, IM2WIN_FP32_KERNEL (a variant name | regs),
  * IM2WIN_FP32_TILE, IM2WIN_FP32_MFMA_TILE (variant names),
- * IM2WIN_TRANSFORM_ORDER and IM2WIN_TILE_ORDER (xcd | linear).  A value
+ * IM2WIN_TRANSFORM_ORDER and IM2WIN_TILE_ORDER (xcd | linear),
+ * IM2WIN_TAP_ORDER (linear | column), IM2WIN_FP16_SPLIT (1..8: the K range
+ * of the row-per-pixel fp16 kernel split over that many workgroups per output
+ * tile, their fp32 partial tiles added afterwards in a fixed order; a split
+ * the default plan does not make needs ks * tiles * 64 KiB of workspace beyond
+ * conv_workspace_bytes, else IM2WIN_EWORKSPACE).  A value
  * that names no kernel, contradictory values, or a forced kernel that cannot
  * run the layer make the call return IM2WIN_EINVAL (checked after the
  * workspace size, before the device).  Numerics: fp32 conv accumulates in fp32 (FMA); fp16 and bf16 conv

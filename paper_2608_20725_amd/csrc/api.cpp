@@ -114,7 +114,17 @@ int64_t packed_filter_bytes(const Shape &sh, int dt)
     return valu > mfma ? valu : mfma;
 }
 
-int64_t workspace_bytes(const Shape &sh, int dt) { return sh.pad_end + packed_filter_bytes(sh, dt); }
+int64_t workspace_bytes(const Shape &sh, int dt)
+{
+    const int64_t base = sh.pad_end + packed_filter_bytes(sh, dt);
+    if (dt == IM2WIN_F32)
+        return base;
+    // the split-K region of the plan a call makes without tuning variables
+    Plan16 p;
+    if (plan_fp16(sh, default_tuning(), &p) != IM2WIN_OK)
+        return base;
+    return base + split_bytes(sh, p);
+}
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -425,13 +435,18 @@ int conv16(void *ws, int64_t ws_bytes, const uint16_t *filt_khkwcico, uint16_t *
     Plan16 plan;
     if ((rc = read_tuning(&tu)) != IM2WIN_OK || (rc = plan_fp16(sh, tu, &plan)) != IM2WIN_OK)
         return rc;
+    // a K split forced through the tuning may need more than the default plan
+    const int64_t pf = packed_filter_bytes(sh, dt);
+    if (ws_bytes < sh.pad_end + pf + split_bytes(sh, plan))
+        return IM2WIN_EWORKSPACE;
     if ((rc = check_device()) != IM2WIN_OK)
         return rc;
     void *packed = (char *)ws + sh.pad_end;
+    void *split = plan.ks > 1 ? (char *)packed + pf : nullptr;
     const hipStream_t st = (hipStream_t)hip_stream;
-    if ((rc = launch_status(launch_pack_fp16(sh, plan, filt_khkwcico, packed, st))) != IM2WIN_OK)
+    if ((rc = launch_status(launch_pack_fp16(sh, plan, filt_khkwcico, packed, st, split))) != IM2WIN_OK)
         return rc;
-    return launch_status(launch_conv_fp16(sh, plan, tu, ws, packed, out_nhwc, st, op));
+    return launch_status(launch_conv_fp16(sh, plan, tu, ws, packed, out_nhwc, st, op, split));
 }
 
 }  // namespace

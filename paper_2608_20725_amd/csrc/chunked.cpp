@@ -147,7 +147,15 @@ int check_chunked(const void *in, const void *filt, void *out, void *ws, int64_t
         return IM2WIN_EWORKSPACE;
     if ((rc = read_tuning(tu)) != IM2WIN_OK)
         return rc;
-    return dt == IM2WIN_F32 ? plan_fp32(p->chunk, *tu, false, p32) : plan_fp16(p->chunk, *tu, p16);
+    if (dt == IM2WIN_F32)
+        return plan_fp32(p->chunk, *tu, false, p32);
+    // Chunks run the row-per-pixel kernel without a K split: the split's
+    // counters and partial tiles would be shared by the chunks in flight on
+    // the two streams.  A split forced through the tuning is refused.
+    if (tu->fp16_split > 1)
+        return IM2WIN_EINVAL;
+    tu->fp16_split = 1;
+    return plan_fp16(p->chunk, *tu, p16);
 }
 
 int run_chunked(const void *in, const void *filt, void *out, void *ws, int64_t ws_bytes, int64_t N,

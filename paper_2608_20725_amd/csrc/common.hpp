@@ -115,9 +115,11 @@ struct TapOrder {
 struct TileGrid {
     uint32_t gx, gy, xcd;
 
-    __device__ inline void tile(uint32_t &x, uint32_t &y) const
+    __device__ inline void tile(uint32_t &x, uint32_t &y) const { tile_of(blockIdx.x, x, y); }
+
+    // Tile of block b (b < gx * gy).
+    __device__ inline void tile_of(uint32_t b, uint32_t &x, uint32_t &y) const
     {
-        const uint32_t b = blockIdx.x;
         if (!xcd) {
             y = b / gx;
             x = b - y * gx;
@@ -240,6 +242,10 @@ int launch_status(hipError_t e);
 //   IM2WIN_TAP_ORDER       linear | column: the K-loop order of the DMA-staged
 //                          fp32 kernel (column by default) and of the
 //                          row-per-pixel fp16 kernel (linear by default)
+//   IM2WIN_FP16_SPLIT      1..kMaxSplit: K split of the row-per-pixel fp16
+//                          kernel (refused for other kernels, for a split
+//                          that leaves a block no stage, and in the
+//                          mini-batch path)
 namespace im2win {
 
 struct Tuning {
@@ -252,8 +258,15 @@ struct Tuning {
     bool transform_linear, tile_linear;
     enum { kDefault = 0, kLinear = 1, kColumn = 2 };
     int tap_order;  // kDefault: each kernel's own (column for the DMA fp32 kernel, linear for the others)
+    int fp16_split; // K split of the row-per-pixel kernel: 0 (the planner's choice) or 1..kMaxSplit
 };
 int read_tuning(Tuning *t);
+// The tuning every call runs without tuning variables.
+Tuning default_tuning();
+
+// K split of the row-per-pixel fp16 kernel: at most this many workgroups per
+// output tile.
+constexpr int kMaxSplit = 8;
 
 // Variant tables of each kernel family: index of a name, -1 if none.
 int col_find(const char *name);
@@ -272,7 +285,8 @@ int mfma32_find(const char *name);
 enum class Fam16 { Col, Pipe, Seg, Regs };
 struct Plan16 {
     Fam16 fam;
-    int v;  // variant index within the family (Regs: 0..2 tile by C_o)
+    int v;       // variant index within the family (Regs: 0..2 tile by C_o)
+    int ks = 1;  // row-per-pixel kernel: K split over ks workgroups per tile (1: none)
 };
 enum class Fam32 { Dma, Regs, Mfma };
 struct Plan32 {
@@ -281,6 +295,9 @@ struct Plan32 {
 };
 // IM2WIN_OK, or IM2WIN_EINVAL for a forced kernel that cannot run the layer.
 int plan_fp16(const Shape &sh, const Tuning &t, Plan16 *p);
+// Bytes of the split-K region of a plan (the fp32 partial tiles), placed
+// after the packed filter; 0 when ks = 1.
+int64_t split_bytes(const Shape &sh, const Plan16 &p);
 int plan_fp32(const Shape &sh, const Tuning &t, bool mfma, Plan32 *p);
 // "family variant", e.g. "conv_fp16_col k3c64p128t32s2"; at most 63 characters.
 void plan16_name(const Shape &sh, const Plan16 &p, char *buf, int len);
@@ -325,10 +342,12 @@ const char *mfma32_name(int v);
 // Operand type of the 16-bit matrix-core kernels (every one of them is
 // instantiated for both).
 enum class Op16 { F16, BF16 };
+// `split`: the plan's split-K region (split_bytes(sh, p) bytes), nullptr when
+// ks = 1 (the pack does not use it).
 hipError_t launch_pack_fp16(const Shape &sh, const Plan16 &p, const uint16_t *filt, void *packed,
-                            hipStream_t st);
+                            hipStream_t st, void *split = nullptr);
 hipError_t launch_conv_fp16(const Shape &sh, const Plan16 &p, const Tuning &t, const void *ws,
-                            const void *packed, uint16_t *out, hipStream_t st, Op16 op);
+                            const void *packed, uint16_t *out, hipStream_t st, Op16 op, void *split = nullptr);
 // Column-staged fp16 kernel: the default variant for this layer (-1: the
 // row-per-pixel kernels run), whether a variant can run it, its name and
 // taps per stage (the packed-filter tile).
@@ -336,6 +355,9 @@ int col_default(const Shape &sh);
 bool col_fits(const Shape &sh, int v);
 const char *col_name(int v);
 int col_stage_taps(int v);
+// Rows of each packed filter slice of the column-staged kernel: C_o rounded up
+// to the variant's channels per tile (at most C_o_pad).
+int64_t col_packed_rows(const Shape &sh, int v);
 // The layer runs the one-slot row-per-pixel fp16 kernel (many tiles, C_o >= 128).
 bool fp16_single_slot_rows(const Shape &sh);
 // Segment-staged fp16 kernel for windows that are not 16-byte aligned: the
@@ -347,7 +369,12 @@ hipError_t launch_conv_fp16_seg(const Shape &sh, int v, const void *ws, const vo
                                 uint16_t *out, hipStream_t st, Op16 op);
 hipError_t launch_conv_fp16_col(const Shape &sh, int v, const Tuning &t, const void *ws, const void *packed,
                                 uint16_t *out, hipStream_t st, Op16 op);
-// Row-per-pixel fp16 tiles: default for the layer, name.
+// Row-per-pixel fp16 tiles: default for the layer, name, and the K split the
+// planner picks for a tile (1: none).
 int pipe_default(const Shape &sh);
 const char *pipe_name(int v);
+int pipe_split_default(const Shape &sh, int v);
+// Output tiles of a row-per-pixel variant on a layer, and its 64-tap stages.
+int64_t pipe_tiles(const Shape &sh, int v);
+int64_t pipe_tile_elems(int v);
 } // namespace im2win

@@ -49,6 +49,12 @@ struct C16Args {
     TileGrid tg;             // pixel x channel tiles of the 1-D launch
     FastDiv div_Wo;
     TapOrder to;             // order of the row kernel's 64-tap stages
+    // K split (row kernel): block b works on tile b % ntiles over stages
+    // z*spl .. z*spl+spl-1, z = b / ntiles; with ks > 1 each block stores its
+    // fp32 partial tile in `part` and split_sum adds the ks partials of every
+    // output afterwards.
+    float *part;
+    uint32_t ks, spl, ntiles;
 };
 
 // ---------------------------------------------------------------------------
@@ -372,6 +378,7 @@ struct Pipe {
     uint32_t voff[C::I];    // byte offset of this lane's chunk at tap 0 (kOOB: no pixel)
     uint32_t vchunk[C::I];  // first tap of this lane's chunk within a stage
     uint32_t wave, lane, K, nst, apitch;
+    uint32_t sb;  // first stage of this block's K range
     TapOrder to;
     uint32_t arow, brow;
     floatx16 acc[WM][WN];
@@ -382,7 +389,7 @@ struct Pipe {
     {
         // first tap of the stage (column order only when every stage is
         // whole: K_h*C_i a multiple of 64)
-        const uint32_t k0 = to.map(s * BK);
+        const uint32_t k0 = to.map((s + sb) * BK);
         const bool tail = k0 + BK > K;
         const bool past = s >= nst;
 #pragma unroll
@@ -467,6 +474,76 @@ struct Pipe {
     }
 };
 
+// Partial tile of a block of a K-split launch (K range z of tile `tile`),
+// stored in accumulator order: wave w, block (i, j), accumulator quad q, lane
+// l at float offset ((w*WM + i)*WN + j)*4 + q)*256 + 4*l of the tile's slot, so
+// each store instruction writes 1 KiB contiguously.  split_sum reads them back
+// with the same numbering.
+template <int WM, int WN>
+__device__ inline void split_store(const floatx16 (&acc)[WM][WN], const C16Args &a, uint32_t z, uint32_t tile,
+                                   uint32_t wave, uint32_t lane, uint32_t nwaves)
+{
+    constexpr int WE = WM * WN * 16 * 64;  // floats per wave
+    float *dst = a.part + ((uint64_t)z * a.ntiles + tile) * ((uint64_t)nwaves * WE) + (uint64_t)wave * WE;
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                *reinterpret_cast<float4 *>(dst + ((i * WN + j) * 4 + q) * 256 + 4 * lane) =
+                    make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+}
+
+// Second kernel of a K-split launch: every output is the sum of its ks
+// partials, added in the fixed order z = 0, 1, ..., ks-1 (reproducible run to
+// run), rounded to 16 bits once.  One thread per accumulator quad of a tile
+// (4 consecutive channels of one pixel).
+struct SumArgs {
+    const float *part;
+    uint16_t *out;
+    uint64_t quads;           // ntiles * tile_elems / 4
+    uint32_t ks, ntiles, P, Co;
+    uint32_t WM, WN, WGN, BMc, BNp, tile_quads;
+    TileGrid tg;
+};
+
+template <class E>
+__global__ __launch_bounds__(256) void split_sum(SumArgs a)
+{
+    const uint64_t u = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (u >= a.quads)
+        return;
+    const uint32_t tile = (uint32_t)(u / a.tile_quads), r = (uint32_t)(u - (uint64_t)tile * a.tile_quads);
+    const uint32_t wq = a.WM * a.WN * 4 * 64;  // quads per wave
+    const uint32_t wave = r / wq, r2 = r - wave * wq;
+    const uint32_t lane = r2 & 63, r3 = r2 >> 6, q = r3 & 3, ij = r3 >> 2;
+    const uint32_t j = ij % a.WN, i = ij / a.WN;
+    const uint32_t wm = wave / a.WGN, wn = wave - wm * a.WGN;
+    uint32_t tx, ty;
+    a.tg.tile_of(tile, tx, ty);
+    const uint32_t p = tx * a.BNp + wn * 32 * a.WN + 32 * j + (lane & 31);
+    const uint32_t c = ty * a.BMc + wm * 32 * a.WM + 32 * i + 8 * q + 4 * (lane >> 5);
+    if (p >= a.P || c >= a.Co)
+        return;
+    const uint64_t stride = (uint64_t)a.ntiles * a.tile_quads;
+    const float4 *src = reinterpret_cast<const float4 *>(a.part) + u;
+    float4 sum = src[0];
+    for (uint32_t z = 1; z < a.ks; ++z) {
+        const float4 v = src[z * stride];
+        sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
+    }
+    const uint32_t h[4] = {E::bits(sum.x), E::bits(sum.y), E::bits(sum.z), E::bits(sum.w)};
+    uint16_t *o = a.out + (uint64_t)p * a.Co + c;
+    if (c + 3 < a.Co && (a.Co & 3) == 0) {
+        *reinterpret_cast<uint2 *>(o) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    } else {
+        for (int e = 0; e < 4; ++e)
+            if (c + e < a.Co)
+                o[e] = (uint16_t)h[e];
+    }
+}
+
 template <class E, int WM, int WN, int WGM, int WGN, int NSTAGE>
 __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
 {
@@ -485,10 +562,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
     w.lane = tid & 63;
     w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     w.K = a.K;
-    w.nst = a.K_pad / BK;
+    // this block's tile and K range
+    const uint32_t z = blockIdx.x / a.ntiles, tile = blockIdx.x - z * a.ntiles;
+    const uint32_t nst_all = a.K_pad / BK;
+    w.sb = z * a.spl;
+    w.nst = w.sb >= nst_all ? 0u : nst_all - w.sb < a.spl ? nst_all - w.sb : a.spl;
     const uint32_t wm = w.wave / WGN, wn = w.wave % WGN;
     uint32_t tx, ty;
-    a.tg.tile(tx, ty);
+    a.tg.tile_of(tile, tx, ty);
     const uint32_t p0 = tx * C::BNp;
     const uint32_t ch0 = ty * C::BMc;
 
@@ -571,6 +652,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
     // no load may still be writing LDS when the workgroup ends
     wait_vmcnt<0>();
 
+    if (a.ks > 1) {
+        split_store<WM, WN>(w.acc, a, z, tile, w.wave, w.lane, C::NW);
+        return;
+    }
     if constexpr (epilogue16_bytes<C::BMc, C::BNp>() <= C::STAGE) {
         store_tile_lds<E, WM, WN, WGM, WGN>(w.acc, r0, a.out, a.P, a.Co, p0, ch0, wm, wn, w.lane, tid);
         return;
@@ -591,6 +676,7 @@ struct PipeVariant {
     const char *name;
     const void *f[2];  // fp16 and bf16 operands
     int bm, bn, nt;
+    int wm, wn, wgn;   // wave tile (MFMA blocks) and waves along pixels
 };
 
 template <int WM, int WN, int WGM, int WGN, int NS>
@@ -599,7 +685,7 @@ PipeVariant pipe_variant(const char *name)
     return PipeVariant{name,
                        {(const void *)&conv_fp16_pipe<F16Op, WM, WN, WGM, WGN, NS>,
                         (const void *)&conv_fp16_pipe<BF16Op, WM, WN, WGM, WGN, NS>},
-                       32 * WM * WGM, 32 * WN * WGN, 64 * WGM * WGN};
+                       32 * WM * WGM, 32 * WN * WGN, 64 * WGM * WGN, WM, WN, WGN};
 }
 
 // Tile shapes of the pipelined kernel: channels x pixels per workgroup,
@@ -652,6 +738,48 @@ const char *pipe_name(int v)
     return pipe_variants(&n)[v].name;
 }
 
+int64_t pipe_tiles(const Shape &sh, int v)
+{
+    int n;
+    const PipeVariant &pv = pipe_variants(&n)[v];
+    return ((sh.P + pv.bn - 1) / pv.bn) * ((sh.Co + pv.bm - 1) / pv.bm);
+}
+
+int64_t pipe_tile_elems(int v)
+{
+    int n;
+    const PipeVariant &pv = pipe_variants(&n)[v];
+    return (int64_t)pv.bm * pv.bn;
+}
+
+namespace {
+
+// K split of the 128 x 128 two-slot tile on a layer with at most 128 such
+// tiles (fewer than one per CU) and at least 32 stages: the largest ks <= 4
+// whose partial tiles keep the whole workspace within the size of the
+// layer's im2col matrix; 1 when none does.  Measured on 3x3 C = 512 at 7x7
+// (128 images, 100 tiles, 72 stages): unsplit 64 x 128 tiles 331 TFLOP/s,
+// 128 x 128 tiles split 2 / 3 / 4 ways 350 / 376 / 408 (split 3 and 4 need
+// more workspace than im2col); with more tiles or fewer stages the split's
+// second kernel and partial-tile traffic cost more than it gains.
+int split128(const Shape &sh)
+{
+    const int v = pipe_find("c128p128s2");
+    const int64_t tiles = pipe_tiles(sh, v), nst = sh.K_pad / BK;
+    if (sh.Ci % 8 != 0 || sh.Co < 128 || tiles > 128 || nst < 32)
+        return 1;
+    const int64_t base = sh.pad_end + sh.Co_pad * sh.Kw * sh.Tp * 2;  // window tensor, pad, packed filter
+    const int64_t im2col = sh.P * sh.K * 2;
+    for (int ks = 4; ks >= 2; --ks) {
+        const int64_t spl = (nst + ks - 1) / ks;
+        if ((ks - 1) * spl < nst && base + ks * tiles * pipe_tile_elems(v) * 4 <= im2col)
+            return ks;
+    }
+    return 1;
+}
+
+}  // namespace
+
 int pipe_default(const Shape &sh)
 {
     // Defaults, measured per layer on MI355X: shapes that leave LDS for
@@ -665,6 +793,10 @@ int pipe_default(const Shape &sh)
         return pipe_find("c32p128s3");
     if (fp16_single_slot_rows(sh))
         return pipe_find("c128p128s1");
+    // too few 128 x 128 tiles to fill the chip: split K over them where the
+    // workspace allows, else 64 x 128 tiles
+    if (split128(sh) > 1)
+        return pipe_find("c128p128s2");
     if (sh.Co <= 64 || tiles(128, 128) < 256)
         return pipe_find("c64p128s3");
     if (tiles(256, 256) >= 128 && tiles(256, 256) <= 256 && sh.Co >= 256)
@@ -672,8 +804,15 @@ int pipe_default(const Shape &sh)
     return pipe_find("c128p128s2");
 }
 
-hipError_t launch_pack_fp16(const Shape &sh, const Plan16 &p, const uint16_t *filt, void *packed, hipStream_t st)
+int pipe_split_default(const Shape &sh, int v)
 {
+    return v == pipe_find("c128p128s2") ? split128(sh) : 1;
+}
+
+hipError_t launch_pack_fp16(const Shape &sh, const Plan16 &p, const uint16_t *filt, void *packed, hipStream_t st,
+                            void *split)
+{
+    (void)split;
     PackArgs a;
     a.filt = filt;
     a.packed = static_cast<uint16_t *>(packed);
@@ -686,8 +825,12 @@ hipError_t launch_pack_fp16(const Shape &sh, const Plan16 &p, const uint16_t *fi
         // kernel: one tile of K_pad taps
         a.tb = p.fam == Fam16::Regs ? a.tpad : (uint32_t)BK;
     }
-    a.grans = (uint64_t)sh.Co_pad * a.nv * a.tpad / 8;
-    a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad;
+    // the column-staged kernel's slices hold C_o rounded up to its tile's
+    // channel count (a stage's filter rows are then one contiguous run);
+    // the other kernels' tiles use C_o_pad = C_o rounded up to 256
+    const int64_t rows = p.fam == Fam16::Col ? col_packed_rows(sh, p.v) : sh.Co_pad;
+    a.grans = (uint64_t)rows * a.nv * a.tpad / 8;
+    a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)rows;
     a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
     uint64_t blocks = (a.grans + 255) / 256;
     if (blocks > 65536)
@@ -697,7 +840,7 @@ hipError_t launch_pack_fp16(const Shape &sh, const Plan16 &p, const uint16_t *fi
 }
 
 hipError_t launch_conv_fp16(const Shape &sh, const Plan16 &p, const Tuning &t, const void *ws,
-                            const void *packed, uint16_t *out, hipStream_t st, Op16 op)
+                            const void *packed, uint16_t *out, hipStream_t st, Op16 op, void *split)
 {
     if (p.fam == Fam16::Col)
         return launch_conv_fp16_col(sh, p.v, t, ws, packed, out, st, op);
@@ -720,14 +863,38 @@ hipError_t launch_conv_fp16(const Shape &sh, const Plan16 &p, const Tuning &t, c
     // register-staged kernel always walks its taps in linear order.
     a.to = make_taporder(sh.Kw, sh.Kh, sh.Ci, (uint32_t)BK, t.tap_order != Tuning::kColumn || p.fam != Fam16::Pipe);
     void *args[] = {&a};
+    const uint32_t nst = (uint32_t)(sh.K_pad / BK);
+    a.ks = 1; a.spl = nst; a.part = nullptr;
     if (p.fam == Fam16::Pipe) {
         int n;
         const PipeVariant &v = pipe_variants(&n)[p.v];
         const int64_t gx = (sh.P + v.bn - 1) / v.bn, gy = (sh.Co + v.bm - 1) / v.bm;
-        if (gx * gy > 0x7fffffff)
+        if (gx * gy * p.ks > 0x7fffffff)
             return hipErrorInvalidValue;
         a.tg = make_tilegrid(gx, gy, t.tile_linear);
-        return hipLaunchKernel(v.f[op == Op16::BF16], dim3((uint32_t)(gx * gy)), dim3(v.nt), args, 0, st);
+        a.ntiles = (uint32_t)(gx * gy);
+        if (p.ks <= 1)
+            return hipLaunchKernel(v.f[op == Op16::BF16], dim3((uint32_t)(gx * gy)), dim3(v.nt), args, 0, st);
+        if (split == nullptr)
+            return hipErrorInvalidValue;
+        a.ks = (uint32_t)p.ks;
+        a.spl = (nst + a.ks - 1) / a.ks;
+        a.part = static_cast<float *>(split);
+        hipError_t e =
+            hipLaunchKernel(v.f[op == Op16::BF16], dim3((uint32_t)(gx * gy * a.ks)), dim3(v.nt), args, 0, st);
+        if (e != hipSuccess)
+            return e;
+        SumArgs sa;
+        sa.part = a.part;
+        sa.out = out;
+        sa.ks = a.ks; sa.ntiles = a.ntiles; sa.P = a.P; sa.Co = a.Co;
+        sa.WM = v.wm; sa.WN = v.wn; sa.WGN = v.wgn; sa.BMc = v.bm; sa.BNp = v.bn;
+        sa.tile_quads = (uint32_t)(v.bm * v.bn / 4);
+        sa.quads = (uint64_t)a.ntiles * sa.tile_quads;
+        sa.tg = a.tg;
+        void *sargs[] = {&sa};
+        const void *fs = op == Op16::BF16 ? (const void *)&split_sum<BF16Op> : (const void *)&split_sum<F16Op>;
+        return hipLaunchKernel(fs, dim3((uint32_t)((sa.quads + 255) / 256)), dim3(256), sargs, 0, st);
     }
     const void *f;
     int bm, bn;
@@ -751,6 +918,7 @@ hipError_t launch_conv_fp16(const Shape &sh, const Plan16 &p, const Tuning &t, c
     if (gx * gy > 0x7fffffff)
         return hipErrorInvalidValue;
     a.tg = make_tilegrid(gx, gy, t.tile_linear);
+    a.ntiles = (uint32_t)(gx * gy);
     return hipLaunchKernel(f, dim3((uint32_t)(gx * gy)), dim3(256), args, 0, st);
 }
 

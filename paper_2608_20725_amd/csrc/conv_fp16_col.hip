@@ -508,6 +508,12 @@ int col_stage_taps(int plan)
     return col_variants(&n)[plan].bt;
 }
 
+int64_t col_packed_rows(const Shape &sh, int plan)
+{
+    int n;
+    return round_up(sh.Co, col_variants(&n)[plan].bm);
+}
+
 hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const Tuning &t, const void *ws, const void *packed,
                                 uint16_t *out, hipStream_t st, Op16 op)
 {
@@ -518,8 +524,9 @@ hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const Tuning &t, cons
     a.packed = static_cast<const uint16_t *>(packed);
     a.out = out;
     a.win_bytes = (uint64_t)sh.win_bytes;
-    a.pk_bytes = (uint64_t)sh.Co_pad * sh.Kw * sh.Tp * 2;
-    a.Co_pad = (uint32_t)sh.Co_pad;
+    const int64_t rows = col_packed_rows(sh, plan);
+    a.pk_bytes = (uint64_t)rows * sh.Kw * sh.Tp * 2;
+    a.Co_pad = (uint32_t)rows;
     a.P = (uint32_t)sh.P; a.Co = (uint32_t)sh.Co; a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L;
     a.T = (uint32_t)(sh.Kh * sh.Ci); a.Tp = (uint32_t)sh.Tp; a.s = (uint32_t)sh.s;
     a.ms = (uint32_t)(sh.s < sh.Kw ? sh.s : sh.Kw);

@@ -78,6 +78,16 @@ int read_tuning(Tuning *t)
         else if (*e)
             return IM2WIN_EINVAL;
     }
+    t->fp16_split = 0;
+    if (const char *e = getenv("IM2WIN_FP16_SPLIT")) {
+        if (*e) {
+            char *end = nullptr;
+            const long v = strtol(e, &end, 10);
+            if (*end != 0 || v < 1 || v > kMaxSplit)
+                return IM2WIN_EINVAL;
+            t->fp16_split = (int)v;
+        }
+    }
     // contradictory choices
     const int fam16 = (t->fp16_col >= 0) + (t->fp16_seg >= 0) + (t->fp16_tile >= 0 || t->fp16_kernel == Tuning::kPipe) +
                       (t->fp16_kernel == Tuning::kRegs);
@@ -88,7 +98,62 @@ int read_tuning(Tuning *t)
     return IM2WIN_OK;
 }
 
+Tuning default_tuning()
+{
+    Tuning t;
+    t.fp16_kernel = Tuning::kAuto;
+    t.fp16_col = t.fp16_tile = t.fp16_seg = -1;
+    t.fp32_kernel = t.fp32_tile = t.fp32_mfma_tile = -1;
+    t.transform_linear = t.tile_linear = false;
+    t.tap_order = Tuning::kDefault;
+    t.fp16_split = 0;
+    return t;
+}
+
+namespace {
+
+// Every one of the ks K ranges of ceil(nst / ks) stages is non-empty.
+bool split_ok(const Shape &sh, int ks)
+{
+    const int64_t nst = sh.K_pad / 64, spl = (nst + ks - 1) / ks;
+    return ks >= 1 && ks <= kMaxSplit && (ks - 1) * spl < nst;
+}
+
+// The K split of a row-per-pixel plan: forced by the tuning, else the
+// planner's choice for the variant.
+int with_split(const Shape &sh, const Tuning &t, Plan16 *p)
+{
+    p->ks = 1;
+    if (p->fam != Fam16::Pipe) {
+        return t.fp16_split > 1 ? IM2WIN_EINVAL : IM2WIN_OK;
+    }
+    const int ks = t.fp16_split > 0 ? t.fp16_split : pipe_split_default(sh, p->v);
+    if (!split_ok(sh, ks))
+        return IM2WIN_EINVAL;
+    p->ks = ks;
+    return IM2WIN_OK;
+}
+
+int plan_fp16_family(const Shape &sh, const Tuning &t, Plan16 *p);
+
+}  // namespace
+
+int64_t split_bytes(const Shape &sh, const Plan16 &p)
+{
+    if (p.fam != Fam16::Pipe || p.ks <= 1)
+        return 0;
+    return (int64_t)p.ks * pipe_tiles(sh, p.v) * pipe_tile_elems(p.v) * 4;
+}
+
 int plan_fp16(const Shape &sh, const Tuning &t, Plan16 *p)
+{
+    const int rc = plan_fp16_family(sh, t, p);
+    return rc != IM2WIN_OK ? rc : with_split(sh, t, p);
+}
+
+namespace {
+
+int plan_fp16_family(const Shape &sh, const Tuning &t, Plan16 *p)
 {
     const bool aligned = sh.Ci % 8 == 0;  // every window starts on a 16-byte boundary
     // register-staged tile by output channels
@@ -124,6 +189,8 @@ int plan_fp16(const Shape &sh, const Tuning &t, Plan16 *p)
     *p = sg >= 0 ? Plan16{Fam16::Seg, sg} : Plan16{Fam16::Regs, regs_tile};
     return IM2WIN_OK;
 }
+
+}  // namespace
 
 int plan_fp32(const Shape &sh, const Tuning &t, bool mfma, Plan32 *p)
 {
@@ -167,7 +234,12 @@ void plan16_name(const Shape &sh, const Plan16 &p, char *buf, int len)
 {
     switch (p.fam) {
     case Fam16::Col: snprintf(buf, len, "conv_fp16_col %s", col_name(p.v)); break;
-    case Fam16::Pipe: snprintf(buf, len, "conv_fp16_pipe %s", pipe_name(p.v)); break;
+    case Fam16::Pipe:
+        if (p.ks > 1)
+            snprintf(buf, len, "conv_fp16_pipe %s k%d", pipe_name(p.v), p.ks);
+        else
+            snprintf(buf, len, "conv_fp16_pipe %s", pipe_name(p.v));
+        break;
     case Fam16::Seg: snprintf(buf, len, "conv_fp16_seg %s", seg_name(p.v)); break;
     case Fam16::Regs: {
         static const char *tiles[] = {"c32p256", "c64p256", "c128p128"};

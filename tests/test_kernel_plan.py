@@ -13,7 +13,7 @@ from paper_2608_20725_amd import workloads
 EINVAL = -1
 VARS = ("IM2WIN_FP16_KERNEL", "IM2WIN_FP16_COL", "IM2WIN_FP16_TILE", "IM2WIN_FP16_SEG", "IM2WIN_FP32_KERNEL",
         "IM2WIN_FP32_TILE", "IM2WIN_FP32_MFMA_TILE", "IM2WIN_TRANSFORM_ORDER", "IM2WIN_TILE_ORDER",
-        "IM2WIN_TAP_ORDER")
+        "IM2WIN_TAP_ORDER", "IM2WIN_FP16_SPLIT")
 
 
 @pytest.fixture(autouse=True)
@@ -149,3 +149,41 @@ def test_chunk_plan_differs_from_last_chunk_standalone(shape, n_chunk, dt):
     full_chunk = name((n_chunk,) + shape[1:], dt)
     last_alone = name((last,) + shape[1:], dt)
     assert full_chunk != last_alone, (full_chunk, last_alone)
+
+
+@pytest.mark.parametrize("value", ["0", "9", "-1", "2x", "1.5"])
+def test_split_out_of_range_refused(monkeypatch, value):
+    monkeypatch.setenv("IM2WIN_FP16_SPLIT", value)
+    assert status((1, 64, 10, 10, 128, 3, 3, 1), "f16") == EINVAL
+
+
+def test_split_reported_and_refused_where_it_cannot_run(monkeypatch):
+    sh = (2, 64, 24, 24, 128, 3, 3, 1)   # K = 576: 9 stages of 64 taps
+    # the layer's default kernel is column-staged: no K split there
+    assert name(sh, "f16").startswith("conv_fp16_col ")
+    monkeypatch.setenv("IM2WIN_FP16_SPLIT", "3")
+    assert status(sh, "f16") == EINVAL
+    monkeypatch.setenv("IM2WIN_FP16_TILE", "c128p128s2")
+    assert name(sh, "f16") == "conv_fp16_pipe c128p128s2 k3"
+    assert name(sh, "bf16") == "conv_fp16_pipe c128p128s2 k3"
+    monkeypatch.setenv("IM2WIN_FP16_SPLIT", "1")
+    assert name(sh, "f16") == "conv_fp16_pipe c128p128s2"
+    # one 64-tap stage cannot be split in two
+    monkeypatch.setenv("IM2WIN_FP16_SPLIT", "2")
+    assert status((1, 64, 10, 10, 128, 1, 1, 1), "f16") == EINVAL
+    # 9 stages in 8 ranges of 2 leave the last range empty
+    monkeypatch.setenv("IM2WIN_FP16_SPLIT", "8")
+    assert status(sh, "f16") == EINVAL
+    # fp32 ignores the 16-bit split
+    assert name(sh, "f32").startswith("conv_fp32_dma ")
+
+
+@pytest.mark.parametrize("layer", workloads.ALL, ids=lambda l: l.name)
+def test_default_plan_workspace_not_above_im2col_by_the_split(layer):
+    # a K split the planner makes by default keeps the whole 16-bit workspace
+    # within the layer's im2col matrix
+    sh = lay(layer)
+    n = name(sh, "f16")
+    if n.split()[-1].startswith("k") and n.split()[0] == "conv_fp16_pipe":
+        ws = pkg.conv_workspace_bytes(*sh, "f16")
+        assert ws <= pkg.conv_im2col_bytes(sh[0], sh[1], sh[2], sh[3], sh[5], sh[6], sh[7], "f16")
