@@ -231,6 +231,7 @@ int launch_status(hipError_t e);
 // the kernels against each other (the ablation of the paper's techniques);
 // without them every layer runs the kernel its shape selects.
 //   IM2WIN_FP16_KERNEL     pipe (row-per-pixel kernels) | regs (register-staged)
+//                          | stem (short unaligned windows, filter in registers)
 //   IM2WIN_FP16_COL        a column-staged variant name
 //   IM2WIN_FP16_TILE       a row-per-pixel tile name (implies pipe)
 //   IM2WIN_FP16_SEG        a segment-staged variant name
@@ -249,8 +250,8 @@ int launch_status(hipError_t e);
 namespace im2win {
 
 struct Tuning {
-    enum { kAuto = 0, kPipe = 1, kRegs = 2 };
-    int fp16_kernel;                   // kAuto, kPipe, kRegs
+    enum { kAuto = 0, kPipe = 1, kRegs = 2, kStem = 3 };
+    int fp16_kernel;                   // kAuto, kPipe, kRegs, kStem
     int fp16_col, fp16_tile, fp16_seg; // variant index, -1: not forced
     int fp32_kernel;                   // DMA variant index, -1: not forced, -2: register-staged kernel
     int fp32_tile;                     // register-staged tile index, -1: not forced
@@ -282,7 +283,7 @@ int mfma32_find(const char *name);
 // layer of N images also runs any layer that differs only in having fewer
 // images (the fit checks do not grow as N shrinks), which the mini-batch
 // path relies on.
-enum class Fam16 { Col, Pipe, Seg, Regs };
+enum class Fam16 { Col, Pipe, Seg, Regs, Stem };
 struct Plan16 {
     Fam16 fam;
     int v;       // variant index within the family (Regs: 0..2 tile by C_o)
@@ -367,6 +368,13 @@ bool seg_fits(const Shape &sh, int v);
 const char *seg_name(int v);
 hipError_t launch_conv_fp16_seg(const Shape &sh, int v, const void *ws, const void *packed,
                                 uint16_t *out, hipStream_t st, Op16 op);
+// Short-window fp16 kernel (windows not 16-byte aligned, K <= 160, C_o <= 128,
+// C_o % 8 == 0): its variant for the layer (-1: cannot run it), name, launch.
+int stem_plan(const Shape &sh);
+int stem_default(const Shape &sh);
+const char *stem_name(int v);
+hipError_t launch_conv_fp16_stem(const Shape &sh, int v, const void *ws, const void *packed, uint16_t *out,
+                                 hipStream_t st, Op16 op);
 hipError_t launch_conv_fp16_col(const Shape &sh, int v, const Tuning &t, const void *ws, const void *packed,
                                 uint16_t *out, hipStream_t st, Op16 op);
 // Row-per-pixel fp16 tiles: default for the layer, name, and the K split the

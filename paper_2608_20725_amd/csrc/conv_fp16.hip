@@ -846,6 +846,8 @@ hipError_t launch_conv_fp16(const Shape &sh, const Plan16 &p, const Tuning &t, c
         return launch_conv_fp16_col(sh, p.v, t, ws, packed, out, st, op);
     if (p.fam == Fam16::Seg)
         return launch_conv_fp16_seg(sh, p.v, ws, packed, out, st, op);
+    if (p.fam == Fam16::Stem)
+        return launch_conv_fp16_stem(sh, p.v, ws, packed, out, st, op);
     C16Args a;
     a.ws = static_cast<const uint16_t *>(ws);
     a.packed = static_cast<const uint16_t *>(packed);

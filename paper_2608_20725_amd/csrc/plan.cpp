@@ -52,6 +52,8 @@ int read_tuning(Tuning *t)
             t->fp16_kernel = Tuning::kPipe;
         else if (strcmp(e, "regs") == 0)
             t->fp16_kernel = Tuning::kRegs;
+        else if (strcmp(e, "stem") == 0)
+            t->fp16_kernel = Tuning::kStem;
         else if (*e)
             return IM2WIN_EINVAL;
     }
@@ -90,7 +92,7 @@ int read_tuning(Tuning *t)
     }
     // contradictory choices
     const int fam16 = (t->fp16_col >= 0) + (t->fp16_seg >= 0) + (t->fp16_tile >= 0 || t->fp16_kernel == Tuning::kPipe) +
-                      (t->fp16_kernel == Tuning::kRegs);
+                      (t->fp16_kernel == Tuning::kRegs) + (t->fp16_kernel == Tuning::kStem);
     if (fam16 > 1)
         return IM2WIN_EINVAL;
     if (t->fp32_tile >= 0 && t->fp32_kernel >= 0)
@@ -162,6 +164,13 @@ int plan_fp16_family(const Shape &sh, const Tuning &t, Plan16 *p)
         *p = Plan16{Fam16::Regs, regs_tile};
         return IM2WIN_OK;
     }
+    if (t.fp16_kernel == Tuning::kStem) {
+        const int v = stem_plan(sh);
+        if (v < 0)
+            return IM2WIN_EINVAL;
+        *p = Plan16{Fam16::Stem, v};
+        return IM2WIN_OK;
+    }
     if (t.fp16_col >= 0) {
         if (!col_fits(sh, t.fp16_col))
             return IM2WIN_EINVAL;
@@ -183,6 +192,11 @@ int plan_fp16_family(const Shape &sh, const Tuning &t, Plan16 *p)
     if (aligned) {
         const int c = col_default(sh);
         *p = c >= 0 ? Plan16{Fam16::Col, c} : Plan16{Fam16::Pipe, pipe_default(sh)};
+        return IM2WIN_OK;
+    }
+    const int sm = stem_default(sh);
+    if (sm >= 0) {
+        *p = Plan16{Fam16::Stem, sm};
         return IM2WIN_OK;
     }
     const int sg = seg_default(sh);
@@ -241,6 +255,7 @@ void plan16_name(const Shape &sh, const Plan16 &p, char *buf, int len)
             snprintf(buf, len, "conv_fp16_pipe %s", pipe_name(p.v));
         break;
     case Fam16::Seg: snprintf(buf, len, "conv_fp16_seg %s", seg_name(p.v)); break;
+    case Fam16::Stem: snprintf(buf, len, "conv_fp16_stem %s", stem_name(p.v)); break;
     case Fam16::Regs: {
         static const char *tiles[] = {"c32p256", "c64p256", "c128p128"};
         // unaligned 16-byte loads for windows of 128 taps or more, element

@@ -144,6 +144,8 @@ def assert_kernel(shape, dtype, var, value, dilation=1):
         assert got.split()[0] == want, got
     elif value == "pipe":
         assert got.split()[0] == "conv_fp16_pipe", got
+    elif value == "stem":
+        assert got.split()[0] == "conv_fp16_stem", got
     else:
         assert got.split()[1] == value, got
     return got

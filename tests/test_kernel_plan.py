@@ -49,7 +49,8 @@ def test_every_layer_has_a_plan(layer):
     f16 = name(sh, "f16")
     assert f16 == name(sh, "bf16")  # same kernels for both 16-bit operand types
     fam = f16.split()[0]
-    assert fam in (("conv_fp16_col", "conv_fp16_pipe") if aligned16 else ("conv_fp16_seg", "conv_fp16_kernel"))
+    assert fam in (("conv_fp16_col", "conv_fp16_pipe") if aligned16 else
+                   ("conv_fp16_stem", "conv_fp16_seg", "conv_fp16_kernel"))
     f32 = name(sh, "f32")
     assert f32.split()[0] in ("conv_fp32_dma", "conv_fp32_kernel")
     if layer.C_i % 4 == 0:
@@ -187,3 +188,22 @@ def test_default_plan_workspace_not_above_im2col_by_the_split(layer):
     if n.split()[-1].startswith("k") and n.split()[0] == "conv_fp16_pipe":
         ws = pkg.conv_workspace_bytes(*sh, "f16")
         assert ws <= pkg.conv_im2col_bytes(sh[0], sh[1], sh[2], sh[3], sh[5], sh[6], sh[7], "f16")
+
+
+@pytest.mark.parametrize("shape,want", [
+    ((2, 3, 224, 224, 64, 3, 3, 1), "conv_fp16_stem m2k2"),     # 27 taps: the default
+    ((2, 3, 30, 30, 128, 4, 4, 1), "conv_fp16_stem m4k4"),      # 48 taps, 128 channels
+    ((2, 3, 227, 227, 64, 7, 7, 2), "conv_fp16_seg "),          # 147 taps: segment-staged
+    ((2, 3, 30, 30, 20, 3, 3, 1), "conv_fp16_seg "),            # C_o not a multiple of 8
+    ((2, 3, 30, 30, 136, 3, 3, 1), "conv_fp16_seg "),           # C_o > 128
+])
+def test_stem_default(shape, want):
+    assert name(shape, "f16").startswith(want)
+
+
+def test_stem_forced(monkeypatch):
+    monkeypatch.setenv("IM2WIN_FP16_KERNEL", "stem")
+    assert name((2, 3, 227, 227, 64, 7, 7, 2), "f16") == "conv_fp16_stem m2k10"   # up to 160 taps
+    assert status((2, 3, 227, 227, 96, 11, 11, 4), "f16") == EINVAL               # 363 taps
+    assert status((2, 64, 20, 20, 64, 3, 3, 1), "f16") == EINVAL                  # aligned windows
+    assert status((2, 3, 30, 30, 20, 3, 3, 1), "f16") == EINVAL                   # C_o % 8
