@@ -235,7 +235,8 @@ int launch_status(hipError_t e);
 //   IM2WIN_FP16_COL        a column-staged variant name
 //   IM2WIN_FP16_TILE       a row-per-pixel tile name (implies pipe)
 //   IM2WIN_FP16_SEG        a segment-staged variant name
-//   IM2WIN_FP32_KERNEL     a DMA-staged variant name | regs
+//   IM2WIN_FP32_KERNEL     a DMA-staged variant name | regs | stem (short
+//                          unaligned windows, filter from the scalar cache)
 //   IM2WIN_FP32_TILE       a register-staged tile name (implies regs)
 //   IM2WIN_FP32_MFMA_TILE  a matrix-core fp32 tile name
 //   IM2WIN_TRANSFORM_ORDER linear | xcd
@@ -253,7 +254,8 @@ struct Tuning {
     enum { kAuto = 0, kPipe = 1, kRegs = 2, kStem = 3 };
     int fp16_kernel;                   // kAuto, kPipe, kRegs, kStem
     int fp16_col, fp16_tile, fp16_seg; // variant index, -1: not forced
-    int fp32_kernel;                   // DMA variant index, -1: not forced, -2: register-staged kernel
+    int fp32_kernel;                   // DMA variant index, -1: not forced, -2: register-staged kernel,
+                                       // -3: short-window kernel
     int fp32_tile;                     // register-staged tile index, -1: not forced
     int fp32_mfma_tile;                // -1: not forced
     bool transform_linear, tile_linear;
@@ -289,7 +291,7 @@ struct Plan16 {
     int v;       // variant index within the family (Regs: 0..2 tile by C_o)
     int ks = 1;  // row-per-pixel kernel: K split over ks workgroups per tile (1: none)
 };
-enum class Fam32 { Dma, Regs, Mfma };
+enum class Fam32 { Dma, Regs, Mfma, Stem };
 struct Plan32 {
     Fam32 fam;
     int v;  // variant or tile index within the family
@@ -336,6 +338,13 @@ bool dma32_fits(const Shape &sh, int v);
 const char *dma32_name(int v);
 hipError_t launch_conv_fp32_dma(const Shape &sh, int v, const Tuning &t, const void *ws, const void *packed,
                                 float *out, hipStream_t st);
+// Short-window fp32 kernel (windows not 16-byte aligned, K <= 32, C_o % 4 == 0):
+// its variant for the layer (-1: cannot run it), name, launch.
+int stem32_plan(const Shape &sh);
+int stem32_default(const Shape &sh);
+const char *stem32_name(int v);
+hipError_t launch_conv_fp32_stem(const Shape &sh, int v, const void *ws, const void *packed, float *out,
+                                 hipStream_t st);
 // Register-staged fp32 kernel: whether a tile can run the layer, its name.
 bool regs32_fits(const Shape &sh, int v);
 const char *regs32_name(int v);

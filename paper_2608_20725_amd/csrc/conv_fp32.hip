@@ -524,6 +524,8 @@ hipError_t launch_conv_fp32(const Shape &sh, const Plan32 &p, const Tuning &t, c
 {
     if (p.fam == Fam32::Dma)
         return launch_conv_fp32_dma(sh, p.v, t, ws, packed, out, st);
+    if (p.fam == Fam32::Stem)
+        return launch_conv_fp32_stem(sh, p.v, ws, packed, out, st);
     C32Args a;
     a.ws = static_cast<const float *>(ws);
     a.packed = static_cast<const float *>(packed);

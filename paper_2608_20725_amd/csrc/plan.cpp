@@ -66,6 +66,8 @@ int read_tuning(Tuning *t)
     const char *e = getenv("IM2WIN_FP32_KERNEL");
     if (e && strcmp(e, "regs") == 0)
         t->fp32_kernel = -2;
+    else if (e && strcmp(e, "stem") == 0)
+        t->fp32_kernel = -3;
     else if ((rc = read_name("IM2WIN_FP32_KERNEL", dma32_find, &t->fp32_kernel)) != IM2WIN_OK)
         return rc;
     if ((rc = read_order("IM2WIN_TRANSFORM_ORDER", "xcd", &t->transform_linear)) != IM2WIN_OK ||
@@ -95,7 +97,7 @@ int read_tuning(Tuning *t)
                       (t->fp16_kernel == Tuning::kRegs) + (t->fp16_kernel == Tuning::kStem);
     if (fam16 > 1)
         return IM2WIN_EINVAL;
-    if (t->fp32_tile >= 0 && t->fp32_kernel >= 0)
+    if (t->fp32_tile >= 0 && (t->fp32_kernel >= 0 || t->fp32_kernel == -3))
         return IM2WIN_EINVAL;
     return IM2WIN_OK;
 }
@@ -224,6 +226,13 @@ int plan_fp32(const Shape &sh, const Tuning &t, bool mfma, Plan32 *p)
         *p = Plan32{Fam32::Dma, t.fp32_kernel};
         return IM2WIN_OK;
     }
+    if (t.fp32_kernel == -3) {
+        const int v = stem32_plan(sh);
+        if (v < 0)
+            return IM2WIN_EINVAL;
+        *p = Plan32{Fam32::Stem, v};
+        return IM2WIN_OK;
+    }
     if (t.fp32_kernel == -2 || t.fp32_tile >= 0) {
         const int v = t.fp32_tile >= 0 ? t.fp32_tile : 0;
         if (!regs32_fits(sh, v)) {
@@ -233,6 +242,11 @@ int plan_fp32(const Shape &sh, const Tuning &t, bool mfma, Plan32 *p)
             return IM2WIN_OK;
         }
         *p = Plan32{Fam32::Regs, v};
+        return IM2WIN_OK;
+    }
+    const int sm = stem32_default(sh);
+    if (sm >= 0) {
+        *p = Plan32{Fam32::Stem, sm};
         return IM2WIN_OK;
     }
     const int d = dma32_default(sh);
@@ -272,6 +286,7 @@ void plan32_name(const Shape &sh, const Plan32 &p, char *buf, int len)
     switch (p.fam) {
     case Fam32::Dma: snprintf(buf, len, "conv_fp32_dma %s", dma32_name(p.v)); break;
     case Fam32::Regs: snprintf(buf, len, "conv_fp32_kernel %s", regs32_name(p.v)); break;
+    case Fam32::Stem: snprintf(buf, len, "conv_fp32_stem %s", stem32_name(p.v)); break;
     case Fam32::Mfma: snprintf(buf, len, "conv_fp32_mfma %s", mfma32_name(p.v)); break;
     }
 }

@@ -145,7 +145,8 @@ def assert_kernel(shape, dtype, var, value, dilation=1):
     elif value == "pipe":
         assert got.split()[0] == "conv_fp16_pipe", got
     elif value == "stem":
-        assert got.split()[0] == "conv_fp16_stem", got
+        want = "conv_fp32_stem" if var.startswith("IM2WIN_FP32") else "conv_fp16_stem"
+        assert got.split()[0] == want, got
     else:
         assert got.split()[1] == value, got
     return got

@@ -1,5 +1,7 @@
-"""The short-window fp16/bf16 kernel (windows not 16-byte aligned, at most
-160 taps; the 3-channel stems): every output against the fp64 oracle, the
+"""The short-window kernels for windows that are not 16-byte aligned (the
+3-channel stems): fp16/bf16 on the matrix cores (at most 160 taps) and fp32
+on the vector ALUs (at most 32 taps).  fp16: every output against the fp64
+oracle, the
 same bits as the segment-staged kernel where both run (both add the 16-tap
 k-steps of each window in order on the same matrix instruction), ragged last
 blocks and tiles over many images, and non-finite inputs kept in their own
@@ -86,3 +88,44 @@ def test_stem_integer_inputs_exact(monkeypatch):
     run = Run(x, w, s, torch.float16)
     ref = oracle.conv(x.double().numpy(), w.double().numpy(), s)
     assert np.array_equal(run.out.float().cpu().numpy(), torch.from_numpy(ref).half().float().numpy())
+
+
+# fp32: up to 32 taps
+SHAPES32 = [s for s in SHAPES if s[5] * s[6] * s[1] <= 32 and s[4] % 4 == 0] + [
+    (2, 5, 19, 23, 36, 2, 3, 1),     # 30 taps, C_o = 36: a ragged 32-channel pass
+    (3, 3, 21, 50, 100, 3, 3, 2),    # C_o = 100: four passes, the last with one chunk
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES32, ids=_id)
+def test_stem32_against_oracle_and_dma_kernel(shape, monkeypatch):
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    say("stem32", shape)
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=37)
+    monkeypatch.setenv("IM2WIN_FP32_KERNEL", "stem")
+    assert_kernel(shape, "f32", "IM2WIN_FP32_KERNEL", "stem")
+    run = Run(x, w, s, torch.float32)
+    check_full(run, x, w)
+    run.check_out_guards()
+    run.check_workspace_guard()
+    # the DMA-staged kernel adds the same taps in the same order
+    monkeypatch.setenv("IM2WIN_FP32_KERNEL", "p6c8l8s2k16g4")
+    other = Run(x, w, s, torch.float32)
+    assert torch.equal(run.out.view(torch.int32), other.out.view(torch.int32))
+
+
+def test_stem32_nonfinite_and_integer(monkeypatch):
+    monkeypatch.setenv("IM2WIN_FP32_KERNEL", "stem")
+    N, Ci, H, W, Co, Kh, Kw, s = (2, 3, 14, 40, 64, 3, 3, 1)
+    g = torch.Generator().manual_seed(8)
+    x = torch.randint(-4, 5, (N, H, W, Ci), generator=g).float()
+    w = torch.randint(-4, 5, (Kh, Kw, Ci, Co), generator=g).float()
+    run = Run(x, w, s, torch.float32)
+    ref = oracle.conv(x.double().numpy(), w.double().numpy(), s)
+    assert np.array_equal(run.out.cpu().numpy(), ref.astype(np.float32))
+    x[1, 5, 7, 2] = float("inf")
+    x[0, 0, 39, 0] = float("nan")
+    run = Run(x, w, s, torch.float32)
+    with np.errstate(invalid="ignore", over="ignore"):
+        ref = oracle.conv(x.double().numpy(), w.double().numpy(), s)
+    assert np.array_equal(np.isfinite(run.out.cpu().numpy()), np.isfinite(ref))

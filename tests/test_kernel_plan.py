@@ -52,7 +52,7 @@ def test_every_layer_has_a_plan(layer):
     assert fam in (("conv_fp16_col", "conv_fp16_pipe") if aligned16 else
                    ("conv_fp16_stem", "conv_fp16_seg", "conv_fp16_kernel"))
     f32 = name(sh, "f32")
-    assert f32.split()[0] in ("conv_fp32_dma", "conv_fp32_kernel")
+    assert f32.split()[0] in ("conv_fp32_dma", "conv_fp32_kernel", "conv_fp32_stem")
     if layer.C_i % 4 == 0:
         assert name(sh, "f32", fp32_matrix_cores=True).startswith("conv_fp32_mfma ")
     else:   # the matrix-core fp32 kernel needs 16-byte window chunks
@@ -105,7 +105,7 @@ def test_forced_mfma_tile_on_unaligned_layer_refused(monkeypatch):
     monkeypatch.setenv("IM2WIN_FP32_MFMA_TILE", "c128p128s2")
     assert status((1, 3, 10, 10, 64, 3, 3, 1), "f32", fp32_matrix_cores=True) == EINVAL
     # the vector-ALU entry point ignores it
-    assert name((1, 3, 10, 10, 64, 3, 3, 1), "f32").startswith("conv_fp32_dma ")
+    assert name((1, 3, 10, 10, 64, 3, 3, 1), "f32").startswith("conv_fp32_stem ")
 
 
 @pytest.mark.parametrize("var,value,expect", [
@@ -207,3 +207,23 @@ def test_stem_forced(monkeypatch):
     assert status((2, 3, 227, 227, 96, 11, 11, 4), "f16") == EINVAL               # 363 taps
     assert status((2, 64, 20, 20, 64, 3, 3, 1), "f16") == EINVAL                  # aligned windows
     assert status((2, 3, 30, 30, 20, 3, 3, 1), "f16") == EINVAL                   # C_o % 8
+
+
+@pytest.mark.parametrize("shape,want", [
+    ((2, 3, 224, 224, 64, 3, 3, 1), "conv_fp32_stem k27"),
+    ((2, 3, 30, 30, 16, 2, 2, 1), "conv_fp32_stem k16"),
+    ((2, 5, 30, 30, 64, 2, 3, 1), "conv_fp32_dma "),        # 30 taps: the DMA-staged kernel
+    ((2, 3, 30, 30, 18, 3, 3, 1), "conv_fp32_dma "),        # C_o not a multiple of 4
+    ((2, 8, 30, 30, 64, 3, 3, 1), "conv_fp32_dma "),        # 16-byte-aligned windows
+])
+def test_stem32_default(shape, want):
+    assert name(shape, "f32").startswith(want)
+
+
+def test_stem32_forced(monkeypatch):
+    monkeypatch.setenv("IM2WIN_FP32_KERNEL", "stem")
+    assert name((2, 5, 30, 30, 64, 2, 3, 1), "f32") == "conv_fp32_stem k32"
+    assert status((2, 3, 30, 30, 64, 5, 5, 1), "f32") == EINVAL    # 75 taps
+    assert status((2, 8, 30, 30, 64, 3, 3, 1), "f32") == EINVAL    # aligned windows
+    monkeypatch.setenv("IM2WIN_FP32_TILE", "m4n16f")
+    assert status((2, 3, 30, 30, 64, 3, 3, 1), "f32") == EINVAL    # two fp32 kernels forced
