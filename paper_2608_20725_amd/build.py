@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libim2win.so")
-SOURCES = ["api.cpp", "plan.cpp", "chunked.cpp", "transform.hip", "conv_fp32.hip", "conv_fp16.hip", "conv_fp16_col.hip", "conv_fp32_dma.hip", "conv_fp16_seg.hip", "conv_fp32_mfma.hip", "conv_fp16_stem.hip", "conv_fp32_stem.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "chunked.cpp", "transform.hip", "conv_fp32.hip", "conv_fp16.hip", "conv_fp16_col.hip", "conv_fp32_dma.hip", "conv_fp16_seg.hip", "conv_fp32_mfma.hip", "conv_fp16_stem.hip", "conv_fp32_stem.hip", "conv_fp32_cols.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

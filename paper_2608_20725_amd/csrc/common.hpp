@@ -238,6 +238,7 @@ int launch_status(hipError_t e);
 //   IM2WIN_FP32_KERNEL     a DMA-staged variant name | regs | stem (short
 //                          unaligned windows, filter from the scalar cache)
 //   IM2WIN_FP32_TILE       a register-staged tile name (implies regs)
+//   IM2WIN_FP32_COLS       a column-staged variant name
 //   IM2WIN_FP32_MFMA_TILE  a matrix-core fp32 tile name
 //   IM2WIN_TRANSFORM_ORDER linear | xcd
 //   IM2WIN_TILE_ORDER      linear | xcd
@@ -257,6 +258,7 @@ struct Tuning {
     int fp32_kernel;                   // DMA variant index, -1: not forced, -2: register-staged kernel,
                                        // -3: short-window kernel
     int fp32_tile;                     // register-staged tile index, -1: not forced
+    int fp32_cols;                     // column-staged variant index, -1: not forced
     int fp32_mfma_tile;                // -1: not forced
     bool transform_linear, tile_linear;
     enum { kDefault = 0, kLinear = 1, kColumn = 2 };
@@ -291,7 +293,7 @@ struct Plan16 {
     int v;       // variant index within the family (Regs: 0..2 tile by C_o)
     int ks = 1;  // row-per-pixel kernel: K split over ks workgroups per tile (1: none)
 };
-enum class Fam32 { Dma, Regs, Mfma, Stem };
+enum class Fam32 { Dma, Regs, Mfma, Stem, Cols };
 struct Plan32 {
     Fam32 fam;
     int v;  // variant or tile index within the family
@@ -338,6 +340,15 @@ bool dma32_fits(const Shape &sh, int v);
 const char *dma32_name(int v);
 hipError_t launch_conv_fp32_dma(const Shape &sh, int v, const Tuning &t, const void *ws, const void *packed,
                                 float *out, hipStream_t st);
+// Column-staged fp32 kernel (each distinct input column of a tile loaded
+// once per tap block): variant index of a name, name, fit, default (-1: the
+// DMA-staged kernel runs), launch.
+int cols32_find(const char *name);
+const char *cols32_name(int v);
+bool cols32_fits(const Shape &sh, int v);
+int cols32_default(const Shape &sh);
+hipError_t launch_conv_fp32_cols(const Shape &sh, int v, const Tuning &t, const void *ws, const void *packed,
+                                 float *out, hipStream_t st);
 // Short-window fp32 kernel (windows not 16-byte aligned, K <= 32, C_o % 4 == 0):
 // its variant for the layer (-1: cannot run it), name, launch.
 int stem32_plan(const Shape &sh);

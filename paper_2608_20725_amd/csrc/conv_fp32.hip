@@ -511,7 +511,8 @@ hipError_t launch_pack_fp32(const Shape &sh, const Plan32 &p, const float *filt,
     a.quads = (uint64_t)sh.K_pad32 * sh.Co_pad32 / 4;
     a.K = (uint32_t)sh.K; a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
     a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
-    a.pair_swap = p.fam == Fam32::Dma;  // the DMA-staged kernel reads channel pairs swapped
+    // the DMA- and column-staged kernels read channel pairs swapped
+    a.pair_swap = p.fam == Fam32::Dma || p.fam == Fam32::Cols;
     uint64_t blocks = (a.quads + 255) / 256;
     if (blocks > 65536)
         blocks = 65536;
@@ -526,6 +527,8 @@ hipError_t launch_conv_fp32(const Shape &sh, const Plan32 &p, const Tuning &t, c
         return launch_conv_fp32_dma(sh, p.v, t, ws, packed, out, st);
     if (p.fam == Fam32::Stem)
         return launch_conv_fp32_stem(sh, p.v, ws, packed, out, st);
+    if (p.fam == Fam32::Cols)
+        return launch_conv_fp32_cols(sh, p.v, t, ws, packed, out, st);
     C32Args a;
     a.ws = static_cast<const float *>(ws);
     a.packed = static_cast<const float *>(packed);

@@ -61,7 +61,8 @@ int read_tuning(Tuning *t)
         (rc = read_name("IM2WIN_FP16_TILE", pipe_find, &t->fp16_tile)) != IM2WIN_OK ||
         (rc = read_name("IM2WIN_FP16_SEG", seg_find, &t->fp16_seg)) != IM2WIN_OK ||
         (rc = read_name("IM2WIN_FP32_TILE", regs32_find, &t->fp32_tile)) != IM2WIN_OK ||
-        (rc = read_name("IM2WIN_FP32_MFMA_TILE", mfma32_find, &t->fp32_mfma_tile)) != IM2WIN_OK)
+        (rc = read_name("IM2WIN_FP32_MFMA_TILE", mfma32_find, &t->fp32_mfma_tile)) != IM2WIN_OK ||
+        (rc = read_name("IM2WIN_FP32_COLS", cols32_find, &t->fp32_cols)) != IM2WIN_OK)
         return rc;
     const char *e = getenv("IM2WIN_FP32_KERNEL");
     if (e && strcmp(e, "regs") == 0)
@@ -97,7 +98,8 @@ int read_tuning(Tuning *t)
                       (t->fp16_kernel == Tuning::kRegs) + (t->fp16_kernel == Tuning::kStem);
     if (fam16 > 1)
         return IM2WIN_EINVAL;
-    if (t->fp32_tile >= 0 && (t->fp32_kernel >= 0 || t->fp32_kernel == -3))
+    if ((t->fp32_tile >= 0) + (t->fp32_kernel >= 0 || t->fp32_kernel == -3 || t->fp32_kernel == -2) +
+            (t->fp32_cols >= 0) > 1)
         return IM2WIN_EINVAL;
     return IM2WIN_OK;
 }
@@ -107,7 +109,7 @@ Tuning default_tuning()
     Tuning t;
     t.fp16_kernel = Tuning::kAuto;
     t.fp16_col = t.fp16_tile = t.fp16_seg = -1;
-    t.fp32_kernel = t.fp32_tile = t.fp32_mfma_tile = -1;
+    t.fp32_kernel = t.fp32_tile = t.fp32_mfma_tile = t.fp32_cols = -1;
     t.transform_linear = t.tile_linear = false;
     t.tap_order = Tuning::kDefault;
     t.fp16_split = 0;
@@ -226,6 +228,12 @@ int plan_fp32(const Shape &sh, const Tuning &t, bool mfma, Plan32 *p)
         *p = Plan32{Fam32::Dma, t.fp32_kernel};
         return IM2WIN_OK;
     }
+    if (t.fp32_cols >= 0) {
+        if (!cols32_fits(sh, t.fp32_cols))
+            return IM2WIN_EINVAL;
+        *p = Plan32{Fam32::Cols, t.fp32_cols};
+        return IM2WIN_OK;
+    }
     if (t.fp32_kernel == -3) {
         const int v = stem32_plan(sh);
         if (v < 0)
@@ -247,6 +255,11 @@ int plan_fp32(const Shape &sh, const Tuning &t, bool mfma, Plan32 *p)
     const int sm = stem32_default(sh);
     if (sm >= 0) {
         *p = Plan32{Fam32::Stem, sm};
+        return IM2WIN_OK;
+    }
+    const int cl = cols32_default(sh);
+    if (cl >= 0) {
+        *p = Plan32{Fam32::Cols, cl};
         return IM2WIN_OK;
     }
     const int d = dma32_default(sh);
@@ -287,6 +300,7 @@ void plan32_name(const Shape &sh, const Plan32 &p, char *buf, int len)
     case Fam32::Dma: snprintf(buf, len, "conv_fp32_dma %s", dma32_name(p.v)); break;
     case Fam32::Regs: snprintf(buf, len, "conv_fp32_kernel %s", regs32_name(p.v)); break;
     case Fam32::Stem: snprintf(buf, len, "conv_fp32_stem %s", stem32_name(p.v)); break;
+    case Fam32::Cols: snprintf(buf, len, "conv_fp32_cols %s", cols32_name(p.v)); break;
     case Fam32::Mfma: snprintf(buf, len, "conv_fp32_mfma %s", mfma32_name(p.v)); break;
     }
 }

@@ -405,3 +405,36 @@ def test_nonfinite_inputs_stay_in_their_windows(case):
     r = rel_err(y[fin], ref[fin], absref[fin])
     assert r <= TOL[dtype], "max |err|/sum|x||w| = %.3g" % r
     run.check_out_guards()
+
+
+# The column-staged fp32 kernel (IM2WIN_FP32_COLS; each distinct input column
+# of a tile loaded once per tap block): every output against the oracle on
+# shapes with several strip runs per tile, ragged pixel and channel tiles, a
+# tap block cut by T = K_h*C_i, and stride 2; its serialized ring gives the
+# same bits.
+COLS32_CASES = [
+    ("k3p256t16", (2, 8, 19, 23, 72, 3, 3, 1)),     # T = 24: the second 16-tap block half used
+    ("k3p128t16", (3, 4, 9, 40, 130, 3, 3, 1)),     # three channel tiles, the last of 2
+    ("k3p256t8", (2, 12, 30, 17, 64, 3, 3, 1)),     # 15 output columns per strip: many runs per tile
+    ("k5p256t8", (2, 16, 14, 20, 40, 5, 5, 1)),
+    ("k7p256t8", (2, 8, 23, 121, 40, 7, 7, 2)),
+    ("k7p128t8", (1, 4, 20, 60, 64, 7, 7, 1)),
+]
+
+
+@pytest.mark.parametrize("case", COLS32_CASES, ids=lambda c: c[0] + "-" + _id(c[1]))
+def test_fp32_column_kernel(case, monkeypatch):
+    name, shape = case
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    say("fp32 column-staged", name, shape)
+    monkeypatch.setenv("IM2WIN_FP32_COLS", name)
+    assert_kernel(shape, "f32", "IM2WIN_FP32_COLS", name)
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=41)
+    run = Run(x, w, s, torch.float32)
+    check_full(run, x, w)
+    run.check_out_guards()
+    run.check_workspace_guard()
+    if name == "k3p256t16":
+        monkeypatch.setenv("IM2WIN_FP32_COLS", name + "-serial")
+        twin = Run(x, w, s, torch.float32)
+        assert torch.equal(run.out.view(torch.int32), twin.out.view(torch.int32))

@@ -13,7 +13,7 @@ from paper_2608_20725_amd import workloads
 EINVAL = -1
 VARS = ("IM2WIN_FP16_KERNEL", "IM2WIN_FP16_COL", "IM2WIN_FP16_TILE", "IM2WIN_FP16_SEG", "IM2WIN_FP32_KERNEL",
         "IM2WIN_FP32_TILE", "IM2WIN_FP32_MFMA_TILE", "IM2WIN_TRANSFORM_ORDER", "IM2WIN_TILE_ORDER",
-        "IM2WIN_TAP_ORDER", "IM2WIN_FP16_SPLIT")
+        "IM2WIN_TAP_ORDER", "IM2WIN_FP16_SPLIT", "IM2WIN_FP32_COLS")
 
 
 @pytest.fixture(autouse=True)
@@ -227,3 +227,13 @@ def test_stem32_forced(monkeypatch):
     assert status((2, 8, 30, 30, 64, 3, 3, 1), "f32") == EINVAL    # aligned windows
     monkeypatch.setenv("IM2WIN_FP32_TILE", "m4n16f")
     assert status((2, 3, 30, 30, 64, 3, 3, 1), "f32") == EINVAL    # two fp32 kernels forced
+
+
+def test_fp32_column_kernel_forced(monkeypatch):
+    monkeypatch.setenv("IM2WIN_FP32_COLS", "k3p256t16")
+    assert name((2, 64, 24, 24, 64, 3, 3, 1), "f32") == "conv_fp32_cols k3p256t16"
+    assert status((2, 64, 24, 24, 64, 5, 5, 1), "f32") == EINVAL    # a 3-wide variant on a 5x5 layer
+    assert status((2, 3, 24, 24, 64, 3, 3, 1), "f32") == EINVAL     # windows not 16-byte aligned
+    assert status((2, 512, 7, 7, 512, 3, 3, 1), "f32") == EINVAL    # 52 strip runs: rows past the budget
+    monkeypatch.setenv("IM2WIN_FP32_KERNEL", "p8c8l8s2k16")
+    assert status((2, 64, 24, 24, 64, 3, 3, 1), "f32") == EINVAL    # two fp32 kernels forced
