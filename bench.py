@@ -62,12 +62,13 @@ METRIC = "conv TFLOPS (fp32 VALU, fp16 MFMA) + peak workspace bytes vs im2col"
 # kernel sources they were taken on (SHA-256 over KERNEL_SOURCES); after any
 # change to those sources the figure is reported as null until measured again.
 KERNEL_SOURCES = ("common.hpp", "epilogue16.hpp", "mfma16.hpp", "conv_fp32_dma.hip", "conv_fp32.hip",
-                  "conv_fp16.hip", "conv_fp16_col.hip", "conv_fp16_seg.hip")
+                  "conv_fp32_stem.hip", "conv_fp16.hip", "conv_fp16_col.hip", "conv_fp16_seg.hip",
+                  "conv_fp16_stem.hip")
 CONV_TRAFFIC = {
-    "source_sha256": None,
+    "source_sha256": "fc587fbb5e1eed51dd1164d9eb7eb2a8cd639de4c34db42ac586e34b64371740",
     "workload": "sweep",
-    "f32": None,    # bytes per step, fetched + written
-    "f16": None,
+    "f32": 31966371760,    # bytes per step, fetched + written
+    "f16": 6463079506,
 }
 
 
@@ -513,7 +514,7 @@ def measure_minibatch(l, pkg, torch, workloads, steps, warmup, n_chunk=32):
 
 def roofline_blocks(agg, workload):
     f32, f16 = agg["f32"], agg["f16"]
-    r32 = {"kernel": "fp32 windowed conv on the vector ALUs (conv_fp32_dma variants), all layers of the step",
+    r32 = {"kernel": "fp32 windowed conv on the vector ALUs (conv_fp32_dma, conv_fp32_stem), all layers of the step",
            "bound": "alu", "achieved": f32["TFLOP/s"], "peak": PEAK_FP32_VECTOR_TF, "unit": "TFLOP/s",
            "frac": round(f32["TFLOP/s"] / PEAK_FP32_VECTOR_TF, 4), "traffic": conv_traffic(workload, "f32"),
            "per": "step (one conv call per layer; achieved = algorithmic FLOPs / summed average durations)",
