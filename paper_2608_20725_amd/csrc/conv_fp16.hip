@@ -351,6 +351,8 @@ struct PipeCfg {
     static constexpr int BLOCKS = ROWS / 8;   // 8-row (1 KiB) blocks per stage
     static_assert(BLOCKS % NW == 0, "blocks split evenly over the waves");
     static constexpr int I = BLOCKS / NW;     // load instructions per wave per stage
+    static_assert((BMc / 8) % NW == 0, "filter blocks split evenly over the waves");
+    static constexpr int IF = BMc / 8 / NW;   // of which filter blocks
     static_assert(NSTAGE == 1 || (NSTAGE - 2) * I <= 63, "vmcnt range");
     static constexpr int LDS = NSTAGE * STAGE;
 };
@@ -390,19 +392,27 @@ struct Pipe {
         // first tap of the stage (column order only when every stage is
         // whole: K_h*C_i a multiple of 64)
         const uint32_t k0 = to.map((s + sb) * BK);
-        const bool tail = k0 + BK > K;
         const bool past = s >= nst;
+        // a window chunk whose first tap (within the stage) is at or past
+        // `lim` reads nothing: every chunk of a stage past the end, the
+        // chunks past K in the last stage
+        const uint32_t lim = past ? 0u : k0 + BK <= K ? 0xffffffffu : k0 < K ? K - k0 : 0u;
+        // filter rows: taps k0 .. k0+63 are tile k0/64 of the packed filter
+        // (apitch bytes each); window rows: taps k0 .. k0+63
+        const uint32_t fadd = (k0 / BK) * apitch, wadd = 2u * k0;
 #pragma unroll
         for (int j = 0; j < C::I; ++j) {
+            // block wave + NW*j: the first IF loads of every wave fill
+            // filter blocks, so which buffer a load reads is known at compile
+            // time and the offsets are plain selects
             const uint32_t b = wave + C::NW * j;
-            const bool filt = b < (uint32_t)C::BMc / 8;
-            // filter rows: taps k0 .. k0+63 are tile k0/64 of the packed
-            // filter (apitch bytes each); window rows: taps k0 .. k0+63
-            uint32_t off = voff[j] + (filt ? (k0 / BK) * apitch : 2u * k0);
-            if (past || (!filt && tail && k0 + vchunk[j] >= K))
-                off = kOOB;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(filt ? rf : rw, (lds_ptr)(stage + 1024 * b), 16, off,
-                                                     0, 0, 0);
+            if (j < C::IF) {
+                const uint32_t off = past ? kOOB : voff[j] + fadd;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rf, (lds_ptr)(stage + 1024 * b), 16, off, 0, 0, 0);
+            } else {
+                const uint32_t off = vchunk[j] >= lim ? kOOB : voff[j] + wadd;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(stage + 1024 * b), 16, off, 0, 0, 0);
+            }
         }
     }
 

@@ -77,6 +77,7 @@ struct ColCfg {
     static constexpr int ROWS = AROWS + NRMAX;
     static constexpr int NBLK = (ROWS + RPI - 1) / RPI;  // 1 KiB blocks per stage
     static constexpr int IB = (NBLK + NW - 1) / NW;      // loads per wave per stage
+    static constexpr int IA = (AROWS / RPI) % NW == 0 ? AROWS / RPI / NW : -1;  // A loads per wave
     // Every wave issues IB loads per stage (those past the stage's rows read
     // nothing and fill spare LDS with zeros), so outstanding-load counts are
     // the same for all stages and the ring waits are exact.
@@ -125,12 +126,17 @@ struct ColTile {
     __device__ inline void issue(uint32_t st, char *slot)
     {
         const uint32_t t0 = st * C::BT;
-        const bool past = st >= nst;
+        // a chunk whose first t is at or past `lim` reads nothing (A rows
+        // have bcm = 0: only stages past the end or past T)
+        const uint32_t lim = st >= nst ? 0u : t0 < T ? T - t0 : 0u;
+        const uint32_t aadd = st * apitch, badd = 2u * t0;
 #pragma unroll
         for (int i = 0; i < C::IB; ++i) {
             const uint32_t b = wave + C::NW * i;
-            const bool isA = b * C::RPI < (uint32_t)C::AROWS;
-            const uint32_t off = (!past && t0 + bcm[i] < T) ? boff[i] + (isA ? st * apitch : 2u * t0) : kOOB;
+            // where the A blocks split evenly over the waves, the first IA
+            // loads of every wave are A blocks (known at compile time)
+            const bool isA = C::IA >= 0 ? i < C::IA : b * C::RPI < (uint32_t)C::AROWS;
+            const uint32_t off = bcm[i] < lim ? boff[i] + (isA ? aadd : badd) : kOOB;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(isA ? rf : rw, (lds_ptr)(slot + 1024 * b), 16, off,
                                                      0, 0, 0);
         }

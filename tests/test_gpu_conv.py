@@ -207,8 +207,10 @@ VARIANT_CASES = [
                          "k3c256p192t32s2w8"],
      (2, 64, 24, 24, 300, 3, 3, 1), torch.float16, False),
     # the 7x7 column-staged tiles (filter width 7, stride 1 and 2)
-    ("IM2WIN_FP16_COL", ["k7c64p256t16s3", "k7c64p128t16s2"], (2, 16, 19, 40, 70, 7, 7, 1), torch.float16, False),
-    ("IM2WIN_FP16_COL", ["k7c64p256t16s3", "k7c64p128t16s2"], (2, 8, 23, 121, 40, 7, 7, 2), torch.float16, False),
+    ("IM2WIN_FP16_COL", ["k7c64p256t16s3", "k7c64p128t16s2", "k7c64p256t32s2"],
+     (2, 16, 19, 40, 70, 7, 7, 1), torch.float16, False),
+    ("IM2WIN_FP16_COL", ["k7c64p256t16s3", "k7c64p128t16s2", "k7c64p256t32s2"],
+     (2, 8, 23, 121, 40, 7, 7, 2), torch.float16, False),
     ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16", "p6c8l8s2k16", "p4c8l8s2k16", "p4c16l1s2k16", "p8c8l8s2k16g4",
                             "p4c12l8s2k16", "p8c12l8s2k16", "p4c12l8s2k16g4", "p8c12l8s2k16g4", "regs"],
      (2, 16, 17, 19, 100, 3, 3, 1), torch.float32, True),
