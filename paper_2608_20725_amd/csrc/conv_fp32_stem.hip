@@ -36,24 +36,23 @@ constexpr int kS32Waves = 4;
 typedef const float __attribute__((address_space(4))) *cfloat_ptr;
 
 // The window of this lane's pixel in block blk, as 16-byte loads from its
-// 4-byte-aligned start (unaligned loads; at most 3 elements past the last
-// window, inside the zero pad after the tensor); values past K are set to 0.
+// 4-byte-aligned start, issued without branches (raw: values past K belong
+// to the next window or to the zero pad after the tensor, at most 60 bytes
+// past the last window; a pixel past P reads the tensor's first bytes).
+// They are masked where they are used, so that the compiler's memory-counter
+// waits do not make these prefetch loads wait for the previous block's
+// stores.
 template <int KMAX>
-__device__ inline void load_window(const S32Args &a, uint32_t blk, uint32_t lane, float (&x)[(KMAX + 3) / 4 * 4])
+__device__ inline void load_window(const S32Args &a, uint32_t blk, uint32_t lane, u32x4 (&x)[(KMAX + 3) / 4])
 {
     const uint32_t p = blk * 64 + lane;
     const bool live = p < a.P;
     const uint32_t q = live ? fdiv(p, a.div_Wo) : 0u;
-    const char *win = reinterpret_cast<const char *>(a.ws + (uint64_t)q * a.L + (uint64_t)(p - q * a.Wo) * a.S);
+    const uint64_t w0 = live ? (uint64_t)q * a.L + (uint64_t)(p - q * a.Wo) * a.S : 0u;
+    const char *win = reinterpret_cast<const char *>(a.ws + w0);
 #pragma unroll
-    for (int g = 0; g < (KMAX + 3) / 4; ++g) {
-        float v[4] = {0.f, 0.f, 0.f, 0.f};
-        if (live && (uint32_t)(4 * g) < a.K)
-            __builtin_memcpy(v, win + 16 * g, 16);
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            x[4 * g + e] = (uint32_t)(4 * g + e) < a.K ? v[e] : 0.f;
-    }
+    for (int g = 0; g < (KMAX + 3) / 4; ++g)
+        __builtin_memcpy(&x[g], win + 16 * g, 16);
 }
 
 template <int KMAX>
@@ -70,19 +69,24 @@ __global__ __launch_bounds__(64 * kS32Waves) void conv_fp32_stem(S32Args a)
     const cfloat_ptr filt = (cfloat_ptr)a.packed;
 
     uint32_t blk = blockIdx.x * kS32Waves + wave;
-    float xn[KW4 * 4];
-    if (blk < a.nblk)
-        load_window<KMAX>(a, blk, lane, xn);
+    u32x4 xn[KW4];
+    load_window<KMAX>(a, blk, lane, xn);
     for (; blk < a.nblk; blk += nw) {
+        // this block's taps: zero past K and for pixels past P
+        const bool live = blk * 64 + lane < a.P;
         float x[KW4 * 4];
 #pragma unroll
-        for (int t = 0; t < KW4 * 4; ++t)
-            x[t] = xn[t];
-        // the next block's window loads run under this block's FMAs and stores
-        if (blk + nw < a.nblk)
-            load_window<KMAX>(a, blk + nw, lane, xn);
+        for (int g = 0; g < KW4; ++g)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                x[4 * g + e] = live && (uint32_t)(4 * g + e) < a.K ? __uint_as_float(xn[g][e]) : 0.f;
+        // the next block's window loads run under this block's FMAs and
+        // stores (past the last block they are issued too and never used)
+        load_window<KMAX>(a, blk + nw, lane, xn);
+        // the block's rows are one contiguous run of the output; rows past
+        // the last pixel fall outside the resource and are dropped
         const uint32_t live_rows = a.P - blk * 64 < 64 ? a.P - blk * 64 : 64;
-        float *dst = a.out + (uint64_t)blk * 64 * a.Co;
+        const __amdgpu_buffer_rsrc_t ro = make_rsrc(a.out + (uint64_t)blk * 64 * a.Co, live_rows * a.Co * 4u);
         for (uint32_t c0 = 0; c0 < a.Co; c0 += 32) {
             float acc[32];
 #pragma unroll
@@ -105,14 +109,15 @@ __global__ __launch_bounds__(64 * kS32Waves) void conv_fp32_stem(S32Args a)
             __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's rows are in LDS
             __builtin_amdgcn_wave_barrier();
             // instruction i: rows 8*i + lane/8, chunk lane%8 (channels
-            // c0 + 4*(lane%8) ..): eight 128-byte line pieces of the output
+            // c0 + 4*(lane%8) ..): eight 128-byte line pieces of the output;
+            // chunks past C_o read nothing (their offset is out of range)
             const uint32_t k = lane & 7;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const uint32_t r = 8 * i + (lane >> 3);
-                if (r < live_rows && c0 + 4 * k < a.Co)
-                    *reinterpret_cast<float4 *>(dst + (uint64_t)r * a.Co + c0 + 4 * k) =
-                        *reinterpret_cast<const float4 *>(lds + r * 32 + 4 * (k ^ (r & 7)));
+                const u32x4 v = *reinterpret_cast<const u32x4 *>(lds + r * 32 + 4 * (k ^ (r & 7)));
+                __builtin_amdgcn_raw_buffer_store_b128(v, ro, c0 + 4 * k < a.Co ? (r * a.Co + c0 + 4 * k) * 4u : kOOB,
+                                                       0, 0);
             }
             __builtin_amdgcn_s_waitcnt(0xC07F);  // reads done before the next rows land
             __builtin_amdgcn_wave_barrier();
