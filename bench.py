@@ -65,10 +65,10 @@ KERNEL_SOURCES = ("common.hpp", "epilogue16.hpp", "mfma16.hpp", "conv_fp32_dma.h
                   "conv_fp32_stem.hip", "conv_fp16.hip", "conv_fp16_col.hip", "conv_fp16_seg.hip",
                   "conv_fp16_stem.hip")
 CONV_TRAFFIC = {
-    "source_sha256": "fc587fbb5e1eed51dd1164d9eb7eb2a8cd639de4c34db42ac586e34b64371740",
+    "source_sha256": "c264de96d062ae5107fb1898fa871732a1fc01ef57ecbbf1238edfc7663468e3",
     "workload": "sweep",
-    "f32": 31966371760,    # bytes per step, fetched + written
-    "f16": 6463079506,
+    "f32": 31961820371,    # bytes per step, fetched + written
+    "f16": 6463528894,
 }
 
 
