@@ -387,33 +387,46 @@ struct Pipe {
 
     // Stage s >= nst (past the end of K) loads nothing: every offset is out of
     // range and the slot is filled with zeros.
-    __device__ inline void issue(uint32_t s, char *stage)
+    // Offsets of stage s's loads.  A window chunk whose first tap (within
+    // the stage) is at or past `lim` reads nothing: every chunk of a stage
+    // past the end, the chunks past K in the last stage.  Filter rows: taps
+    // k0 .. k0+63 are tile k0/64 of the packed filter (apitch bytes each);
+    // window rows: taps k0 .. k0+63.
+    struct StageLoads {
+        uint32_t lim, fadd, wadd;
+        bool past;
+    };
+    __device__ inline StageLoads stage_loads(uint32_t s) const
     {
         // first tap of the stage (column order only when every stage is
         // whole: K_h*C_i a multiple of 64)
         const uint32_t k0 = to.map((s + sb) * BK);
         const bool past = s >= nst;
-        // a window chunk whose first tap (within the stage) is at or past
-        // `lim` reads nothing: every chunk of a stage past the end, the
-        // chunks past K in the last stage
-        const uint32_t lim = past ? 0u : k0 + BK <= K ? 0xffffffffu : k0 < K ? K - k0 : 0u;
-        // filter rows: taps k0 .. k0+63 are tile k0/64 of the packed filter
-        // (apitch bytes each); window rows: taps k0 .. k0+63
-        const uint32_t fadd = (k0 / BK) * apitch, wadd = 2u * k0;
-#pragma unroll
-        for (int j = 0; j < C::I; ++j) {
-            // block wave + NW*j: the first IF loads of every wave fill
-            // filter blocks, so which buffer a load reads is known at compile
-            // time and the offsets are plain selects
-            const uint32_t b = wave + C::NW * j;
-            if (j < C::IF) {
-                const uint32_t off = past ? kOOB : voff[j] + fadd;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rf, (lds_ptr)(stage + 1024 * b), 16, off, 0, 0, 0);
-            } else {
-                const uint32_t off = vchunk[j] >= lim ? kOOB : voff[j] + wadd;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(stage + 1024 * b), 16, off, 0, 0, 0);
-            }
+        return StageLoads{past ? 0u : k0 + BK <= K ? 0xffffffffu : k0 < K ? K - k0 : 0u, (k0 / BK) * apitch,
+                          2u * k0, past};
+    }
+
+    // Load j of a stage (j < I): block wave + NW*j.  The first IF loads of
+    // every wave fill filter blocks, so which buffer a load reads is known
+    // at compile time and the offsets are plain selects.
+    __device__ inline void issue_one(int j, const StageLoads &sl, char *stage)
+    {
+        const uint32_t b = wave + C::NW * j;
+        if (j < C::IF) {
+            const uint32_t off = sl.past ? kOOB : voff[j] + sl.fadd;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rf, (lds_ptr)(stage + 1024 * b), 16, off, 0, 0, 0);
+        } else {
+            const uint32_t off = vchunk[j] >= sl.lim ? kOOB : voff[j] + sl.wadd;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(stage + 1024 * b), 16, off, 0, 0, 0);
         }
+    }
+
+    __device__ inline void issue(uint32_t s, char *stage)
+    {
+        const StageLoads sl = stage_loads(s);
+#pragma unroll
+        for (int j = 0; j < C::I; ++j)
+            issue_one(j, sl, stage);
     }
 
     // Fragments of k-step ks of the stage.
@@ -434,14 +447,27 @@ struct Pipe {
 
     // All k-steps of one stage; the fragments of step ks+1 are read before
     // the matrix operations of step ks, so their LDS latency runs under them
-    // (with about one wave per SIMD nothing else would hide it).
-    __device__ inline void compute(const char *stage)
+    // (with about one wave per SIMD nothing else would hide it).  With
+    // `nslot` set, the loads of stage `ns` into it are issued a few at a time
+    // after the matrix operations of the first k-steps, so that their issue
+    // runs while the matrix cores work instead of before the first multiply.
+    __device__ inline void compute(const char *stage, uint32_t ns = 0, char *nslot = nullptr)
     {
+        constexpr int KS = BK / 16;
+        // loads per k-step: spread over all k-steps (measured against the
+        // same loads packed into the first two k-steps or the first one: 3x3
+        // C = 512 at 7x7, 424 against 422 / 424 TFLOP/s; 3x3 C = 256 at
+        // 12x12, 685 against 676 / 661; all of them issued before the first
+        // multiply gave 390 and 668)
+        constexpr int LPS = (C::I + KS - 1) / KS;
+        StageLoads sl{};
+        if (nslot)
+            sl = stage_loads(ns);
         v8 af[2][WM], bf[2][WN];
         frags(stage, 0, af[0], bf[0]);
 #pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-            if (ks + 1 < BK / 16)
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + 1 < KS)
                 frags(stage, ks + 1, af[(ks + 1) & 1], bf[(ks + 1) & 1]);
             // keep the reads above the matrix operations (the scheduler would
             // otherwise sink them below to reuse the same registers)
@@ -451,6 +477,12 @@ struct Pipe {
 #pragma unroll
                 for (int j = 0; j < WN; ++j)
                     acc[i][j] = E::mfma(af[ks & 1][i], bf[ks & 1][j], acc[i][j]);
+            if (nslot && ks * LPS < C::I) {
+#pragma unroll
+                for (int j = ks * LPS; j < (ks + 1) * LPS && j < C::I; ++j)
+                    issue_one(j, sl, nslot);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
     }
 
@@ -463,11 +495,10 @@ struct Pipe {
     template <int N>
     __device__ inline void step(uint32_t st, char (&cur)[N], char (&next)[N])
     {
+        // st < nst: the loops of the kernel run real stages only
         wait_vmcnt<(NSTAGE - 2) * C::I>();
         ring_barrier();
-        issue(st + NSTAGE - 1, next);
-        if (st < nst)
-            compute(cur);
+        compute(cur, st + NSTAGE - 1, next);
     }
 
     // One slot, no double buffering (the ablation of Alg. 1's double
@@ -633,31 +664,47 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
 
     // prologue: stages 0 .. NSTAGE-2 into slots 0 .. NSTAGE-2, then stage st
     // in slot st % NSTAGE
+    // (whole rounds of the ring, then the last nst % NSTAGE stages; each
+    // step multiplies a real stage and issues the one NSTAGE-1 ahead, which
+    // past the end loads zeros)
     w.issue(0, r0);
+    uint32_t st = 0;
     if constexpr (NSTAGE == 1) {
-        for (uint32_t st = 0; st < w.nst; ++st)
+        for (; st < w.nst; ++st)
             w.step_single(st, r0);
     } else if constexpr (NSTAGE == 2) {
-        for (uint32_t st = 0; st < w.nst; st += 2) {
+        for (; st + 2 <= w.nst; st += 2) {
             w.step(st, r0, r1);
             w.step(st + 1, r1, r0);
         }
+        if (st < w.nst)
+            w.step(st, r0, r1);
     } else if constexpr (NSTAGE == 3) {
         w.issue(1, r1);
-        for (uint32_t st = 0; st < w.nst; st += 3) {
+        for (; st + 3 <= w.nst; st += 3) {
             w.step(st, r0, r2);
             w.step(st + 1, r1, r0);
             w.step(st + 2, r2, r1);
         }
+        if (st < w.nst)
+            w.step(st, r0, r2);
+        if (st + 1 < w.nst)
+            w.step(st + 1, r1, r0);
     } else {
         w.issue(1, r1);
         w.issue(2, r2);
-        for (uint32_t st = 0; st < w.nst; st += 4) {
+        for (; st + 4 <= w.nst; st += 4) {
             w.step(st, r0, r3);
             w.step(st + 1, r1, r0);
             w.step(st + 2, r2, r1);
             w.step(st + 3, r3, r2);
         }
+        if (st < w.nst)
+            w.step(st, r0, r3);
+        if (st + 1 < w.nst)
+            w.step(st + 1, r1, r0);
+        if (st + 2 < w.nst)
+            w.step(st + 2, r2, r1);
     }
     // no load may still be writing LDS when the workgroup ends
     wait_vmcnt<0>();

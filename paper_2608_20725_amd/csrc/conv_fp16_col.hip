@@ -59,6 +59,11 @@ struct ColArgs {
 };
 
 constexpr uint32_t kNoCol = 0xffffffffu;  // B row with no column (past the last pixel)
+// Next-stage loads issued after each k-step's matrix operations (two per
+// step measured best: 7x7 C = 64 stride 2 at 224x224, 759 TFLOP/s against
+// 747 / 731 / 719 with 4 / 8 / 16 per step and 709 with all of them issued
+// before the stage's first multiply)
+constexpr int kLoadsPerStep = 2;
 
 template <int KW_, int BT_, int WM_, int WN_, int WGM_, int WGN_, int NRMAX_, int NS_>
 struct ColCfg {
@@ -123,23 +128,34 @@ struct ColTile {
     floatx16 acc[C::WM][C::WN];
 
     // Stage st >= nst (past the end of the slices) loads nothing.
-    __device__ inline void issue(uint32_t st, char *slot)
+    // Offsets of stage st's loads: a chunk whose first t is at or past `lim`
+    // reads nothing (A rows have bcm = 0: only stages past the end or past T).
+    struct StageLoads {
+        uint32_t lim, aadd, badd;
+    };
+    __device__ inline StageLoads stage_loads(uint32_t st) const
     {
         const uint32_t t0 = st * C::BT;
-        // a chunk whose first t is at or past `lim` reads nothing (A rows
-        // have bcm = 0: only stages past the end or past T)
-        const uint32_t lim = st >= nst ? 0u : t0 < T ? T - t0 : 0u;
-        const uint32_t aadd = st * apitch, badd = 2u * t0;
+        return StageLoads{st >= nst ? 0u : t0 < T ? T - t0 : 0u, st * apitch, 2u * t0};
+    }
+
+    // Load i of a stage (i < IB).
+    __device__ inline void issue_one(int i, const StageLoads &sl, char *slot)
+    {
+        const uint32_t b = wave + C::NW * i;
+        // where the A blocks split evenly over the waves, the first IA loads
+        // of every wave are A blocks (known at compile time)
+        const bool isA = C::IA >= 0 ? i < C::IA : b * C::RPI < (uint32_t)C::AROWS;
+        const uint32_t off = bcm[i] < sl.lim ? boff[i] + (isA ? sl.aadd : sl.badd) : kOOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(isA ? rf : rw, (lds_ptr)(slot + 1024 * b), 16, off, 0, 0, 0);
+    }
+
+    __device__ inline void issue(uint32_t st, char *slot)
+    {
+        const StageLoads sl = stage_loads(st);
 #pragma unroll
-        for (int i = 0; i < C::IB; ++i) {
-            const uint32_t b = wave + C::NW * i;
-            // where the A blocks split evenly over the waves, the first IA
-            // loads of every wave are A blocks (known at compile time)
-            const bool isA = C::IA >= 0 ? i < C::IA : b * C::RPI < (uint32_t)C::AROWS;
-            const uint32_t off = bcm[i] < lim ? boff[i] + (isA ? aadd : badd) : kOOB;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(isA ? rf : rw, (lds_ptr)(slot + 1024 * b), 16, off,
-                                                     0, 0, 0);
-        }
+        for (int i = 0; i < C::IB; ++i)
+            issue_one(i, sl, slot);
     }
 
     // Fragments of k-step ks (filter column v = ks / (BT/16)).
@@ -161,10 +177,16 @@ struct ColTile {
     }
 
     // All k-steps of one stage; the fragments of step ks+1 are read before
-    // the matrix operations of step ks.
-    __device__ inline void compute(const char *slot)
+    // the matrix operations of step ks.  With `nslot` set, the loads of stage
+    // `nst_` into it are issued a few at a time after the matrix operations
+    // of each k-step, so their issue runs while the matrix cores work instead
+    // of before the stage's first multiply.
+    __device__ inline void compute(const char *slot, uint32_t nst_ = 0, char *nslot = nullptr)
     {
         constexpr int KS = C::KW * C::BT / 16;
+        StageLoads sl{};
+        if (nslot)
+            sl = stage_loads(nst_);
         v8 af[2][C::WM], bf[2][C::WN];
         frags(slot, 0, af[0], bf[0]);
 #pragma unroll
@@ -176,6 +198,15 @@ struct ColTile {
 #pragma unroll
                 for (int j = 0; j < C::WN; ++j)
                     acc[i][j] = E::mfma(af[ks & 1][i], bf[ks & 1][j], acc[i][j]);
+            if (nslot && ks * kLoadsPerStep < C::IB) {
+                // loads 2*ks, 2*ks+1 after step ks: early in the stage, so
+                // they have most of it to land, and kept there (the
+                // scheduler would otherwise sink them to its end)
+#pragma unroll
+                for (int i = ks * kLoadsPerStep; i < (ks + 1) * kLoadsPerStep && i < C::IB; ++i)
+                    issue_one(i, sl, nslot);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
     }
 
@@ -195,11 +226,10 @@ struct ColTile {
             issue(st + C::NS - 1, next);
             return;
         }
+        // st < nst: the loops below run real stages only
         wait_vmcnt<(C::NS - 2) * C::IB>();
         ring_barrier();
-        issue(st + C::NS - 1, next);
-        if (st < nst)
-            compute(cur);
+        compute(cur, st + C::NS - 1, next);
     }
 };
 
@@ -296,28 +326,44 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
 
     // prologue: stages 0 .. NS-2 into slots 0 .. NS-2; stage st then sits
     // in slot st % NS
+    // (whole rounds of the ring, then the last nst % NS stages; each step
+    // multiplies a real stage and issues the one NS-1 ahead, which past the
+    // end loads zeros)
     w.issue(0, r0);
+    uint32_t st = 0;
     if constexpr (C::NS == 2) {
-        for (uint32_t st = 0; st < w.nst; st += 2) {
+        for (; st + 2 <= w.nst; st += 2) {
             w.step(st, r0, r1);
             w.step(st + 1, r1, r0);
         }
+        if (st < w.nst)
+            w.step(st, r0, r1);
     } else if constexpr (C::NS == 3) {
         w.issue(1, r1);
-        for (uint32_t st = 0; st < w.nst; st += 3) {
+        for (; st + 3 <= w.nst; st += 3) {
             w.step(st, r0, r2);
             w.step(st + 1, r1, r0);
             w.step(st + 2, r2, r1);
         }
+        if (st < w.nst)
+            w.step(st, r0, r2);
+        if (st + 1 < w.nst)
+            w.step(st + 1, r1, r0);
     } else {
         w.issue(1, r1);
         w.issue(2, r2);
-        for (uint32_t st = 0; st < w.nst; st += 4) {
+        for (; st + 4 <= w.nst; st += 4) {
             w.step(st, r0, r3);
             w.step(st + 1, r1, r0);
             w.step(st + 2, r2, r1);
             w.step(st + 3, r3, r2);
         }
+        if (st < w.nst)
+            w.step(st, r0, r3);
+        if (st + 1 < w.nst)
+            w.step(st + 1, r1, r0);
+        if (st + 2 < w.nst)
+            w.step(st + 2, r2, r1);
     }
     // no load may still be writing LDS when the workgroup ends
     wait_vmcnt<0>();
