@@ -241,6 +241,9 @@ int launch_status(hipError_t e);
 //   IM2WIN_FP32_COLS       a column-staged variant name
 //   IM2WIN_FP32_MFMA_TILE  a matrix-core fp32 tile name
 //   IM2WIN_TRANSFORM_ORDER linear | xcd
+//   IM2WIN_TRANSFORM_KERNEL pieces | gather: the 3-channel layers' transform
+//                          (one load per 3-channel pixel, where it is the
+//                          faster, or one per element)
 //   IM2WIN_TILE_ORDER      linear | xcd
 //   IM2WIN_TAP_ORDER       linear | column: the K-loop order of the DMA-staged
 //                          fp32 kernel (column by default) and of the
@@ -261,6 +264,7 @@ struct Tuning {
     int fp32_cols;                     // column-staged variant index, -1: not forced
     int fp32_mfma_tile;                // -1: not forced
     bool transform_linear, tile_linear;
+    bool transform_gather;             // 3-channel transform: element gather only
     enum { kDefault = 0, kLinear = 1, kColumn = 2 };
     int tap_order;  // kDefault: each kernel's own (column for the DMA fp32 kernel, linear for the others)
     int fp16_split; // K split of the row-per-pixel kernel: 0 (the planner's choice) or 1..kMaxSplit

@@ -74,6 +74,13 @@ int read_tuning(Tuning *t)
     if ((rc = read_order("IM2WIN_TRANSFORM_ORDER", "xcd", &t->transform_linear)) != IM2WIN_OK ||
         (rc = read_order("IM2WIN_TILE_ORDER", "xcd", &t->tile_linear)) != IM2WIN_OK)
         return rc;
+    t->transform_gather = false;
+    if (const char *e = getenv("IM2WIN_TRANSFORM_KERNEL")) {
+        if (strcmp(e, "gather") == 0)
+            t->transform_gather = true;
+        else if (*e && strcmp(e, "pieces") != 0)
+            return IM2WIN_EINVAL;
+    }
     t->tap_order = Tuning::kDefault;
     if (const char *e = getenv("IM2WIN_TAP_ORDER")) {
         if (strcmp(e, "linear") == 0)
@@ -111,6 +118,7 @@ Tuning default_tuning()
     t.fp16_col = t.fp16_tile = t.fp16_seg = -1;
     t.fp32_kernel = t.fp32_tile = t.fp32_mfma_tile = t.fp32_cols = -1;
     t.transform_linear = t.tile_linear = false;
+    t.transform_gather = false;
     t.tap_order = Tuning::kDefault;
     t.fp16_split = 0;
     return t;

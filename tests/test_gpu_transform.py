@@ -100,6 +100,30 @@ def test_transform_linear_block_order_same_bytes(shape, monkeypatch):
 # Unaligned windows (C_i * elt not a multiple of 16 bytes) take the element
 # gather: odd channel counts, strips that end inside a granule, K_h = H, a
 # tall filter over a wide input, stride > K.
+# The 3-channel layers' one-load-per-pixel gather (fp32; fp16 and bf16 with
+# K_h <= 3) against the element gather: the same bytes, pad included, on odd
+# and even widths, strides up to the filter height, and the Table I stems.
+PIECES3 = [(2, 3, 12, 13, 3, 3, 1), (2, 3, 10, 11, 2, 2, 2), (1, 3, 7, 6, 1, 1, 1), (3, 3, 17, 16, 5, 5, 2),
+           (1, 3, 23, 31, 7, 7, 3), (2, 3, 29, 27, 11, 11, 4), (1, 3, 11, 9, 11, 3, 1), (2, 3, 9, 40, 3, 3, 3),
+           (2, 3, 227, 227, 11, 11, 4), (2, 3, 227, 227, 7, 7, 2), (2, 3, 224, 224, 3, 3, 1)]
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "f16", "bf16"])
+@pytest.mark.parametrize("shape", PIECES3, ids=lambda s: "x".join(map(str, s)))
+def test_transform_3ch_pieces_equal_gather(shape, dtype, monkeypatch):
+    N, Ci, H, W, Kh, Kw, s = shape
+    x, w = workloads.draw(N, Ci, H, W, 2, Kh, Kw, seed=7 + sum(shape))
+    outs = []
+    for kernel in ("pieces", "gather"):
+        monkeypatch.setenv("IM2WIN_TRANSFORM_KERNEL", kernel)
+        say("transform", kernel, shape, dtype)
+        run = Run(x, w, s, dtype, conv=False)
+        if not outs:
+            _compare(run, x)
+        outs.append(run.ws.cpu())
+    assert torch.equal(outs[0], outs[1])
+
+
 UNALIGNED = [(2, 3, 12, 12, 3, 3, 1), (3, 5, 11, 13, 5, 3, 2), (1, 7, 9, 31, 9, 2, 3), (2, 1, 8, 8, 8, 8, 1),
              (2, 3, 227, 40, 11, 11, 4), (1, 3, 30, 300, 27, 5, 1), (2, 6, 10, 10, 2, 2, 3)]
 

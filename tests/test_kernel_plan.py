@@ -13,7 +13,7 @@ from paper_2608_20725_amd import workloads
 EINVAL = -1
 VARS = ("IM2WIN_FP16_KERNEL", "IM2WIN_FP16_COL", "IM2WIN_FP16_TILE", "IM2WIN_FP16_SEG", "IM2WIN_FP32_KERNEL",
         "IM2WIN_FP32_TILE", "IM2WIN_FP32_MFMA_TILE", "IM2WIN_TRANSFORM_ORDER", "IM2WIN_TILE_ORDER",
-        "IM2WIN_TAP_ORDER", "IM2WIN_FP16_SPLIT", "IM2WIN_FP32_COLS")
+        "IM2WIN_TAP_ORDER", "IM2WIN_FP16_SPLIT", "IM2WIN_FP32_COLS", "IM2WIN_TRANSFORM_KERNEL")
 
 
 @pytest.fixture(autouse=True)
@@ -133,6 +133,16 @@ def test_orders_accept_both_names(monkeypatch):
         assert name((1, 64, 10, 10, 64, 3, 3, 1), "f32")
     monkeypatch.setenv("IM2WIN_TAP_ORDER", "xcd")   # the tile orders' word is not a tap order
     assert status((1, 64, 10, 10, 64, 3, 3, 1), "f32") == EINVAL
+
+
+def test_transform_kernel_names(monkeypatch):
+    """IM2WIN_TRANSFORM_KERNEL takes pieces or gather; any other word is
+    refused by every call, the query included."""
+    for v in ("pieces", "gather", ""):
+        monkeypatch.setenv("IM2WIN_TRANSFORM_KERNEL", v)
+        assert name((1, 3, 32, 32, 16, 3, 3, 1), "f16")
+    monkeypatch.setenv("IM2WIN_TRANSFORM_KERNEL", "vec")
+    assert status((1, 3, 32, 32, 16, 3, 3, 1), "f16") == EINVAL
 
 
 # The mini-batch path makes its plan for a full chunk and runs it on the
