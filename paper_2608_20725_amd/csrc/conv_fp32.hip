@@ -48,27 +48,27 @@ struct C32Args {
 };
 
 // ---------------------------------------------------------------------------
-// Filter repack: one thread per 4 consecutive channels of one tap row of F'.
+// Filter repack: one thread per 4 consecutive channels of one tap row of F'
+// (32-bit indices, the host checks the count; divisions by multiplication).
 struct Pack32Args {
     const float *filt;
     float *packed;
-    uint64_t quads;
+    uint32_t quads;
     uint32_t K, Co, Co_pad, Ci, Kh, Kw;
     uint32_t pair_swap;  // store channels 2i and 2i+1 swapped (the DMA-staged kernel's order)
+    FastDiv div_qpr, div_khci, div_ci;  // C_o_pad/4, K_h*C_i, C_i
 };
 
 __global__ __launch_bounds__(256) void pack_filter_fp32(Pack32Args a)
 {
     const uint32_t qpr = a.Co_pad / 4;  // quads per packed row
-    for (uint64_t g = (uint64_t)blockIdx.x * 256 + threadIdx.x; g < a.quads;
-         g += (uint64_t)gridDim.x * 256) {
-        const uint32_t k = (uint32_t)(g / qpr);
-        const uint32_t j0 = (uint32_t)(g % qpr) * 4;
+    for (uint32_t g = blockIdx.x * 256 + threadIdx.x; g < a.quads; g += gridDim.x * 256) {
+        const uint32_t k = fdiv(g, a.div_qpr);
+        const uint32_t j0 = (g - k * qpr) * 4;
         float v[4] = {0.f, 0.f, 0.f, 0.f};
         if (k < a.K) {
-            const uint32_t khci = a.Kh * a.Ci;
-            const uint32_t vv = k / khci, rem = k % khci;
-            const uint32_t u = rem / a.Ci, r = rem % a.Ci;
+            const uint32_t vv = fdiv(k, a.div_khci), rem = k - vv * a.Kh * a.Ci;
+            const uint32_t u = fdiv(rem, a.div_ci), r = rem - u * a.Ci;
             const float *src = a.filt + (((uint64_t)u * a.Kw + vv) * a.Ci + r) * a.Co;
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -508,12 +508,18 @@ hipError_t launch_pack_fp32(const Shape &sh, const Plan32 &p, const float *filt,
     Pack32Args a;
     a.filt = filt;
     a.packed = static_cast<float *>(packed);
-    a.quads = (uint64_t)sh.K_pad32 * sh.Co_pad32 / 4;
+    const uint64_t quads = (uint64_t)sh.K_pad32 * sh.Co_pad32 / 4;
+    if (quads >= (1ull << 31))
+        return hipErrorInvalidValue;
+    a.quads = (uint32_t)quads;
     a.K = (uint32_t)sh.K; a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
     a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
+    a.div_qpr = make_fastdiv(a.Co_pad / 4);
+    a.div_khci = make_fastdiv(a.Kh * a.Ci);
+    a.div_ci = make_fastdiv(a.Ci);
     // the DMA- and column-staged kernels read channel pairs swapped
     a.pair_swap = p.fam == Fam32::Dma || p.fam == Fam32::Cols;
-    uint64_t blocks = (a.quads + 255) / 256;
+    uint64_t blocks = (quads + 255) / 256;
     if (blocks > 65536)
         blocks = 65536;
     void *args[] = {&a};
