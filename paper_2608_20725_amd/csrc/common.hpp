@@ -241,6 +241,9 @@ int launch_status(hipError_t e);
 //   IM2WIN_FP32_COLS       a column-staged variant name
 //   IM2WIN_FP32_MFMA_TILE  a matrix-core fp32 tile name
 //   IM2WIN_TRANSFORM_ORDER linear | xcd
+//   IM2WIN_FP16_PERSIST    on | off: column-staged fp16 kernel in one round of
+//                          workgroups that walk the tiles (on by default
+//                          where it applies) or one workgroup per tile
 //   IM2WIN_TRANSFORM_KERNEL pieces | gather: the 3-channel layers' transform
 //                          (one load per 3-channel pixel, where it is the
 //                          faster, or one per element)
@@ -265,6 +268,7 @@ struct Tuning {
     int fp32_mfma_tile;                // -1: not forced
     bool transform_linear, tile_linear;
     bool transform_gather;             // 3-channel transform: element gather only
+    bool col_persist;                  // column-staged fp16 kernel: persistent launch where it applies
     enum { kDefault = 0, kLinear = 1, kColumn = 2 };
     int tap_order;  // kDefault: each kernel's own (column for the DMA fp32 kernel, linear for the others)
     int fp16_split; // K split of the row-per-pixel kernel: 0 (the planner's choice) or 1..kMaxSplit

@@ -54,6 +54,8 @@ struct ColArgs {
     uint64_t win_bytes;
     uint64_t pk_bytes;       // bytes of G
     uint32_t P, Co, Co_pad, Wo, L, T, Tp, s, ms, nst;
+    uint32_t ntiles;         // gx * gy
+    uint32_t persist;        // 1: each workgroup walks tiles blockIdx.x, + gridDim.x, ...
     TileGrid tg;             // pixel x channel tiles of the 1-D launch
     FastDiv div_Wo;
 };
@@ -65,11 +67,12 @@ constexpr uint32_t kNoCol = 0xffffffffu;  // B row with no column (past the last
 // before the stage's first multiply)
 constexpr int kLoadsPerStep = 2;
 
-template <int KW_, int BT_, int WM_, int WN_, int WGM_, int WGN_, int NRMAX_, int NS_>
+template <int KW_, int BT_, int WM_, int WN_, int WGM_, int WGN_, int NRMAX_, int NS_, bool PERSIST_ = true>
 struct ColCfg {
     static constexpr int KW = KW_, BT = BT_, WM = WM_, WN = WN_, WGM = WGM_, WGN = WGN_;
     static constexpr int NS = NS_;              // ring slots
     static constexpr bool SERIAL = false;       // see Serialized
+    static constexpr bool PERSIST = PERSIST_;   // the persistent tile loop is compiled in
     static constexpr int NW = WGM * WGN;        // waves
     static constexpr int NT = 64 * NW;
     static constexpr int BM = 32 * WM * WGM;    // channels per tile
@@ -90,6 +93,12 @@ struct ColCfg {
     static_assert(NS >= 2 && NS <= 4, "ring depth");
     static_assert((NS - 2) * IB <= 63, "vmcnt range");
     static constexpr int SWS = CH == 4 ? 2 : 3;          // swizzle shift
+    // LDS per workgroup (ring slots, the two-slot kernels' unused slot
+    // stand-ins, the column table) and the waves per SIMD it leaves room for:
+    // the register budget the compiler is held to, so that a persistent
+    // tile loop does not cost occupancy
+    static constexpr int LDSB = NS * STAGE + (4 - NS) * 1024 + 4 * NRMAX;
+    static constexpr int WPE = (160 * 1024 / LDSB) * NW / 4 < 1 ? 1 : (160 * 1024 / LDSB) * NW / 4;
     static_assert(BT == 16 || BT == 32 || BT == 64, "stage depth");
     static_assert(AROWS % RPI == 0, "A and B rows meet at a block boundary");
 };
@@ -231,10 +240,108 @@ struct ColTile {
         ring_barrier();
         compute(cur, st + C::NS - 1, next);
     }
+
+    // The tile's resources, column table, per-lane load offsets and B rows
+    // (the table in LDS; two workgroup barriers, with nothing in flight).
+    template <int N>
+    __device__ inline void setup(const ColArgs &a, uint32_t tile, uint32_t (&tbl)[N], uint32_t tid, uint32_t &p0,
+                                 uint32_t &ch0)
+    {
+        uint32_t tx, ty;
+        a.tg.tile_of(tile, tx, ty);
+        p0 = tx * C::BN;
+        ch0 = ty * C::BM;
+        const uint32_t q0 = fdiv(p0, a.div_Wo);
+
+        // B rows address the window tensor from strip q0 on, A rows the
+        // filter from row ch0 on; anything past either buffer reads zero.
+        const uint64_t tb = (uint64_t)q0 * a.L;
+        const uint64_t wleft = a.win_bytes - tb * 2;
+        rw = make_rsrc(a.ws + tb, (uint32_t)(wleft < kMaxRecords ? wleft : kMaxRecords));
+        // the packed filter in BT-tap tiles: tile st holds, for each filter
+        // column v, the C_o_pad rows of slice v; addressed from row ch0 of
+        // (tile 0, v 0)
+        const uint64_t fb = (uint64_t)ch0 * C::BT;
+        rf = make_rsrc(a.packed + fb, (uint32_t)(a.pk_bytes - fb * 2));
+        apitch = (uint32_t)C::KW * a.Co_pad * C::BT * 2u;
+
+        // Column table: element offset (from strip q0) of the column each B
+        // row holds.  Pixel slot n owns rows R(n) .. R(n)+ms-1; the last pixel
+        // of a strip run also owns the K_w - ms rows after them.
+        for (uint32_t r = tid; r < (uint32_t)C::NRMAX; r += C::NT)
+            tbl[r] = kNoCol;
+        __syncthreads();
+        const uint32_t kwm = C::KW - a.ms;
+        for (uint32_t n = tid; n < (uint32_t)C::BN; n += C::NT) {
+            const uint32_t p = p0 + n;
+            if (p < a.P) {
+                const uint32_t q = fdiv(p, a.div_Wo);
+                const uint32_t c = p - q * a.Wo;
+                const uint32_t k = q - q0;
+                const uint32_t R = n * a.ms + k * kwm;
+                const bool last = n == (uint32_t)C::BN - 1 || p + 1 == a.P || c + 1 == a.Wo;
+                const uint32_t nv = last ? (uint32_t)C::KW : a.ms;
+                for (uint32_t v = 0; v < nv; ++v)
+                    tbl[R + v] = k * a.L + (c * a.s + v) * a.T;
+            }
+        }
+        __syncthreads();
+
+        // Per-lane load offsets, fixed for the whole tile.
+#pragma unroll
+        for (int i = 0; i < C::IB; ++i) {
+            const uint32_t b = wave + C::NW * i;
+            const uint32_t row = b * C::RPI + lane / C::CH;
+            const uint32_t c = (lane % C::CH) ^ sw<C>(row);
+            boff[i] = kOOB;
+            bcm[i] = 0;
+            if (row < (uint32_t)C::AROWS) {
+                const uint32_t v = row / C::BM, jl = row % C::BM;
+                boff[i] = ((v * a.Co_pad + jl) * C::BT + 8 * c) * 2u;
+            } else if (row < (uint32_t)C::ROWS) {
+                const uint32_t e = tbl[row - C::AROWS];
+                if (e != kNoCol)
+                    boff[i] = (e + 8 * c) * 2u;
+                bcm[i] = 8 * c;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < C::WN; ++j) {
+            const uint32_t n = wn * 32 * C::WN + 32 * j + (lane & 31);
+            const uint32_t p = p0 + n;
+            // a pixel past P reads row 0 (its result is never stored)
+            Rj[j] = p < a.P ? n * a.ms + (fdiv(p, a.div_Wo) - q0) * kwm : 0;
+        }
+    }
+
+    __device__ inline void zero_acc()
+    {
+#pragma unroll
+        for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::WN; ++j)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    acc[i][j][e] = 0.f;
+    }
 };
 
+// A workgroup may walk several tiles (a persistent launch) when its ring has
+// two slots and the tile's epilogue fits one: after a tile's last stage
+// (which sits in slot 1, the stage count being even) it stages the finished
+// tile in slot 1, sets up the next tile, stores the finished one and issues
+// the next tile's first stage into slot 0, so that stage's loads and the
+// stores are in flight together instead of the loads waiting behind a new
+// workgroup's start.
+template <class C>
+constexpr bool col_persist_ok()
+{
+    return C::PERSIST && C::NS == 2 && !C::SERIAL && epilogue16_bytes<C::BM, C::BN>() <= C::STAGE &&
+           (C::BN * (2 * C::BM / 16)) % C::NT == 0;
+}
+
 template <class C, class E>
-__global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
+__global__ __launch_bounds__(C::NT, C::WPE) void conv_fp16_col(ColArgs a)
 {
     constexpr int S2 = C::NS > 2 ? C::STAGE : 1024, S3 = C::NS > 3 ? C::STAGE : 1024;
     __shared__ __attribute__((aligned(1024))) char r0[C::STAGE];
@@ -252,77 +359,9 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
     w.wn = w.wave % C::WGN;
     w.T = a.T;
     w.nst = a.Tp / C::BT;
-    uint32_t tx, ty;
-    a.tg.tile(tx, ty);
-    const uint32_t p0 = tx * C::BN;
-    const uint32_t ch0 = ty * C::BM;
-    const uint32_t q0 = fdiv(p0, a.div_Wo);
-
-    // B rows address the window tensor from strip q0 on, A rows the filter
-    // from row ch0 on; anything past either buffer reads zero.
-    const uint64_t tb = (uint64_t)q0 * a.L;
-    const uint64_t wleft = a.win_bytes - tb * 2;
-    w.rw = make_rsrc(a.ws + tb, (uint32_t)(wleft < kMaxRecords ? wleft : kMaxRecords));
-    // the packed filter in BT-tap tiles: tile st holds, for each filter column
-    // v, the C_o_pad rows of slice v; addressed from row ch0 of (tile 0, v 0)
-    const uint64_t fb = (uint64_t)ch0 * C::BT;
-    w.rf = make_rsrc(a.packed + fb, (uint32_t)(a.pk_bytes - fb * 2));
-    w.apitch = (uint32_t)C::KW * a.Co_pad * C::BT * 2u;
-
-    // Column table: element offset (from strip q0) of the column each B row
-    // holds.  Pixel slot n owns rows R(n) .. R(n)+ms-1; the last pixel of a
-    // strip run also owns the K_w - ms rows after them.
-    for (uint32_t r = tid; r < (uint32_t)C::NRMAX; r += C::NT)
-        tbl[r] = kNoCol;
-    __syncthreads();
-    const uint32_t kwm = C::KW - a.ms;
-    for (uint32_t n = tid; n < (uint32_t)C::BN; n += C::NT) {
-        const uint32_t p = p0 + n;
-        if (p < a.P) {
-            const uint32_t q = fdiv(p, a.div_Wo);
-            const uint32_t c = p - q * a.Wo;
-            const uint32_t k = q - q0;
-            const uint32_t R = n * a.ms + k * kwm;
-            const bool last = n == (uint32_t)C::BN - 1 || p + 1 == a.P || c + 1 == a.Wo;
-            const uint32_t nv = last ? (uint32_t)C::KW : a.ms;
-            for (uint32_t v = 0; v < nv; ++v)
-                tbl[R + v] = k * a.L + (c * a.s + v) * a.T;
-        }
-    }
-    __syncthreads();
-
-    // Per-lane load offsets, fixed for the whole tile.
-#pragma unroll
-    for (int i = 0; i < C::IB; ++i) {
-        const uint32_t b = w.wave + C::NW * i;
-        const uint32_t row = b * C::RPI + w.lane / C::CH;
-        const uint32_t c = (w.lane % C::CH) ^ sw<C>(row);
-        w.boff[i] = kOOB;
-        w.bcm[i] = 0;
-        if (row < (uint32_t)C::AROWS) {
-            const uint32_t v = row / C::BM, jl = row % C::BM;
-            w.boff[i] = ((v * a.Co_pad + jl) * C::BT + 8 * c) * 2u;
-        } else if (row < (uint32_t)C::ROWS) {
-            const uint32_t e = tbl[row - C::AROWS];
-            if (e != kNoCol)
-                w.boff[i] = (e + 8 * c) * 2u;
-            w.bcm[i] = 8 * c;
-        }
-    }
-#pragma unroll
-    for (int j = 0; j < C::WN; ++j) {
-        const uint32_t n = w.wn * 32 * C::WN + 32 * j + (w.lane & 31);
-        const uint32_t p = p0 + n;
-        // a pixel past P reads row 0 (its result is never stored)
-        w.Rj[j] = p < a.P ? n * a.ms + (fdiv(p, a.div_Wo) - q0) * kwm : 0;
-    }
-#pragma unroll
-    for (int i = 0; i < C::WM; ++i)
-#pragma unroll
-        for (int j = 0; j < C::WN; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                w.acc[i][j][e] = 0.f;
+    uint32_t tile = blockIdx.x, p0, ch0;
+    w.setup(a, tile, tbl, tid, p0, ch0);
+    w.zero_acc();
 
     // prologue: stages 0 .. NS-2 into slots 0 .. NS-2; stage st then sits
     // in slot st % NS
@@ -332,12 +371,38 @@ __global__ __launch_bounds__(C::NT) void conv_fp16_col(ColArgs a)
     w.issue(0, r0);
     uint32_t st = 0;
     if constexpr (C::NS == 2) {
-        for (; st + 2 <= w.nst; st += 2) {
-            w.step(st, r0, r1);
-            w.step(st + 1, r1, r0);
+        for (;;) {
+            st = 0;
+            for (; st + 2 <= w.nst; st += 2) {
+                w.step(st, r0, r1);
+                w.step(st + 1, r1, r0);
+            }
+            if (st < w.nst)
+                w.step(st, r0, r1);
+            if constexpr (col_persist_ok<C>()) {
+                const uint32_t next = tile + gridDim.x;
+                if (a.persist && next < a.ntiles) {
+                    // the last stage (odd) is in r1, the zero loads of the
+                    // stage past the end went to r0
+                    wait_vmcnt<0>();
+                    ring_barrier();
+                    // the finished sums into r1 (so that they are not live
+                    // beside the next tile's load offsets), the next tile's
+                    // set-up, r1 out to the output, then the next tile's
+                    // first stage into r0: the first wait of the next tile
+                    // covers these stores and loads in flight together
+                    stage_tile_lds_ring<E, C::WM, C::WN, C::WGM, C::WGN>(w.acc, r1, w.wm, w.wn, w.lane);
+                    w.zero_acc();
+                    const uint32_t pc = p0, cc = ch0;
+                    w.setup(a, next, tbl, tid, p0, ch0);
+                    copy_tile_out_ring<C::BM, C::BN, C::NT>(r1, a.out, a.P, a.Co, pc, cc, tid);
+                    w.issue(0, r0);
+                    tile = next;
+                    continue;
+                }
+            }
+            break;
         }
-        if (st < w.nst)
-            w.step(st, r0, r1);
     } else if constexpr (C::NS == 3) {
         w.issue(1, r1);
         for (; st + 3 <= w.nst; st += 3) {
@@ -410,15 +475,17 @@ struct ColVariant {
     const char *name;
     const void *f[2];  // fp16 and bf16 operands
     int kw, bm, bn, nrmax, bt, nt;
+    bool persist_ok;   // may walk several tiles per workgroup
 };
 
-template <int KW, int BT, int WM, int WN, int WGM, int WGN, int NRMAX, int NS, bool SERIAL = false>
+template <int KW, int BT, int WM, int WN, int WGM, int WGN, int NRMAX, int NS, bool SERIAL = false,
+          bool PERSIST = true>
 ColVariant col_variant(const char *name)
 {
-    using B = ColCfg<KW, BT, WM, WN, WGM, WGN, NRMAX, NS>;
+    using B = ColCfg<KW, BT, WM, WN, WGM, WGN, NRMAX, NS, PERSIST>;
     using C = typename std::conditional<SERIAL, Serialized<B>, B>::type;
     return ColVariant{name, {(const void *)&conv_fp16_col<C, F16Op>, (const void *)&conv_fp16_col<C, BF16Op>}, KW,
-                      C::BM, C::BN, NRMAX, BT, C::NT};
+                      C::BM, C::BN, NRMAX, BT, C::NT, col_persist_ok<C>()};
 }
 
 const ColVariant *col_variants(int *n)
@@ -429,7 +496,9 @@ const ColVariant *col_variants(int *n)
         col_variant<3, 32, 1, 2, 2, 2, 160, 2>("k3c64p128t32s2"),
         col_variant<3, 16, 2, 4, 2, 2, 288, 3>("k3c128p256t16s3"),
         col_variant<7, 16, 2, 2, 1, 4, 544, 3>("k7c64p256t16s3"),
-        col_variant<7, 16, 1, 2, 2, 2, 288, 2>("k7c64p128t16s2"),
+        // (without the persistent loop: at three waves per SIMD its
+        // registers would spill)
+        col_variant<7, 16, 1, 2, 2, 2, 288, 2, false, false>("k7c64p128t16s2"),
         // eight waves, 256 x 256 tiles (large C_o)
         col_variant<3, 32, 4, 2, 2, 4, 320, 2>("k3c256p256t32s2w8"),
         col_variant<3, 32, 2, 3, 4, 2, 256, 2>("k3c256p192t32s2w8"),
@@ -588,8 +657,32 @@ hipError_t launch_conv_fp16_col(const Shape &sh, int plan, const Tuning &t, cons
     if (gx * gy > 0x7fffffff)
         return hipErrorInvalidValue;
     a.tg = make_tilegrid(gx, gy, t.tile_linear);
+    a.ntiles = (uint32_t)(gx * gy);
+    a.persist = 0;
+    uint32_t grid = a.ntiles;
+    const void *f = v.f[op == Op16::BF16];
+    // Persistent launch (one round of resident workgroups walking the
+    // tiles) where the variant allows it, the stage count is even (the last
+    // stage then sits in slot 1), the output rows are 16-byte aligned and the
+    // tile's output rows fit 31-bit offsets; unless IM2WIN_FP16_PERSIST=off.
+    if (v.persist_ok && t.col_persist && (sh.Tp / v.bt) % 2 == 0 && sh.Co % 8 == 0 &&
+        (int64_t)v.bn * sh.Co * 2 < (int64_t)kMaxRecords) {
+        int dev = 0, cus = 0, per_cu = 0;
+        hipError_t e = hipGetDevice(&dev);
+        if (e == hipSuccess)
+            e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e == hipSuccess)
+            e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, f, v.nt, 0);
+        if (e != hipSuccess)
+            return e;
+        const int64_t g = (int64_t)(cus > 0 ? cus : 1) * (per_cu > 0 ? per_cu : 1);
+        if (g < (int64_t)a.ntiles) {
+            a.persist = 1;
+            grid = (uint32_t)g;
+        }
+    }
     void *args[] = {&a};
-    return hipLaunchKernel(v.f[op == Op16::BF16], dim3((uint32_t)(gx * gy)), dim3(v.nt), args, 0, st);
+    return hipLaunchKernel(f, dim3(grid), dim3(v.nt), args, 0, st);
 }
 
 }  // namespace im2win

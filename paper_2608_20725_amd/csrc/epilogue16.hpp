@@ -83,4 +83,78 @@ __device__ inline void store_tile_lds(const f32x16_acc (&acc)[WM][WN], char *lds
     }
 }
 
+// The same epilogue in two halves, for a workgroup that goes on to another
+// tile: C_o a multiple of 8 (16-byte output pieces) and the tile's pieces
+// dealt evenly to the threads.  Its barriers wait for LDS operations only
+// (__syncthreads would also wait for loads in flight), and every thread
+// issues the same epilogue16_stores() buffer stores, those past the last
+// pixel or channel at out-of-range offsets that store nothing.
+// Slot of 16-byte chunk k of pixel row px (CHR chunks per row): the 16 lanes
+// that write one channel group of 16 consecutive rows, and the lanes that
+// read one row, touch 16 different 16-byte slots of the 64 banks.
+template <int CHR>
+__device__ inline uint32_t epilogue16_swizzle(uint32_t px)
+{
+    return CHR >= 16 ? (px & 15u) : CHR == 8 ? ((px ^ (px >> 3)) & 7u) : ((px ^ (px >> 2)) & 3u);
+}
+
+template <int BM, int BN, int NT>
+constexpr int epilogue16_stores()
+{
+    return BN * (2 * BM / 16) / NT;
+}
+
+// First half: the workgroup's rounded sums into LDS as [pixel][channel].
+template <class E, int WM, int WN, int WGM, int WGN>
+__device__ inline void stage_tile_lds_ring(const f32x16_acc (&acc)[WM][WN], char *lds, uint32_t wm, uint32_t wn,
+                                           uint32_t lane)
+{
+    constexpr int BM = 32 * WM * WGM;
+    constexpr int RB = 2 * BM;    // bytes per pixel row
+    constexpr int CHR = RB / 16;  // 16-byte chunks per row
+    static_assert(CHR >= 4, "at least 32 channels per tile");
+    ring_barrier();
+#pragma unroll
+    for (int j = 0; j < WN; ++j) {
+        const uint32_t px = wn * 32 * WN + 32 * j + (lane & 31);
+#pragma unroll
+        for (int i = 0; i < WM; ++i) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const uint32_t ch = wm * 32 * WM + 32 * i + 8 * g + 4 * (lane >> 5);
+                uint32_t h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    h[e] = E::bits(acc[i][j][4 * g + e]);
+                const uint32_t k = ch / 8;
+                *reinterpret_cast<uint2 *>(lds + px * RB + 16 * (k ^ epilogue16_swizzle<CHR>(px)) + 2 * (ch % 8)) =
+                    make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+            }
+        }
+    }
+    ring_barrier();
+}
+
+// Second half: the tile from LDS to the output, exactly
+// epilogue16_stores<BM, BN, NT>() buffer stores per thread.
+template <int BM, int BN, int NT>
+__device__ inline void copy_tile_out_ring(const char *lds, uint16_t *out, uint32_t P, uint32_t Co, uint32_t p0,
+                                          uint32_t ch0, uint32_t tid)
+{
+    constexpr int RB = 2 * BM;
+    constexpr int CHR = RB / 16;
+    static_assert((BN * CHR) % NT == 0, "whole pieces per thread");
+    // rows from pixel p0 on; pixels past P fall outside the resource
+    const uint32_t rows = P - p0 < (uint32_t)BN ? P - p0 : (uint32_t)BN;
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + (uint64_t)p0 * Co, rows * Co * 2u);
+#pragma unroll
+    for (int n = 0; n < epilogue16_stores<BM, BN, NT>(); ++n) {
+        const uint32_t c = tid + (uint32_t)NT * n;
+        const uint32_t px = c / CHR, k = c % CHR;
+        const uint32_t ch = ch0 + 8 * k;
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(lds + px * RB + 16 * (k ^ epilogue16_swizzle<CHR>(px)));
+        __builtin_amdgcn_raw_buffer_store_b128(v, ro, ch < Co ? (px * Co + ch) * 2u : kOOB, 0, 0);
+    }
+}
+
 }  // namespace im2win

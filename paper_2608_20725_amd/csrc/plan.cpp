@@ -74,6 +74,13 @@ int read_tuning(Tuning *t)
     if ((rc = read_order("IM2WIN_TRANSFORM_ORDER", "xcd", &t->transform_linear)) != IM2WIN_OK ||
         (rc = read_order("IM2WIN_TILE_ORDER", "xcd", &t->tile_linear)) != IM2WIN_OK)
         return rc;
+    t->col_persist = true;
+    if (const char *e = getenv("IM2WIN_FP16_PERSIST")) {
+        if (strcmp(e, "off") == 0)
+            t->col_persist = false;
+        else if (*e && strcmp(e, "on") != 0)
+            return IM2WIN_EINVAL;
+    }
     t->transform_gather = false;
     if (const char *e = getenv("IM2WIN_TRANSFORM_KERNEL")) {
         if (strcmp(e, "gather") == 0)
@@ -119,6 +126,7 @@ Tuning default_tuning()
     t.fp32_kernel = t.fp32_tile = t.fp32_mfma_tile = t.fp32_cols = -1;
     t.transform_linear = t.tile_linear = false;
     t.transform_gather = false;
+    t.col_persist = true;
     t.tap_order = Tuning::kDefault;
     t.fp16_split = 0;
     return t;

@@ -290,6 +290,37 @@ def test_ring_matches_serialized_ring(case, monkeypatch):
     assert torch.equal(outs[0].view(bits), outs[1].view(bits))
 
 
+# Persistent launch of the column-staged kernel (one round of workgroups
+# walking the tiles) against one workgroup per tile: the same sums in the
+# same order per tile, so bit-identical outputs.  Shapes with more tiles than
+# one round holds, so that the persistent loop runs; the oracle checks one.
+PERSIST_CASES = [
+    ("k3c64p128t32s2", (64, 64, 56, 56, 64, 3, 3, 1), torch.float16),
+    ("k3c64p256t32s2", (16, 64, 112, 112, 128, 3, 3, 1), torch.float16),
+    ("k7c64p256t32s2", (8, 64, 224, 224, 64, 7, 7, 2), torch.bfloat16),
+    ("k3c256p192t32s2w8", (256, 512, 14, 14, 512, 3, 3, 1), torch.float16),
+]
+
+
+@pytest.mark.parametrize("case", PERSIST_CASES, ids=lambda c: c[0])
+def test_persistent_column_launch_same_bits(case, monkeypatch):
+    name, shape, dtype = case
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=61)
+    monkeypatch.setenv("IM2WIN_FP16_COL", name)
+    outs = []
+    for mode in ("on", "off"):
+        monkeypatch.setenv("IM2WIN_FP16_PERSIST", mode)
+        say("persist", mode, name, shape, dtype)
+        assert_kernel(shape, dtype, "IM2WIN_FP16_COL", name)
+        run = Run(x, w, s, dtype)
+        if not outs:
+            check_sampled(run, x, w, seed=5)
+        run.check_out_guards()
+        outs.append(run.out.clone())
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+
+
 # The K-loop tap order (IM2WIN_TAP_ORDER): linear, or column slices of one
 # tap range in turn.  Both are fixed orders that the oracle bounds; the
 # DMA-staged fp32 kernel (column by default) and the register-staged one

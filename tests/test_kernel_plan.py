@@ -13,7 +13,8 @@ from paper_2608_20725_amd import workloads
 EINVAL = -1
 VARS = ("IM2WIN_FP16_KERNEL", "IM2WIN_FP16_COL", "IM2WIN_FP16_TILE", "IM2WIN_FP16_SEG", "IM2WIN_FP32_KERNEL",
         "IM2WIN_FP32_TILE", "IM2WIN_FP32_MFMA_TILE", "IM2WIN_TRANSFORM_ORDER", "IM2WIN_TILE_ORDER",
-        "IM2WIN_TAP_ORDER", "IM2WIN_FP16_SPLIT", "IM2WIN_FP32_COLS", "IM2WIN_TRANSFORM_KERNEL")
+        "IM2WIN_TAP_ORDER", "IM2WIN_FP16_SPLIT", "IM2WIN_FP32_COLS", "IM2WIN_TRANSFORM_KERNEL",
+        "IM2WIN_FP16_PERSIST")
 
 
 @pytest.fixture(autouse=True)
@@ -143,6 +144,14 @@ def test_transform_kernel_names(monkeypatch):
         assert name((1, 3, 32, 32, 16, 3, 3, 1), "f16")
     monkeypatch.setenv("IM2WIN_TRANSFORM_KERNEL", "vec")
     assert status((1, 3, 32, 32, 16, 3, 3, 1), "f16") == EINVAL
+
+
+def test_persist_switch_names(monkeypatch):
+    for v in ("on", "off", ""):
+        monkeypatch.setenv("IM2WIN_FP16_PERSIST", v)
+        assert name((1, 64, 10, 10, 64, 3, 3, 1), "f16")
+    monkeypatch.setenv("IM2WIN_FP16_PERSIST", "yes")
+    assert status((1, 64, 10, 10, 64, 3, 3, 1), "f16") == EINVAL
 
 
 # The mini-batch path makes its plan for a full chunk and runs it on the
