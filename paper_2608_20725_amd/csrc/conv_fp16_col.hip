@@ -494,6 +494,7 @@ const ColVariant *col_variants(int *n)
     static const ColVariant v[] = {
         col_variant<3, 32, 2, 2, 1, 4, 288, 2>("k3c64p256t32s2"),
         col_variant<3, 32, 1, 2, 2, 2, 160, 2>("k3c64p128t32s2"),
+        col_variant<3, 32, 2, 2, 2, 2, 160, 2>("k3c128p128t32s2"),
         col_variant<3, 16, 2, 4, 2, 2, 288, 3>("k3c128p256t16s3"),
         col_variant<7, 16, 2, 2, 1, 4, 544, 3>("k7c64p256t16s3"),
         // (without the persistent loop: at three waves per SIMD its
@@ -595,8 +596,11 @@ int col_default(const Shape &sh)
     // TFLOP/s same-process; with C_o = 128, 3x3 at 28x28, 531 vs 548)
     if (sh.Kw == 3 && sh.Co <= 64)
         name = "k3c64p128t32s2";
+    // 64 < C_o <= 128: one 128 x 128 tile reads each window once where two
+    // 64-channel tiles read it twice (3x3 64 -> 128 at 112x112: 771 vs 714
+    // TFLOP/s; 128 -> 128 at 28x28: 646 vs 603-639)
     else if (sh.Kw == 3 && sh.Co <= 128)
-        name = "k3c64p256t32s2";
+        name = "k3c128p128t32s2";
     // 7x7: with stride 1 and C_o <= 64 the 64 x 128 tile (two-slot ring,
     // 49 KiB, three workgroups per CU) measured 785 vs 713 TFLOP/s
     // (7x7 C=64 at 60x60, 64 images); with stride 2 (7x7 C=64 at 224x224)

@@ -204,7 +204,7 @@ VARIANT_CASES = [
     ("IM2WIN_FP16_KERNEL", ["pipe", "regs"], (2, 16, 13, 13, 72, 5, 5, 1), torch.float16, True),
     ("IM2WIN_FP16_KERNEL", ["pipe", "regs"], (1, 64, 20, 20, 300, 3, 3, 1), torch.float16, True),
     ("IM2WIN_FP16_COL", ["k3c64p256t32s2", "k3c64p128t32s2", "k3c128p256t16s3", "k3c256p256t32s2w8",
-                         "k3c256p192t32s2w8"],
+                         "k3c256p192t32s2w8", "k3c128p128t32s2"],
      (2, 64, 24, 24, 300, 3, 3, 1), torch.float16, False),
     # the 7x7 column-staged tiles (filter width 7, stride 1 and 2)
     ("IM2WIN_FP16_COL", ["k7c64p256t16s3", "k7c64p128t16s2", "k7c64p256t32s2"],
@@ -297,6 +297,7 @@ def test_ring_matches_serialized_ring(case, monkeypatch):
 PERSIST_CASES = [
     ("k3c64p128t32s2", (64, 64, 56, 56, 64, 3, 3, 1), torch.float16),
     ("k3c64p256t32s2", (16, 64, 112, 112, 128, 3, 3, 1), torch.float16),
+    ("k3c128p128t32s2", (16, 64, 112, 112, 128, 3, 3, 1), torch.bfloat16),
     ("k7c64p256t32s2", (8, 64, 224, 224, 64, 7, 7, 2), torch.bfloat16),
     ("k3c256p192t32s2w8", (256, 512, 14, 14, 512, 3, 3, 1), torch.float16),
 ]
