@@ -84,22 +84,26 @@ struct WinCols {
 // Order of a kernel's K loop.  A kernel walks its taps in blocks of G (a
 // stage, or part of one); linear order takes block b as taps b*G .. b*G+G-1.
 // Column order (nv filter columns of T = K_h*C_i taps each, T a multiple of
-// G) takes block b as taps v*T + tb*G .. of filter column v = b % nv, with
-// tb = b / nv: the nv column slices of one tap range follow each other.
-// Neighbouring windows share input columns (a column is slice v of one
-// window and slice v + s of the previous one), so in column order the bytes
-// one tile reads for slice v come back for slice v + s a few blocks later,
-// while they are still in L2, instead of s*T/G blocks later.  Each output
-// is still one fixed sequence of taps, so results stay deterministic.
+// G) takes block b as taps v*T + tb*G .. of the (b % nv)-th filter column of
+// the list `cols`, with tb = b / nv: the nv column slices of one tap range
+// follow each other.  Neighbouring windows share input columns (a column is
+// slice v of one window and slice v + s of the previous one), so in column
+// order the bytes one tile reads for slice v come back for slice v + s a
+// few blocks later, while they are still in L2, instead of s*T/G blocks
+// later.  The list takes the columns by residue mod s (0, s, 2s, .., then
+// 1, 1 + s, ..), so slice v + s is the very next block.  Each output is
+// still one fixed sequence of taps, so results stay deterministic.
 struct TapOrder {
     uint32_t nv, T, G;  // nv = 1: linear
+    uint64_t cols;      // column of the j-th column slice of a tap block: bits 4j .. 4j+3
 
     __host__ __device__ inline uint32_t map(uint32_t k) const
     {
         if (nv == 1)
             return k;
         const uint32_t b = k / G, off = k - b * G;
-        const uint32_t tb = b / nv, v = b - tb * nv;
+        const uint32_t tb = b / nv, j = b - tb * nv;
+        const uint32_t v = (uint32_t)(cols >> (4 * j)) & 15u;
         return v * T + tb * G + off;
     }
 };
@@ -144,12 +148,20 @@ constexpr uint32_t kTapBlock32 = 32;
 
 // Column order for blocks of G taps when the layer allows it (K_w > 1,
 // K_h*C_i a multiple of G) and `linear` is not set; else linear order.
-inline TapOrder make_taporder(int64_t Kw, int64_t Kh, int64_t Ci, uint32_t G, bool linear)
+inline TapOrder make_taporder(int64_t Kw, int64_t Kh, int64_t Ci, uint32_t G, bool linear, int64_t s = 1)
 {
     const int64_t T = Kh * Ci;
-    if (linear || Kw <= 1 || T % G != 0)
-        return TapOrder{1u, (uint32_t)T, G};
-    return TapOrder{(uint32_t)Kw, (uint32_t)T, G};
+    if (linear || Kw <= 1 || Kw > 16 || T % G != 0)
+        return TapOrder{1u, (uint32_t)T, G, 0};
+    // columns grouped by residue mod s, ascending within a group: the slice
+    // after column v is column v + s, which holds the taps the next pixel
+    // read in column v (s = 1 or s >= K_w: plain column order)
+    uint64_t cols = 0;
+    int j = 0;
+    for (int64_t r = 0; r < s && r < Kw; ++r)
+        for (int64_t v = r; v < Kw; v += s)
+            cols |= (uint64_t)v << (4 * j++);
+    return TapOrder{(uint32_t)Kw, (uint32_t)T, G, cols};
 }
 
 inline WinCols make_wincols(const Shape &sh)

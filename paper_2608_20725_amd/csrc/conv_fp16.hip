@@ -920,7 +920,8 @@ hipError_t launch_conv_fp16(const Shape &sh, const Plan16 &p, const Tuning &t, c
     // order measured from +3 % (3x3 64 -> 128 at 112x112) to -10 % (3x3
     // 256 -> 512 at 12x12), where the filter tiles' L2 reuse suffers.  The
     // register-staged kernel always walks its taps in linear order.
-    a.to = make_taporder(sh.Kw, sh.Kh, sh.Ci, (uint32_t)BK, t.tap_order != Tuning::kColumn || p.fam != Fam16::Pipe);
+    a.to = make_taporder(sh.Kw, sh.Kh, sh.Ci, (uint32_t)BK, t.tap_order != Tuning::kColumn || p.fam != Fam16::Pipe,
+                         sh.s);
     void *args[] = {&a};
     const uint32_t nst = (uint32_t)(sh.K_pad / BK);
     a.ks = 1; a.spl = nst; a.part = nullptr;

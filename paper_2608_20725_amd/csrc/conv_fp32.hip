@@ -546,7 +546,7 @@ hipError_t launch_conv_fp32(const Shape &sh, const Plan32 &p, const Tuning &t, c
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     // the DMA-staged kernel's tap order (16-tap blocks), so both sum every
     // output in the same order
-    a.to = make_taporder(sh.Kw, sh.Kh, sh.Ci, kTapBlock32, t.tap_order == Tuning::kLinear);
+    a.to = make_taporder(sh.Kw, sh.Kh, sh.Ci, kTapBlock32, t.tap_order == Tuning::kLinear, sh.s);
 
     const Tile &tile = kTiles[p.v];
     // Channel groups per workgroup: the largest of 8, 4, 2, 1 waves (TN

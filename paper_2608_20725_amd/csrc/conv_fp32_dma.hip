@@ -543,9 +543,10 @@ hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const Tuning &t, cons
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     // column tap order unless IM2WIN_TAP_ORDER=linear (7x7 stride 2 C=64 at
     // 224x224: 87.2 vs 84.6 TFLOP/s; 3x3 C=64 at 56x56: 76.4 vs 72.1; other
-    // layers within +-2 %)
+    // layers within +-2 %), its columns grouped by residue mod the stride
+    // (7x7 stride 2: 87.3 vs 83.9 with the columns in plain order)
     a.to = make_taporder(sh.Kw, sh.Kh, sh.Ci, kTapBlock32 > (uint32_t)v.kt ? kTapBlock32 : (uint32_t)v.kt,
-                         t.tap_order == Tuning::kLinear);
+                         t.tap_order == Tuning::kLinear, sh.s);
     const int64_t gx = (sh.P + v.bm - 1) / v.bm, gy = (sh.Co + v.cw - 1) / v.cw;
     if (gx * gy > 0x7fffffff)
         return hipErrorInvalidValue;

@@ -323,13 +323,16 @@ def test_persistent_column_launch_same_bits(case, monkeypatch):
 
 
 # The K-loop tap order (IM2WIN_TAP_ORDER): linear, or column slices of one
-# tap range in turn.  Both are fixed orders that the oracle bounds; the
+# tap range in turn (columns grouped by residue mod the stride).  Both are fixed orders that the oracle bounds; the
 # DMA-staged fp32 kernel (column by default) and the register-staged one
 # follow the same order, so they agree bit for bit in either.
 TAP_CASES = [
     # (shape, dtype, forced variables)
     ((2, 16, 17, 19, 100, 3, 3, 1), torch.float32, {"IM2WIN_FP32_KERNEL": "p8c8l8s2k16"}),
     ((2, 16, 23, 41, 40, 7, 7, 2), torch.float32, {"IM2WIN_FP32_KERNEL": "p4c12l8s2k16"}),
+    # stride 2, K_h*C_i a multiple of 32: columns 0, 2, 4, 6, 1, 3, 5 in turn
+    ((2, 32, 23, 41, 40, 7, 7, 2), torch.float32, {"IM2WIN_FP32_KERNEL": "p8c8l8s2k16"}),
+    ((2, 64, 23, 41, 72, 5, 5, 2), torch.float16, {"IM2WIN_FP16_KERNEL": "pipe"}),
     ((2, 64, 14, 14, 200, 3, 3, 1), torch.float32, {"IM2WIN_FP32_KERNEL": "p4c8l8s2k16t4"}),
     ((2, 64, 20, 20, 96, 3, 3, 1), torch.float16, {"IM2WIN_FP16_KERNEL": "pipe"}),
     ((2, 64, 20, 20, 200, 5, 5, 2), torch.bfloat16, {"IM2WIN_FP16_TILE": "c128p128s1"}),
