@@ -65,10 +65,10 @@ KERNEL_SOURCES = ("common.hpp", "epilogue16.hpp", "mfma16.hpp", "conv_fp32_dma.h
                   "conv_fp32_stem.hip", "conv_fp16.hip", "conv_fp16_col.hip", "conv_fp16_seg.hip",
                   "conv_fp16_stem.hip")
 CONV_TRAFFIC = {
-    "source_sha256": "049c1067e3c98823edec89308096de324f0a831b7b6514a27931be8ed5ae23a8",
+    "source_sha256": "c0e86fd608728b85ff51d856609540f5d0f4c603ecfd2eeaa4579f5cacf9351e",
     "workload": "sweep",
-    "f32": 31948151765,    # bytes per step, fetched + written
-    "f16": 6494084068,
+    "f32": 20401076179,    # bytes per step, fetched + written
+    "f16": 6487754523,
 }
 
 
