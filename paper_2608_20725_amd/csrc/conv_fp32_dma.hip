@@ -511,9 +511,15 @@ int dma32_default(const Shape &sh)
     // unaligned windows (C_i % 4 != 0, the 3-channel stems): the 6-pixel
     // lane tile, 7x7 C_i=3 stride 2 67.2 vs 64.1 TFLOP/s (8-pixel) and 3x3
     // C_i=3 36.6 vs 34.4, same machine
+    // strided overlapping windows (K_w > s > 1) re-read more of their
+    // columns from L2 and run better with the 6-pixel tile's five workgroups
+    // per CU: 7x7 C=64 stride 2 at 224x224, 95.0 vs 92.7 TFLOP/s in the
+    // benchmark step (3x3 C=64 -> 128 stride 1 at 112x112: 94.8 vs 97.7)
+    const bool strided = sh.s > 1 && sh.Kw > sh.s;
     const char *name = !aligned          ? "p6c8l8s2k16g4"
                        : tiles256 <= 128  ? "p8c8l8s2k16t4"
                        : tiles256 <= 1024 ? "p4c8l8s2k16t4"
+                       : strided          ? "p6c8l8s2k16"
                                           : "p8c8l8s2k16";
     // 96-channel tiles where they pad fewer channels than 64-channel ones
     // (C_o = 96: 0 against 32 of 128) and still give four workgroups per CU:

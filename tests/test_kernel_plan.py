@@ -239,6 +239,16 @@ def test_stem32_default(shape, want):
     assert name(shape, "f32").startswith(want)
 
 
+@pytest.mark.parametrize("shape,want", [
+    ((128, 64, 224, 224, 64, 7, 7, 2), "conv_fp32_dma p6c8l8s2k16"),    # K_w > s > 1: the 6-pixel tile
+    ((128, 64, 112, 112, 128, 3, 3, 1), "conv_fp32_dma p8c8l8s2k16"),   # stride 1
+    ((128, 64, 224, 224, 64, 2, 2, 2), "conv_fp32_dma p8c8l8s2k16"),    # K_w = s: no overlap
+    ((2, 16, 23, 41, 40, 7, 7, 2), "conv_fp32_dma p8c8l8s2k16t4"),      # few tiles
+])
+def test_dma32_default(shape, want):
+    assert name(shape, "f32") == want
+
+
 def test_stem32_forced(monkeypatch):
     monkeypatch.setenv("IM2WIN_FP32_KERNEL", "stem")
     assert name((2, 5, 30, 30, 64, 2, 3, 1), "f32") == "conv_fp32_stem k32"
