@@ -39,6 +39,7 @@ struct StemArgs {
     const uint16_t *packed;  // F' in 64-tap tiles: [K_pad/64][Co_pad][64]
     uint16_t *out;
     uint32_t P, K, Co, Co_pad, Wo, nblk;
+    uint32_t streamed;       // 1: output stores streamed (nontemporal)
     uint64_t L, S;           // strip length and window step (elements)
     FastDiv div_Wo;
 };
@@ -126,12 +127,16 @@ struct StemBlock {
         const uint32_t nch = a.Co / 8;  // 16-byte chunks per output row
         const uint32_t c = lane % NCHP, r0 = lane / NCHP;
         char *dst = reinterpret_cast<char *>(a.out + (uint64_t)blk * 32 * a.Co);
+        const __amdgpu_buffer_rsrc_t ro = make_rsrc(dst, live * a.Co * 2u);
 #pragma unroll
         for (int k = 0; k < 32 / RP; ++k) {
             const uint32_t r = r0 + RP * k;
             if (r < live && c < nch) {
-                *reinterpret_cast<u32x4 *>(dst + r * 2 * a.Co + 16 * c) =
-                    *reinterpret_cast<const u32x4 *>(lds + r * PITCH + 16 * (c ^ (r % NCHP)));
+                const u32x4 v = *reinterpret_cast<const u32x4 *>(lds + r * PITCH + 16 * (c ^ (r % NCHP)));
+                if (a.streamed)
+                    store16_nt(v, ro, r * 2 * a.Co + 16 * c);
+                else
+                    *reinterpret_cast<u32x4 *>(dst + r * 2 * a.Co + 16 * c) = v;
             }
         }
         // every lane has read its chunks before the next block's rows land
@@ -263,6 +268,7 @@ hipError_t launch_conv_fp16_stem(const Shape &sh, int plan, const void *ws, cons
     a.P = (uint32_t)sh.P; a.K = (uint32_t)sh.K; a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad;
     a.Wo = (uint32_t)sh.Wo;
     a.nblk = (uint32_t)((sh.P + 31) / 32);
+    a.streamed = stream_out(sh.P * sh.Co * 2) ? 1u : 0u;
     a.L = (uint64_t)sh.L; a.S = (uint64_t)sh.S;
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
     // One round of resident workgroups (as many per CU as registers and LDS
