@@ -65,10 +65,10 @@ KERNEL_SOURCES = ("common.hpp", "epilogue16.hpp", "mfma16.hpp", "conv_fp32_dma.h
                   "conv_fp32_stem.hip", "conv_fp16.hip", "conv_fp16_col.hip", "conv_fp16_seg.hip",
                   "conv_fp16_stem.hip")
 CONV_TRAFFIC = {
-    "source_sha256": "c0e86fd608728b85ff51d856609540f5d0f4c603ecfd2eeaa4579f5cacf9351e",
+    "source_sha256": "03ea643022e06cbdb7a213f1afeeb20ccc75d9ef8d768bbe80da1f4aae55a30f",
     "workload": "sweep",
-    "f32": 20401076179,    # bytes per step, fetched + written
-    "f16": 6487754523,
+    "f32": 16504653055,    # bytes per step, fetched + written
+    "f16": 6499700442,
 }
 
 

@@ -188,20 +188,20 @@ constexpr uint32_t kOOB = 0x80000000u;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr uint32_t kMaxRecords = 0x7fffff00u;
 
-// Large outputs of the stem and DMA-staged kernels are stored with the
-// nontemporal cache policy: the output is written once and not read again
-// by the kernel, and when it is far larger than the caches the streamed
-// writes reach HBM sooner.  Measured in the benchmark step (128 images, same
-// box, alternating builds): the 3x3 3-channel fp16 stem over 224x224 (807 MB
-// of output) 104 -> 154 TFLOP/s, the 7x7 stride-2 3-channel fp32 layer
-// (404 MB) +2.7 %, the larger fp32 layers within +-0.5 %.  Not streamed:
+// Large outputs of the fp16 stem kernel are stored with the nontemporal
+// cache policy: the output is written once and not read again by the
+// kernel, and when it is far larger than the caches the streamed writes
+// reach HBM sooner.  Measured in the benchmark step (128 images, same box,
+// alternating builds): the 3x3 3-channel stem over 224x224 (807 MB of
+// output, whole 4 KiB blocks per wave) 104 -> 154 TFLOP/s.  Not streamed:
 // outputs under 128 MiB (convs writing 3-51 MB lost 7-17 % streamed: the
 // caches absorb them), the column-staged fp16 kernel (194-396 MB: -1 to
-// -1.6 %), and window tensors (the conv reads them next; streamed, the
-// transforms lost up to 11 %).  The streamed stores go through a buffer
-// resource with the nt policy operand: a plain store with a nontemporal
-// hint next to an unhinted one is folded into a single store by the
-// compiler, and the hint lost.
+// -1.6 %), the DMA-staged fp32 kernel (at most +2.7 %, and its 32-byte row
+// pieces, streamed past L2, reached HBM as up to 2.3x the bytes), and window
+// tensors (the conv reads them next; streamed, the transforms lost up to
+// 11 %).  The streamed stores go through a buffer resource with the nt
+// policy operand: a plain store with a nontemporal hint next to an unhinted
+// one is folded into a single store by the compiler, and the hint lost.
 constexpr int kStoreNT = 2;
 constexpr int64_t kStreamOutBytes = (int64_t)128 << 20;
 inline bool stream_out(int64_t out_bytes) { return out_bytes >= kStreamOutBytes; }

@@ -49,7 +49,6 @@ struct D32Args {
     TileGrid tg;             // pixel x channel tiles of the 1-D launch
     FastDiv div_Wo;
     TapOrder to;             // order of the stages' tap blocks (blocks of KT taps)
-    uint32_t streamed;       // 1: output stores streamed (nontemporal)
 };
 
 // Lane tile TM pixels x TN channels; LC lanes of a wave share pixels and
@@ -325,17 +324,6 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
 
     // first channel of this lane, and its first pixel
     const uint32_t jw = jb + (w.wch() * C::LC + w.lane % C::LC) * C::TN;
-    // the workgroup's output rows, for the streamed stores (byte offsets
-    // below 2^31: the launcher streams only then)
-    const uint32_t rows = a.P - p0 < (uint32_t)C::BM ? a.P - p0 : (uint32_t)C::BM;
-    const __amdgpu_buffer_rsrc_t ro = make_rsrc(a.out + (uint64_t)p0 * a.Co, rows * a.Co * 4u);
-    auto put4 = [&](uint32_t p, uint32_t c, float x0, float x1, float x2, float x3) {
-        if (a.streamed)
-            store16_nt(u32x4{__float_as_uint(x0), __float_as_uint(x1), __float_as_uint(x2), __float_as_uint(x3)}, ro,
-                       ((p - p0) * a.Co + jw + c) * 4u);
-        else
-            *reinterpret_cast<float4 *>(a.out + (uint64_t)p * a.Co + jw + c) = make_float4(x0, x1, x2, x3);
-    };
     const uint32_t pl0 = w.wpx() * C::WBM + w.lane / C::LC;
     if constexpr (C::KS > 1) {
         // Every wave stores its sums in LDS; then the KS waves with the same
@@ -389,7 +377,7 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
             if (jw + C::TN <= a.Co && (a.Co & 3) == 0) {
 #pragma unroll
                 for (int c = 0; c < C::TN; c += 4)
-                    put4(p, c, v[c], v[c + 1], v[c + 2], v[c + 3]);
+                    *reinterpret_cast<float4 *>(o + c) = make_float4(v[c], v[c + 1], v[c + 2], v[c + 3]);
             } else {
 #pragma unroll
                 for (int c = 0; c < C::TN; ++c)
@@ -411,7 +399,8 @@ __global__ __launch_bounds__(C::NT) void conv_fp32_dma(D32Args a)
         if (jw + C::TN <= a.Co && (a.Co & 3) == 0) {
 #pragma unroll
             for (int c = 0; c < C::TN; c += 4)
-                put4(p, c, w.acc[t][c], w.acc[t][c + 1], w.acc[t][c + 2], w.acc[t][c + 3]);
+                *reinterpret_cast<float4 *>(o + c) =
+                    make_float4(w.acc[t][c], w.acc[t][c + 1], w.acc[t][c + 2], w.acc[t][c + 3]);
         } else {
 #pragma unroll
             for (int c = 0; c < C::TN; ++c)
@@ -558,7 +547,6 @@ hipError_t launch_conv_fp32_dma(const Shape &sh, int plan, const Tuning &t, cons
     a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)sh.Co_pad32;
     a.Wo = (uint32_t)sh.Wo; a.L = (uint32_t)sh.L; a.wc = make_wincols(sh);
     a.div_Wo = make_fastdiv((uint32_t)sh.Wo);
-    a.streamed = stream_out(sh.P * sh.Co * 4) && (int64_t)v.bm * sh.Co * 4 < (int64_t)kMaxRecords ? 1u : 0u;
     // column tap order unless IM2WIN_TAP_ORDER=linear (7x7 stride 2 C=64 at
     // 224x224: 87.2 vs 84.6 TFLOP/s; 3x3 C=64 at 56x56: 76.4 vs 72.1; other
     // layers within +-2 %), its columns grouped by residue mod the stride
