@@ -65,7 +65,7 @@ KERNEL_SOURCES = ("common.hpp", "epilogue16.hpp", "mfma16.hpp", "conv_fp32_dma.h
                   "conv_fp32_stem.hip", "conv_fp16.hip", "conv_fp16_col.hip", "conv_fp16_seg.hip",
                   "conv_fp16_stem.hip")
 CONV_TRAFFIC = {
-    "source_sha256": "03ea643022e06cbdb7a213f1afeeb20ccc75d9ef8d768bbe80da1f4aae55a30f",
+    "source_sha256": "108fd128b5532e1ee6e806ae4df1414bf04a6114d273f86e0bf4a1f47df41897",
     "workload": "sweep",
     "f32": 16504653055,    # bytes per step, fetched + written
     "f16": 6499700442,

@@ -21,7 +21,8 @@
 //   * the 32 pixels' output rows are contiguous in the NHWC output, so the
 //     wave turns its sums (rounded to 16 bits once, nearest-even) into rows
 //     in a private LDS area and copies the 32*C_o*2 bytes out with 16-byte
-//     stores, 1 KiB per store instruction;
+//     stores, 1 KiB per store instruction (with the nontemporal policy when
+//     the whole output is large; see kStreamOutBytes);
 //   * waves stride over the 32-pixel blocks of the layer; the window loads of
 //     the next block are issued before the current block's multiplies and
 //     stores.
