@@ -58,6 +58,26 @@ def test_stem_against_oracle_and_segment_kernel(shape, dtype, monkeypatch):
     assert torch.equal(mine.view(torch.int16), other.out.view(torch.int16))
 
 
+# An output of 128 MiB or more leaves through streamed (nontemporal) buffer
+# stores: every output against the oracle, the guard bytes after it, and the
+# same bits as the segment-staged kernel's cached stores; 1,172,184 pixels,
+# so the last 32-pixel block is ragged.
+def test_stem_streamed_output(monkeypatch):
+    shape = (24, 3, 223, 223, 64, 3, 3, 1)
+    N, Ci, H, W, Co, Kh, Kw, s = shape
+    assert N * (H - Kh + 1) * (W - Kw + 1) * Co * 2 >= 128 << 20
+    say("stem streamed", shape)
+    x, w = workloads.draw(N, Ci, H, W, Co, Kh, Kw, seed=37)
+    assert_kernel(shape, "f16", "IM2WIN_FP16_KERNEL", "stem")
+    run = Run(x, w, s, torch.float16)
+    check_full(run, x, w)
+    run.check_out_guards()
+    mine = run.out.clone()
+    monkeypatch.setenv("IM2WIN_FP16_SEG", "s64p256")
+    other = Run(x, w, s, torch.float16)
+    assert torch.equal(mine.view(torch.int16), other.out.view(torch.int16))
+
+
 @pytest.mark.parametrize("shape", [(2, 3, 12, 40, 64, 3, 3, 1), (2, 3, 15, 33, 32, 5, 5, 2)], ids=_id)
 def test_stem_nonfinite_inputs_stay_in_their_windows(shape, monkeypatch):
     N, Ci, H, W, Co, Kh, Kw, s = shape
