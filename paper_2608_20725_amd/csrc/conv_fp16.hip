@@ -71,49 +71,76 @@ struct C16Args {
 //     stage depth;
 //   register-staged kernel: nv = 1, tlen = K, TB = tpad = K_pad, i.e. plain
 //     [C_o_pad][K_pad].
-// One thread per 16-byte granule, in output order.
+// A lane packs one 8 x 8 block: channels j0 .. j0+7 of 8 consecutive taps
+// t0 .. t0+7 of slice c.  It reads the 8 taps' filter rows 16 bytes at a
+// time (8 channels), the 8 lanes of a tap reading one 128-byte run of C_o,
+// transposes the block in registers, and writes 8 granules (one per
+// channel), the 8 lanes of a channel block writing one run of packed row.
+// Filters whose rows are not whole 16-byte pieces (C_o % 8, or a base not
+// 16-byte aligned) are read element by element.  TB and tpad are multiples
+// of 64, so a block never straddles a tile.
 struct PackArgs {
     const uint16_t *filt;
     uint16_t *packed;
-    uint64_t grans;
     uint32_t nv, tlen, tpad, tb, Co, Co_pad, Ci, Kh, Kw;
+    uint32_t ntg, njb;    // 8-tap groups per slice (tpad/8), 8-channel blocks (Co_pad/8)
+    uint32_t ntgw, njbw;  // waves along tap groups and channel blocks (8 of each per wave)
+    uint32_t units;       // nv * ntgw * njbw waves
+    uint32_t vec;         // rows are whole aligned 16-byte pieces
+    FastDiv div_khci, div_ci, div_tb;
 };
 
 __global__ __launch_bounds__(256) void pack_filter_fp16(PackArgs a)
 {
-    for (uint64_t g = (uint64_t)blockIdx.x * 256 + threadIdx.x; g < a.grans;
-         g += (uint64_t)gridDim.x * 256) {
-        const uint64_t e0 = g * 8;
-        const uint32_t r0 = (uint32_t)(e0 % a.tb);
-        const uint64_t q = e0 / a.tb;
-        const uint32_t j = (uint32_t)(q % a.Co_pad);
-        const uint64_t q2 = q / a.Co_pad;
-        const uint32_t c = (uint32_t)(q2 % a.nv);
-        const uint32_t t0 = (uint32_t)(q2 / a.nv) * a.tb + r0;
-        uint32_t w[4];
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t unit = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (unit >= a.units)
+        return;
+    const uint32_t jh = unit % a.njbw, rest = unit / a.njbw;
+    const uint32_t th = rest % a.ntgw, c = rest / a.ntgw;
+    const uint32_t tg = th * 8 + (lane & 7), jb = jh * 8 + (lane >> 3);
+    if (tg >= a.ntg || jb >= a.njb)
+        return;
+    const uint32_t t0 = tg * 8, j0 = jb * 8;
+    const uint32_t khci = a.Kh * a.Ci;
+    u32x4 x[8];
 #pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-            uint32_t lo = 0, hi = 0;
+    for (int e = 0; e < 8; ++e) {
+        const uint32_t t = t0 + e;
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (t < a.tlen && j0 < a.Co) {
+            // tap k of window order -> filter row (u, v, r) of [K_h][K_w][C_i]
+            const uint32_t k = c * a.tlen + t;
+            const uint32_t col = fdiv(k, a.div_khci), rem = k - col * khci;
+            const uint32_t u = fdiv(rem, a.div_ci), r = rem - u * a.Ci;
+            const uint16_t *src = a.filt + (((uint64_t)u * a.Kw + col) * a.Ci + r) * a.Co + j0;
+            if (a.vec && j0 + 8 <= a.Co) {
+                v = *reinterpret_cast<const u32x4 *>(src);
+            } else {
+                uint32_t h[8];
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const uint32_t t = t0 + e + h;
-                uint32_t bits = 0;
-                if (j < a.Co && t < a.tlen) {
-                    const uint32_t k = c * a.tlen + t;
-                    const uint32_t khci = a.Kh * a.Ci;
-                    const uint32_t v = k / khci, rem = k % khci;
-                    const uint32_t u = rem / a.Ci, r = rem % a.Ci;
-                    const uint64_t frow = ((uint64_t)u * a.Kw + v) * a.Ci + r;
-                    bits = a.filt[frow * a.Co + j];
-                }
-                if (h == 0)
-                    lo = bits;
-                else
-                    hi = bits;
+                for (int q = 0; q < 8; ++q)
+                    h[q] = j0 + q < a.Co ? src[q] : 0u;
+#pragma unroll
+                for (int d = 0; d < 4; ++d)
+                    v[d] = h[2 * d] | (h[2 * d + 1] << 16);
             }
-            w[e / 2] = lo | (hi << 16);
         }
-        *reinterpret_cast<uint4 *>(a.packed + g * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+        x[e] = v;
+    }
+    const uint32_t tt = fdiv(t0, a.div_tb), tr = t0 - tt * a.tb;
+    uint16_t *dst = a.packed + ((uint64_t)(tt * a.nv + c) * a.Co_pad + j0) * a.tb + tr;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        // channel j0+q: half q%2 of dword q/2 of each tap's piece
+        u32x4 o;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            const uint32_t lo = (x[2 * d][q / 2] >> (16 * (q % 2))) & 0xffffu;
+            const uint32_t hi = (x[2 * d + 1][q / 2] >> (16 * (q % 2))) & 0xffffu;
+            o[d] = lo | (hi << 16);
+        }
+        *reinterpret_cast<u32x4 *>(dst + (uint64_t)q * a.tb) = o;
     }
 }
 
@@ -886,12 +913,21 @@ hipError_t launch_pack_fp16(const Shape &sh, const Plan16 &p, const uint16_t *fi
     // channel count (a stage's filter rows are then one contiguous run);
     // the other kernels' tiles use C_o_pad = C_o rounded up to 256
     const int64_t rows = p.fam == Fam16::Col ? col_packed_rows(sh, p.v) : sh.Co_pad;
-    a.grans = (uint64_t)rows * a.nv * a.tpad / 8;
     a.Co = (uint32_t)sh.Co; a.Co_pad = (uint32_t)rows;
     a.Ci = (uint32_t)sh.Ci; a.Kh = (uint32_t)sh.Kh; a.Kw = (uint32_t)sh.Kw;
-    uint64_t blocks = (a.grans + 255) / 256;
-    if (blocks > 65536)
-        blocks = 65536;
+    if (a.tb % 8 != 0 || a.tpad % a.tb != 0 || rows % 8 != 0)
+        return hipErrorInvalidValue;
+    a.ntg = a.tpad / 8; a.njb = (uint32_t)(rows / 8);
+    a.ntgw = (a.ntg + 7) / 8; a.njbw = (a.njb + 7) / 8;
+    const uint64_t units = (uint64_t)a.nv * a.ntgw * a.njbw;
+    if (units > 0xffffffffull - 3)
+        return hipErrorInvalidValue;
+    a.units = (uint32_t)units;
+    a.vec = (sh.Co % 8 == 0 && (reinterpret_cast<uintptr_t>(filt) & 15) == 0) ? 1u : 0u;
+    a.div_khci = make_fastdiv((uint32_t)(sh.Kh * sh.Ci));
+    a.div_ci = make_fastdiv((uint32_t)sh.Ci);
+    a.div_tb = make_fastdiv(a.tb);
+    const uint64_t blocks = (units + 3) / 4;
     void *args[] = {&a};
     return hipLaunchKernel((const void *)&pack_filter_fp16, dim3((uint32_t)blocks), dim3(256), args, 0, st);
 }
