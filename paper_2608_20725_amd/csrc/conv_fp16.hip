@@ -76,9 +76,9 @@ struct C16Args {
 // time (8 channels), the 8 lanes of a tap reading one 128-byte run of C_o,
 // transposes the block in registers, and writes 8 granules (one per
 // channel), the 8 lanes of a channel block writing one run of packed row.
-// Filters whose rows are not whole 16-byte pieces (C_o % 8, or a base not
-// 16-byte aligned) are read element by element.  TB and tpad are multiples
-// of 64, so a block never straddles a tile.
+// Filters whose rows are not whole 16-byte pieces (C_o % 8; the entry points
+// take only 16-byte aligned bases) are read element by element.  TB and tpad
+// are multiples of 64, so a block never straddles a tile.
 struct PackArgs {
     const uint16_t *filt;
     uint16_t *packed;
@@ -86,7 +86,7 @@ struct PackArgs {
     uint32_t ntg, njb;    // 8-tap groups per slice (tpad/8), 8-channel blocks (Co_pad/8)
     uint32_t ntgw, njbw;  // waves along tap groups and channel blocks (8 of each per wave)
     uint32_t units;       // nv * ntgw * njbw waves
-    uint32_t vec;         // rows are whole aligned 16-byte pieces
+    uint32_t vec;         // rows are whole 16-byte pieces (C_o % 8 == 0)
     FastDiv div_khci, div_ci, div_tb;
 };
 
@@ -923,7 +923,7 @@ hipError_t launch_pack_fp16(const Shape &sh, const Plan16 &p, const uint16_t *fi
     if (units > 0xffffffffull - 3)
         return hipErrorInvalidValue;
     a.units = (uint32_t)units;
-    a.vec = (sh.Co % 8 == 0 && (reinterpret_cast<uintptr_t>(filt) & 15) == 0) ? 1u : 0u;
+    a.vec = sh.Co % 8 == 0 ? 1u : 0u;
     a.div_khci = make_fastdiv((uint32_t)(sh.Kh * sh.Ci));
     a.div_ci = make_fastdiv((uint32_t)sh.Ci);
     a.div_tb = make_fastdiv(a.tb);
