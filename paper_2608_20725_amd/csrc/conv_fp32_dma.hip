@@ -447,7 +447,14 @@ const DVariant *d_variants(int *n)
     // about 3 % of the 256-pixel tile either way (1x1 C=1024: 84.9 and 85.6
     // vs 83.1; 112x112 C_o=128: 90.3 and 88.9 vs 90.8), inside run-to-run
     // spread, so the default stays; a tap-major inner loop that reads every
-    // operand a tap ahead measured no faster.
+    // operand a tap ahead measured no faster.  The 32-pixel tap-split tile
+    // doubled to 64 pixels with eight waves (two pixel groups, same sums in
+    // the same order) runs four waves per SIMD instead of two: 3x3 C=512 at
+    // 14x14 91.9 vs 86.0, 3x3 C=128 at 28x28 85.8 vs 80.9, 5x5 C_o=256 at
+    // 24x24 88.9 vs 86.1, 3x3 C=256 at 12x12 and 14x14 +1 %; on 3x3 C=512 at
+    // 7x7 (104 tiles) the 64-pixel four-wave tile stays ahead (74.0 vs
+    // 73.3), and an eight-wave 128-pixel tile or a two-way split of eight
+    // waves measured lower.
     static const DVariant v[] = {
         d_variant<8, 8, 8, 1, 2, 16>("p8c8l8s2k16"),
         d_variant<6, 8, 8, 1, 2, 16>("p6c8l8s2k16"),
@@ -464,10 +471,13 @@ const DVariant *d_variants(int *n)
         d_variant<4, 8, 8, 1, 2, 16, 4>("p4c8l8s2k16g4"),
         d_variant<8, 8, 8, 1, 2, 16, 16, 4>("p8c8l8s2k16t4"),
         d_variant<4, 8, 8, 1, 2, 16, 16, 4>("p4c8l8s2k16t4"),
+        // eight waves: two 32-pixel groups, each splitting the taps four ways
+        d_variant<4, 8, 8, 1, 2, 16, 16, 4, 8>("p4c8l8s2k16t4w8"),
         // serialized rings of three of the above (check variants)
         d_variant<8, 8, 8, 1, 2, 16, 16, 1, 4, true>("p8c8l8s2k16-serial"),
         d_variant<6, 8, 8, 1, 2, 16, 4, 1, 4, true>("p6c8l8s2k16g4-serial"),
         d_variant<4, 8, 8, 1, 2, 16, 16, 4, 4, true>("p4c8l8s2k16t4-serial"),
+        d_variant<4, 8, 8, 1, 2, 16, 16, 4, 8, true>("p4c8l8s2k16t4w8-serial"),
     };
     *n = (int)(sizeof v / sizeof v[0]);
     return v;
@@ -518,7 +528,7 @@ int dma32_default(const Shape &sh)
     const bool strided = sh.s > 1 && sh.Kw > sh.s;
     const char *name = !aligned          ? "p6c8l8s2k16g4"
                        : tiles256 <= 128  ? "p8c8l8s2k16t4"
-                       : tiles256 <= 1024 ? "p4c8l8s2k16t4"
+                       : tiles256 <= 1024 ? "p4c8l8s2k16t4w8"
                        : strided          ? "p6c8l8s2k16"
                                           : "p8c8l8s2k16";
     // 96-channel tiles where they pad fewer channels than 64-channel ones

@@ -224,8 +224,8 @@ VARIANT_CASES = [
      True),
     # taps split over the waves: another summation order, K = 144 ragged in
     # 64-tap stages
-    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16t4", "p4c8l8s2k16t4"], (2, 16, 17, 19, 100, 3, 3, 1), torch.float32,
-     True),
+    ("IM2WIN_FP32_KERNEL", ["p8c8l8s2k16t4", "p4c8l8s2k16t4", "p4c8l8s2k16t4w8"], (2, 16, 17, 19, 100, 3, 3, 1),
+     torch.float32, True),
     ("IM2WIN_FP16_SEG", ["s64p256", "s96p128", "s128p128"], (2, 6, 13, 90, 200, 3, 5, 1), torch.float16,
      True),
 ]
@@ -268,6 +268,7 @@ SERIAL_CASES = [
     ("IM2WIN_FP32_KERNEL", "p8c8l8s2k16", (8, 64, 56, 56, 64, 3, 3, 1), torch.float32),
     ("IM2WIN_FP32_KERNEL", "p6c8l8s2k16g4", (8, 3, 100, 100, 64, 7, 7, 2), torch.float32),
     ("IM2WIN_FP32_KERNEL", "p4c8l8s2k16t4", (16, 256, 14, 14, 256, 3, 3, 1), torch.float32),
+    ("IM2WIN_FP32_KERNEL", "p4c8l8s2k16t4w8", (16, 256, 14, 14, 256, 3, 3, 1), torch.float32),
 ]
 
 
@@ -371,6 +372,7 @@ ORDER_CASES = [
     # (forced variables, shape, dtype, matrix-core fp32)
     ({}, (2, 16, 17, 19, 300, 3, 3, 1), torch.float32, False),
     ({"IM2WIN_FP32_KERNEL": "p4c8l8s2k16t4"}, (2, 16, 17, 19, 300, 3, 3, 1), torch.float32, False),
+    ({"IM2WIN_FP32_KERNEL": "p4c8l8s2k16t4w8"}, (2, 16, 17, 19, 300, 3, 3, 1), torch.float32, False),
     ({}, (1, 8, 6, 6, 200, 3, 3, 1), torch.float32, False),
     ({}, (2, 64, 24, 24, 300, 3, 3, 1), torch.float32, True),
     ({}, (1, 8, 6, 6, 200, 3, 3, 1), torch.float32, True),

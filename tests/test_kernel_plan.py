@@ -244,6 +244,7 @@ def test_stem32_default(shape, want):
     ((128, 64, 112, 112, 128, 3, 3, 1), "conv_fp32_dma p8c8l8s2k16"),   # stride 1
     ((128, 64, 224, 224, 64, 2, 2, 2), "conv_fp32_dma p8c8l8s2k16"),    # K_w = s: no overlap
     ((2, 16, 23, 41, 40, 7, 7, 2), "conv_fp32_dma p8c8l8s2k16t4"),      # few tiles
+    ((128, 512, 14, 14, 512, 3, 3, 1), "conv_fp32_dma p4c8l8s2k16t4w8"),  # 576 tiles: the eight-wave tap split
 ])
 def test_dma32_default(shape, want):
     assert name(shape, "f32") == want
