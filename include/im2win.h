@@ -63,7 +63,8 @@
  * IM2WIN_TRANSFORM_ORDER and IM2WIN_TILE_ORDER (xcd | linear),
  * IM2WIN_TRANSFORM_KERNEL (pieces | gather: the 3-channel transform),
  * IM2WIN_FP16_PERSIST (on | off: the column-staged kernel's persistent launch),
- * IM2WIN_TAP_ORDER (linear | column), IM2WIN_FP16_SPLIT (1..8: the K range
+ * IM2WIN_TAP_ORDER (linear | column: the filter columns' tap slices in turn,
+ * the columns grouped by residue mod the stride), IM2WIN_FP16_SPLIT (1..8: the K range
  * of the row-per-pixel fp16 kernel split over that many workgroups per output
  * tile, their fp32 partial tiles added afterwards in a fixed order; a split
  * the default plan does not make needs ks * tiles * 64 KiB of workspace beyond
