@@ -612,8 +612,19 @@ __global__ __launch_bounds__(256) void split_sum(SumArgs a)
     }
 }
 
+// Workgroups per CU the compiler is to leave registers for: the one-slot
+// four-wave tile (32 KiB of LDS) fits in 128 registers, four workgroups per
+// CU, without spilling (72 + 64 accumulation registers unhinted, three per
+// CU): 1x1 C=1024 at 14x14, 767 against 700 TFLOP/s.  The other tiles are
+// held to fewer workgroups by their LDS.
+template <int NW, int NSTAGE>
+constexpr int pipe_min_blocks()
+{
+    return NW == 4 && NSTAGE == 1 ? 4 : 1;
+}
+
 template <class E, int WM, int WN, int WGM, int WGN, int NSTAGE>
-__global__ __launch_bounds__(64 * WGM * WGN) void conv_fp16_pipe(C16Args a)
+__global__ __launch_bounds__(64 * WGM * WGN, (pipe_min_blocks<WGM * WGN, NSTAGE>())) void conv_fp16_pipe(C16Args a)
 {
     using C = PipeCfg<WM, WN, WGM, WGN, NSTAGE>;
     static_assert(NSTAGE >= 1 && NSTAGE <= 4, "ring depth");
